@@ -1,0 +1,220 @@
+"""Benchmark of the kNN-LM mixture step on one MI355X.
+
+A step is one knn_lm_mixture call (distances -> top-r -> softmax / scatter /
+lambda-mix) over one batch of queries whose inputs already sit in HBM.  The
+default workload is the Llama-2-7B-shaped decode query: B = 1, d = 4096,
+N = 65536 bf16 keys (64 passages x 1024 tokens), r = 1024, V = 32000.  Two key
+buffers of that shape alternate between steps so the 256 MB last-level cache
+cannot serve a repeated key stream.
+
+Prints one JSON line.  The dominant kernel (the distance stage) is timed with
+HIP events around its launches inside the timed region, on the stream the
+library launches on.  The CPU baseline is the fp64 oracle on a bounded sample
+of the same workload on this host's cores.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0  # MI355X HBM3E, published
+PMC_FILE = os.path.join(ROOT, "profiles", "dist_kernel_decode_7b_pmc.json")
+
+
+def _args():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=1000)
+    ap.add_argument("--warmup", type=int, default=100)
+    ap.add_argument("--workload", default="decode_7b")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle sample")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="after the timed region, run a plain 512 MiB device copy (HBM counter calibration)")
+    return ap.parse_args()
+
+
+def dist_kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in ("dist_kernels.hip", "knnlm_device.h", "knnlm_internal.h"):
+        h.update(open(os.path.join(ROOT, "paper_2405_19325_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per distance launch from committed rocprofv3 counters, if they match this kernel source."""
+    try:
+        rec = json.load(open(PMC_FILE))
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_source_hash") != dist_kernel_source_hash():
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def main():
+    a = _args()
+    if a.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {a.gpus} is not supported by this build "
+              "(the kNN-LM step has no cross-GPU path here).", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2405_19325_amd as knn
+    from workloads import gen
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    spec = gen.config(a.workload)
+    seed = gen.CONFIG_SEEDS[a.workload]
+    w = gen.make(spec, seed, device=dev)
+    keys2 = gen.second_key_copy(spec, seed, device=dev)
+    hints = dict(key_offsets_host=w.key_offsets_host, query_offsets_host=w.query_offsets_host)
+    probs = [knn.MixtureProblem(w.queries, k, w.values, w.key_offsets, w.query_offsets, w.p_lm, w.r, w.mu, w.lam,
+                                **hints) for k in (w.keys, keys2)]
+    torch.cuda.synchronize()
+
+    B = spec.B
+    total_keys = int(w.key_offsets_host[-1])
+    esize = w.keys.element_size()
+    # per-query key rows read: each query's own set (sets with several queries are read once)
+    key_bytes = total_keys * spec.d * esize
+    q_bytes = B * spec.d * esize
+    dist_alg_bytes = key_bytes + q_bytes
+    step_alg_bytes = dist_alg_bytes + 2 * B * spec.V * 4 + B * w.r * 4  # + p_LM in, p_M out, values gathered
+
+    for i in range(a.warmup):
+        probs[i % 2].run()
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(a.steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    start.record(stream)
+    for i in range(a.steps):
+        p = probs[i % 2]
+        ev[i][0].record(stream)
+        p.run_part("distances")
+        ev[i][1].record(stream)
+        p.run_part("select")
+        ev[i][2].record(stream)
+        p.run_part("mix")
+    end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    elapsed_ms = start.elapsed_time(end)
+    dist_ms = [e[0].elapsed_time(e[1]) for e in ev]
+    topr_ms = [e[0].elapsed_time(e[2]) for e in ev]
+    avg_dist_ms = sum(dist_ms) / len(dist_ms)
+    avg_topr_ms = sum(topr_ms) / len(topr_ms)
+    ms_per_step = elapsed_ms / a.steps
+    qps = B * a.steps / (elapsed_ms / 1e3)
+
+    achieved = dist_alg_bytes / (avg_dist_ms / 1e3) / 1e9
+    traffic = measured_traffic()
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
+                "kernel": "distance stage (k_dist_vec)", "alg_bytes_per_launch": dist_alg_bytes,
+                "avg_launch_ms": round(avg_dist_ms, 5)}
+
+    if a.copy_calibration:
+        src = torch.empty(256 * 1024 * 1024, dtype=torch.bfloat16, device=dev)  # 512 MiB
+        src.fill_(1.0)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+
+    cpu = None
+    if not a.no_cpu_baseline:
+        cpu = cpu_baseline(w, spec, seed, a.cpu_seconds)
+
+    line = {
+        "metric": "kNN-LM mixture queries/s + achieved HBM GB/s (d=4096, N=64K keys, r=1024)",
+        "value": round(qps, 1),
+        "unit": "queries/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1)*8/sqrt(d) keys and queries, Zipf(1.1) values, softmax N(0,2) p_LM)",
+        "config": {
+            "workload": (f"{spec.name}: B={B} queries, d={spec.d}, {spec.S} key set(s), N={total_keys} "
+                         f"{spec.dtype} keys, r={spec.r}, V={spec.V}, mu={spec.mu:.6g}, lambda={spec.lam}"),
+            "global_batch": B,
+            "keys_per_query": total_keys // max(1, spec.S),
+            "hidden": spec.d,
+            "r": spec.r,
+            "parallelism": "single GPU",
+            "key_buffers_rotated": 2,
+        },
+        "distance_topr_ms": round(avg_topr_ms, 5),
+        "distance_topr_hbm_frac": round(dist_alg_bytes / (avg_topr_ms / 1e3) / 1e9 / PEAK_HBM_GBS, 4),
+        "step_alg_bytes": step_alg_bytes,
+        "step_hbm_frac": round(step_alg_bytes / (ms_per_step / 1e3) / 1e9 / PEAK_HBM_GBS, 4),
+        "host_wall_s": round(wall, 3),
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+def cpu_baseline(w, spec, seed, budget_s):
+    """The fp64 oracle on a bounded sample: further decode queries against the same key set."""
+    import numpy as np
+
+    import oracle
+    from workloads import gen
+
+    threads = min(16, len(os.sched_getaffinity(0)))
+    n0 = int(w.key_offsets_host[1])  # the sample queries the first key set
+    keys_h, dt = oracle.host_elements(w.keys[:n0])
+    vals = w.values[:n0].cpu().numpy()
+    ko, qo1 = np.array([0, n0], dtype=np.int64), np.array([0, 1], dtype=np.int64)
+    extra = gen.extra_queries(spec, seed, 64, device="cpu")
+    q_all, _ = oracle.host_elements(extra)
+    p_lm = w.p_lm[:1].cpu().numpy()
+    done = 0
+    t0 = time.perf_counter()
+    while done < q_all.shape[0]:
+        q1 = q_all[done:done + 1]
+        ids, dists = oracle.select(q1, keys_h, dt, ko, qo1, spec.r, nthreads=threads)
+        oracle.mix(ids, dists, vals, ko, qo1, p_lm, spec.mu, spec.lam)
+        done += 1
+        if time.perf_counter() - t0 > budget_s:
+            break
+    el = time.perf_counter() - t0
+    return {"value": round(done / el, 3), "unit": "queries/s", "cores": threads, "kind": "oracle",
+            "sample": (f"{done} decode queries of the same shape (d={spec.d}, one set of {n0} keys, "
+                       f"r={spec.r}) through the fp64 oracle select + mix, {el:.1f} s wall, {threads} threads; "
+                       f"CPU: {_cpu_model()}")}
+
+
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,195 @@
+/*
+ * knnlm.h -- C ABI of the MI355X (gfx950) kNN-LM mixture step.
+ *
+ * The operation (paper "Nearest Neighbor Speculative Decoding", Section 2.2,
+ * paragraph "Probability interpolation", eq. non-parametric and eq. kNN-LM;
+ * Section 3.1 "Second-stage kNN token search"; Appendix A): for every decoding
+ * query q_t and the key/value store (K', V') built from that sequence's
+ * retrieved passages,
+ *
+ *   s(q, k)  = -||q - k||^2                        (negative squared L2 distance)
+ *   pi       = the r keys with the largest s       (ties: lower key index first)
+ *   p_kNN(w) = sum_{(k_i, v_i) in pi, v_i = w} exp(mu s(q, k_i)) / sum_{pi} exp(mu s)
+ *   p_M(w)   = lambda p_LM(w) + (1 - lambda) p_kNN(w)
+ *
+ * Data model.  B queries are grouped into S key sets.  Set s owns the query
+ * rows query_offsets[s] .. query_offsets[s+1]-1 and the key rows (and values)
+ * key_offsets[s] .. key_offsets[s+1]-1; neighbour ids are LOCAL row indices
+ * within the query's own set.  Every matrix is row-major and dense.  Queries
+ * carry the key element type (round fp32 queries to it before the call).
+ *
+ * Memory.  Unless a parameter says "host", every pointer is a DEVICE pointer
+ * (hipMalloc'd or torch CUDA storage) on the current device.  The caller owns
+ * every buffer; the library allocates and frees nothing.  Scratch space comes
+ * from the caller's `workspace`, sized by knn_lm_mixture_workspace_size().
+ *
+ * Streams.  `stream` is a hipStream_t (NULL = the default stream).  Calls only
+ * validate on the host and enqueue work; they never synchronise.  Outputs are
+ * valid once the stream reaches that point.  A launch failure returns
+ * KNN_ERR_HIP; a device fault surfaces at the caller's next synchronisation.
+ *
+ * Errors.  No call prints, throws or aborts.  Argument errors are detected on
+ * the host before anything is enqueued and leave every output untouched.
+ *
+ * Preconditions the library does not check on the device: finite query and
+ * key elements, values in [0, V), offsets monotone with key_offsets[0] = 0 and
+ * query_offsets[0] = 0, and planning hints that are true.  If a hint is false
+ * the results are unspecified, but every device access stays inside the
+ * buffers the hints describe.
+ *
+ * Thread safety.  Stateless and re-entrant; concurrent calls need distinct
+ * workspaces.
+ */
+#ifndef KNNLM_H
+#define KNNLM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define KNNLM_ABI_VERSION 1
+
+/* Largest r accepted (the paper retrieves r = 1024, Appendix A). */
+#define KNNLM_MAX_R 4096
+
+typedef enum {
+    KNN_OK = 0,
+    KNN_ERR_INVALID_ARG = 1,  /* null pointer, bad size, mu/lambda out of range, bad hint */
+    KNN_ERR_R_EXCEEDS_N = 2,  /* r larger than the smallest key set (min_keys_per_set) */
+    KNN_ERR_UNSUPPORTED = 3,  /* valid request this build does not serve (r > KNNLM_MAX_R, ...) */
+    KNN_ERR_WORKSPACE = 4,    /* workspace NULL or smaller than knn_lm_mixture_workspace_size() */
+    KNN_ERR_HIP = 5           /* a HIP launch failed */
+} knn_status;
+
+/* Element type of queries and keys. */
+typedef enum { KNN_F32 = 0, KNN_BF16 = 1, KNN_F16 = 2 } knn_dtype;
+
+/* Stages of knn_lm_mixture, runnable one at a time by knn_lm_mixture_part(). */
+typedef enum {
+    KNN_PART_DISTANCES = 1, /* squared distances of every query to its set (into the workspace) */
+    KNN_PART_SELECT = 2,    /* top-r per query: nbr_ids, nbr_dists */
+    KNN_PART_MIX = 3        /* softmax over mu*s, scatter onto values, lambda-mix: p_m */
+} knn_part;
+
+/*
+ * knn_lm_mixture -- the whole step (eq. non-parametric, then eq. kNN-LM).
+ *
+ *   queries        [B, d] dtype.
+ *   keys           [total_keys, d] dtype; set s = rows key_offsets[s]..key_offsets[s+1]-1.
+ *   key_sqnorms    [total_keys] fp32 ||k||^2 from knn_key_sqnorms(), or NULL to
+ *                  compute them on the fly (no extra bytes read).
+ *   values         [total_keys] int32 next-token id of each key, in [0, V).
+ *   key_offsets    [S+1] int64, monotone, key_offsets[0] = 0, key_offsets[S] = total_keys.
+ *   query_offsets  [S+1] int64, monotone, query_offsets[0] = 0, query_offsets[S] = B.
+ *   p_lm           [B, V] fp32 LM next-token distribution.
+ *   B, d, V, S     sizes (all >= 1).
+ *   total_keys     number of key rows.
+ *   min_keys_per_set, max_keys_per_set, max_queries_per_set
+ *                  host planning hints: the smallest key set among sets that
+ *                  own at least one query, the largest key set, and the
+ *                  largest number of queries owned by one set (<= 65535).
+ *   dtype          element type of queries and keys.
+ *   r              neighbours per query, 1 <= r <= min(KNNLM_MAX_R, min_keys_per_set).
+ *   mu             inverse temperature > 0 (the paper uses 1/sqrt(d)).
+ *   lambda         weight of p_LM, in [0, 1] (lambda = 1 returns p_LM bit for bit).
+ *   p_m            [B, V] fp32 out: the mixture.
+ *   nbr_ids        [B, r] int32 out: local key ids of pi, ascending (distance, id).
+ *   nbr_dists      [B, r] fp32 out: their squared L2 distances (>= 0), = -s.
+ *   workspace      device scratch of at least knn_lm_mixture_workspace_size() bytes,
+ *                  256-byte aligned; contents on entry are ignored.
+ */
+knn_status knn_lm_mixture(const void *queries, const void *keys, const float *key_sqnorms,
+                          const int32_t *values, const int64_t *key_offsets,
+                          const int64_t *query_offsets, const float *p_lm, int64_t B, int64_t d,
+                          int64_t V, int64_t S, int64_t total_keys, int64_t min_keys_per_set,
+                          int64_t max_keys_per_set, int64_t max_queries_per_set, knn_dtype dtype,
+                          int32_t r, float mu, float lambda, float *p_m, int32_t *nbr_ids,
+                          float *nbr_dists, void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * knn_lm_mixture_part -- one stage of knn_lm_mixture with the same arguments.
+ * Calling KNN_PART_DISTANCES, KNN_PART_SELECT, KNN_PART_MIX in that order on
+ * one stream with one workspace is exactly knn_lm_mixture.  Pointers a stage
+ * does not use may be NULL (DISTANCES: values, p_lm, p_m, nbr_ids, nbr_dists;
+ * SELECT: queries, keys, key_sqnorms, values, p_lm, p_m; MIX: queries, keys,
+ * key_sqnorms, workspace).
+ */
+knn_status knn_lm_mixture_part(knn_part part, const void *queries, const void *keys,
+                               const float *key_sqnorms, const int32_t *values,
+                               const int64_t *key_offsets, const int64_t *query_offsets,
+                               const float *p_lm, int64_t B, int64_t d, int64_t V, int64_t S,
+                               int64_t total_keys, int64_t min_keys_per_set,
+                               int64_t max_keys_per_set, int64_t max_queries_per_set,
+                               knn_dtype dtype, int32_t r, float mu, float lambda, float *p_m,
+                               int32_t *nbr_ids, float *nbr_dists, void *workspace,
+                               size_t workspace_bytes, void *stream);
+
+/* Bytes of workspace knn_lm_mixture needs for these sizes (0 if they are invalid). */
+size_t knn_lm_mixture_workspace_size(int64_t B, int64_t d, int64_t V, int64_t S,
+                                     int64_t total_keys, int64_t min_keys_per_set,
+                                     int64_t max_keys_per_set, int64_t max_queries_per_set,
+                                     knn_dtype dtype, int32_t r);
+
+/*
+ * knn_lm_mixture_validate -- the host-side argument checks of knn_lm_mixture,
+ * without enqueuing anything.  Pointers are only tested for NULL, never
+ * dereferenced, so it runs without a GPU.
+ */
+knn_status knn_lm_mixture_validate(const void *queries, const void *keys, const int32_t *values,
+                                   const int64_t *key_offsets, const int64_t *query_offsets,
+                                   const float *p_lm, int64_t B, int64_t d, int64_t V, int64_t S,
+                                   int64_t total_keys, int64_t min_keys_per_set,
+                                   int64_t max_keys_per_set, int64_t max_queries_per_set,
+                                   knn_dtype dtype, int32_t r, float mu, float lambda,
+                                   const float *p_m, const int32_t *nbr_ids,
+                                   const float *nbr_dists, const void *workspace,
+                                   size_t workspace_bytes);
+
+/*
+ * knn_distances -- the distance stage alone, written to a caller matrix
+ * (s(q,k) = -||q-k||^2, paper Section 2.2): out[b * ld_out + i] = ||q_b - k_i||^2
+ * (fp32, >= 0) for i < N of b's set, via ||q||^2 - 2 q.k + ||k||^2 with fp32
+ * accumulation.  Entries i >= N of a row are not written.  Requires
+ * ld_out >= max_keys_per_set.  key_sqnorms may be NULL.
+ */
+knn_status knn_distances(const void *queries, const void *keys, const float *key_sqnorms,
+                         const int64_t *key_offsets, const int64_t *query_offsets, int64_t B,
+                         int64_t d, int64_t S, int64_t max_keys_per_set,
+                         int64_t max_queries_per_set, knn_dtype dtype, float *out, int64_t ld_out,
+                         void *stream);
+
+/*
+ * knn_key_sqnorms -- ||k_i||^2 in fp32 for n rows of d elements.  The key store
+ * is built once per input before decoding starts (paper Algorithm 1), so these
+ * can be computed once per store and passed to every later call.  The
+ * summation order equals the one knn_lm_mixture uses on the fly, so a query
+ * equal to a key gets distance exactly 0 either way.
+ */
+knn_status knn_key_sqnorms(const void *keys, int64_t n, int64_t d, knn_dtype dtype, float *out,
+                           void *stream);
+
+/*
+ * knn_mix -- the softmax / scatter / mixture stage alone (eq. non-parametric
+ * and eq. kNN-LM) on caller-given neighbours: for each query b of set s, the
+ * r entries (nbr_ids[b, j], nbr_dists[b, j]) in any order; ids outside
+ * [0, N_s) and values outside [0, V) are skipped.  p_m [B, V] is written.
+ */
+knn_status knn_mix(const int32_t *nbr_ids, const float *nbr_dists, const int32_t *values,
+                   const int64_t *key_offsets, const int64_t *query_offsets, const float *p_lm,
+                   int64_t B, int64_t V, int64_t S, int32_t r, float mu, float lambda, float *p_m,
+                   void *stream);
+
+/* Static text for a status code. */
+const char *knn_status_string(knn_status status);
+
+/* KNNLM_ABI_VERSION of the loaded library. */
+int knn_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KNNLM_H */

@@ -1,0 +1,178 @@
+"""MI355X-native kNN-LM mixture step (Nearest Neighbor Speculative Decoding, Section 2.2).
+
+The Python surface mirrors the C ABI in include/knnlm.h and only marshals
+arguments: device tensors are passed as raw pointers together with the
+current torch stream.  All arithmetic runs in the HIP kernels of libknnlm.so.
+
+    prob = MixtureProblem(queries, keys, values, key_offsets, query_offsets, p_lm, r, mu, lam)
+    p_m, ids, dists = prob.run()
+"""
+from __future__ import annotations
+
+import math
+from typing import Optional, Sequence
+
+import numpy as np
+import torch
+
+from . import _lib
+from ._lib import DTYPES, PARTS, KnnError, load, status_string  # noqa: F401
+
+__all__ = ["MixtureProblem", "mixture", "distances", "key_sqnorms", "mix", "workspace_size", "KnnError",
+           "load", "status_string", "abi_version"]
+
+_TORCH_DTYPES = {torch.float32: "f32", torch.bfloat16: "bf16", torch.float16: "f16"}
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream=None):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else stream
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    try:
+        return DTYPES[_TORCH_DTYPES[t.dtype]]
+    except KeyError:
+        raise TypeError(f"unsupported element type {t.dtype}") from None
+
+
+def _need(cond: bool, msg: str):
+    if not cond:
+        raise ValueError(msg)
+
+
+def abi_version() -> int:
+    return load().knn_abi_version()
+
+
+def workspace_size(B, d, V, S, total_keys, min_keys, max_keys, max_queries, dtype: str, r) -> int:
+    return int(load().knn_lm_mixture_workspace_size(B, d, V, S, total_keys, min_keys, max_keys, max_queries,
+                                                    DTYPES[dtype], r))
+
+
+class MixtureProblem:
+    """Inputs, planning hints, workspace and outputs of repeated knn_lm_mixture calls.
+
+    queries [B, d], keys [total_keys, d] (same dtype: f32/bf16/f16), values
+    [total_keys] int32, key_offsets / query_offsets [S+1] int64, p_lm [B, V]
+    fp32, all on one GPU.  The host copies of the offsets (derived once here
+    unless given) provide the planning hints.
+    """
+
+    def __init__(self, queries: torch.Tensor, keys: torch.Tensor, values: torch.Tensor,
+                 key_offsets: torch.Tensor, query_offsets: torch.Tensor, p_lm: torch.Tensor, r: int,
+                 mu: Optional[float] = None, lam: float = 0.3, key_sqnorms: Optional[torch.Tensor] = None,
+                 key_offsets_host: Optional[Sequence[int]] = None,
+                 query_offsets_host: Optional[Sequence[int]] = None):
+        _need(queries.dim() == 2 and keys.dim() == 2, "queries and keys must be 2-D")
+        _need(queries.dtype == keys.dtype, "queries must carry the key element type")
+        _need(queries.shape[1] == keys.shape[1], "queries and keys must have the same width")
+        for name, t in (("queries", queries), ("keys", keys), ("values", values), ("p_lm", p_lm),
+                        ("key_offsets", key_offsets), ("query_offsets", query_offsets)):
+            _need(t.is_cuda, f"{name} must be a device tensor")
+            _need(t.is_contiguous(), f"{name} must be contiguous")
+        _need(values.dtype == torch.int32 and p_lm.dtype == torch.float32, "values int32, p_lm float32")
+        _need(key_offsets.dtype == torch.int64 and query_offsets.dtype == torch.int64, "offsets must be int64")
+        ko = np.asarray(key_offsets_host if key_offsets_host is not None else key_offsets.cpu().numpy(), np.int64)
+        qo = np.asarray(query_offsets_host if query_offsets_host is not None else query_offsets.cpu().numpy(),
+                        np.int64)
+        _need(len(ko) == len(qo) and len(ko) >= 2, "offsets must have S+1 >= 2 entries")
+        nk = np.diff(ko)
+        nq = np.diff(qo)
+        self.queries, self.keys, self.values = queries, keys, values
+        self.key_offsets, self.query_offsets, self.p_lm = key_offsets, query_offsets, p_lm
+        self.key_sqnorms = key_sqnorms
+        self.B, self.d = int(queries.shape[0]), int(queries.shape[1])
+        self.V = int(p_lm.shape[1])
+        self.S = len(ko) - 1
+        self.total_keys = int(keys.shape[0])
+        self.min_keys = int(nk[nq > 0].min()) if (nq > 0).any() else 0
+        self.max_keys = int(nk.max())
+        self.max_queries = int(nq.max())
+        self.dtype = _dtype_code(queries)
+        self.r = int(r)
+        self.mu = float(1.0 / math.sqrt(self.d) if mu is None else mu)
+        self.lam = float(lam)
+        dev = queries.device
+        nbytes = load().knn_lm_mixture_workspace_size(self.B, self.d, self.V, self.S, self.total_keys,
+                                                      self.min_keys, self.max_keys, self.max_queries,
+                                                      self.dtype, self.r)
+        if nbytes == 0:
+            _lib.check("knn_lm_mixture_workspace_size", self._validate(None, 0))
+        self.workspace = torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=dev)
+        self.p_m = torch.empty((self.B, self.V), dtype=torch.float32, device=dev)
+        self.ids = torch.empty((self.B, self.r), dtype=torch.int32, device=dev)
+        self.dists = torch.empty((self.B, self.r), dtype=torch.float32, device=dev)
+
+    def _args(self, stream):
+        return (_ptr(self.queries), _ptr(self.keys), _ptr(self.key_sqnorms), _ptr(self.values),
+                _ptr(self.key_offsets), _ptr(self.query_offsets), _ptr(self.p_lm), self.B, self.d, self.V, self.S,
+                self.total_keys, self.min_keys, self.max_keys, self.max_queries, self.dtype, self.r, self.mu,
+                self.lam, _ptr(self.p_m), _ptr(self.ids), _ptr(self.dists), _ptr(self.workspace),
+                self.workspace.numel(), _stream(stream))
+
+    def _validate(self, ws, ws_bytes):
+        return load().knn_lm_mixture_validate(
+            _ptr(self.queries), _ptr(self.keys), _ptr(self.values), _ptr(self.key_offsets), _ptr(self.query_offsets),
+            _ptr(self.p_lm), self.B, self.d, self.V, self.S, self.total_keys, self.min_keys, self.max_keys,
+            self.max_queries, self.dtype, self.r, self.mu, self.lam, 1, 1, 1, ws, ws_bytes)
+
+    def run(self, stream=None):
+        """One knn_lm_mixture call; returns (p_m, nbr_ids, nbr_dists), valid after stream sync."""
+        _lib.check("knn_lm_mixture", load().knn_lm_mixture(*self._args(stream)))
+        return self.p_m, self.ids, self.dists
+
+    def run_part(self, part: str, stream=None):
+        """One stage ("distances", "select", "mix") of knn_lm_mixture on this problem's workspace."""
+        _lib.check("knn_lm_mixture_part", load().knn_lm_mixture_part(PARTS[part], *self._args(stream)))
+
+
+def mixture(queries, keys, values, key_offsets, query_offsets, p_lm, r, mu=None, lam=0.3, key_sqnorms=None,
+            key_offsets_host=None, query_offsets_host=None):
+    """One-shot knn_lm_mixture: returns (p_m [B,V] fp32, ids [B,r] int32, dists [B,r] fp32)."""
+    prob = MixtureProblem(queries, keys, values, key_offsets, query_offsets, p_lm, r, mu, lam, key_sqnorms,
+                          key_offsets_host, query_offsets_host)
+    return prob.run()
+
+
+def distances(queries, keys, key_offsets, query_offsets, key_sqnorms=None, key_offsets_host=None,
+              query_offsets_host=None, ld: Optional[int] = None):
+    """knn_distances: squared distances [B, ld] of every query to its own set (entries past N_s untouched, NaN)."""
+    ko = np.asarray(key_offsets_host if key_offsets_host is not None else key_offsets.cpu().numpy(), np.int64)
+    qo = np.asarray(query_offsets_host if query_offsets_host is not None else query_offsets.cpu().numpy(), np.int64)
+    B, d = queries.shape
+    max_keys = int(np.diff(ko).max())
+    max_q = int(np.diff(qo).max())
+    ld = max_keys if ld is None else ld
+    out = torch.full((B, ld), float("nan"), dtype=torch.float32, device=queries.device)
+    st = load().knn_distances(_ptr(queries), _ptr(keys), _ptr(key_sqnorms), _ptr(key_offsets), _ptr(query_offsets),
+                              B, d, len(ko) - 1, max_keys, max_q, _dtype_code(queries), _ptr(out), ld, _stream(None))
+    _lib.check("knn_distances", st)
+    return out
+
+
+def key_sqnorms(keys: torch.Tensor) -> torch.Tensor:
+    """knn_key_sqnorms: ||k||^2 per row, fp32, with the summation order knn_lm_mixture uses."""
+    _need(keys.is_cuda and keys.is_contiguous() and keys.dim() == 2, "keys: contiguous 2-D device tensor")
+    out = torch.empty(keys.shape[0], dtype=torch.float32, device=keys.device)
+    st = load().knn_key_sqnorms(_ptr(keys), keys.shape[0], keys.shape[1], _dtype_code(keys), _ptr(out),
+                                _stream(None))
+    _lib.check("knn_key_sqnorms", st)
+    return out
+
+
+def mix(ids, dists, values, key_offsets, query_offsets, p_lm, mu, lam):
+    """knn_mix: p_M [B, V] from caller-given neighbours (ids local to each query's set, squared distances)."""
+    B, r = ids.shape
+    V = p_lm.shape[1]
+    S = key_offsets.numel() - 1
+    out = torch.empty((B, V), dtype=torch.float32, device=p_lm.device)
+    st = load().knn_mix(_ptr(ids), _ptr(dists), _ptr(values), _ptr(key_offsets), _ptr(query_offsets), _ptr(p_lm),
+                        B, V, S, r, float(mu), float(lam), _ptr(out), _stream(None))
+    _lib.check("knn_mix", st)
+    return out

@@ -1,0 +1,433 @@
+// Distance stage: d(q, k) = ||q||^2 - 2 q.k + ||k||^2 (fp32 accumulation), the
+// squared L2 distance whose negative is the similarity s(q, k) of the paper
+// (Section 2.2, sentence after eq. non-parametric; Appendix A).
+//
+// The work is HBM-bound for every batch size this kernel serves (one to eight
+// queries per key set): each key row is read from HBM exactly once and dotted
+// with every query of its set while it sits in registers.
+//
+// Numerics (shared by the on-the-fly norms here and knn_key_sqnorms): a row is
+// cut into 32-bit words (two bf16/f16 elements or one fp32 element) and
+// 16-byte chunks of four words; lane l of a wave accumulates chunks l, l+64,
+// l+128, ... word by word into one fp32 accumulator (v_dot2_f32_bf16 /
+// v_dot2_f32_f16 for 16-bit elements, FMA for fp32); the 64 lane partials are
+// then summed by a butterfly that leaves the same bits in every lane.
+// ||q||^2, ||k||^2 and q.k all use this order, so q == k gives exactly 0.
+#include "knnlm_device.h"
+#include "knnlm_internal.h"
+
+namespace knnlm {
+
+namespace {
+
+constexpr int kWavesPerDistBlock = kDistThreads / kWave;
+constexpr int kQueryRegChunks = 16;  // 16-byte query chunks a lane may hold in registers
+
+// ---------------------------------------------------------------- vector path
+
+// Per-set tile bounds shared by both distance kernels.  Returns false when the
+// workgroup has no work (uniform over the block).
+struct TileWork {
+    int64_t k0, r0, r1, qb;
+    int nq;
+};
+
+template <int NQ>
+__device__ __forceinline__ bool tile_work(const DistArgs &a, TileWork &t) {
+    const int64_t tiles = a.tiles_per_set;
+    const int64_t s = blockIdx.x / tiles;
+    const int64_t tile = blockIdx.x - s * tiles;
+    t.k0 = a.key_offsets[s];
+    int64_t N = a.key_offsets[s + 1] - t.k0;
+    if (N > a.ld) N = a.ld;
+    t.qb = a.query_offsets[s] + static_cast<int64_t>(blockIdx.y) * NQ;
+    const int64_t qe = a.query_offsets[s + 1];
+    t.r0 = tile * a.rows_per_tile;
+    if (t.qb >= qe || t.r0 >= N) return false;
+    t.nq = static_cast<int>(qe - t.qb < NQ ? qe - t.qb : NQ);
+    t.r1 = (t.r0 + a.rows_per_tile < N) ? t.r0 + a.rows_per_tile : N;
+    return true;
+}
+
+// Block-wide min/max of each query's distances over this tile, for the select stage.
+template <int NQ>
+__device__ __forceinline__ void write_tile_extrema(const DistArgs &a, const TileWork &t, const float (&mn)[NQ],
+                                                   const float (&mx)[NQ]) {
+    constexpr int NW = kWavesPerDistBlock;
+    __shared__ float smin[NW][NQ];
+    __shared__ float smax[NW][NQ];
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    if (lane == 0) {
+#pragma unroll
+        for (int j = 0; j < NQ; ++j) {
+            smin[wave][j] = mn[j];
+            smax[wave][j] = mx[j];
+        }
+    }
+    __syncthreads();
+    if (static_cast<int>(threadIdx.x) < t.nq) {
+        const int j = threadIdx.x;
+        float m = smin[0][j], M = smax[0][j];
+        for (int w = 1; w < NW; ++w) {
+            m = fminf(m, smin[w][j]);
+            M = fmaxf(M, smax[w][j]);
+        }
+        const int64_t tile = t.r0 / a.rows_per_tile;
+        a.tile_min[(t.qb + j) * a.tiles_per_set + tile] = m;
+        a.tile_max[(t.qb + j) * a.tiles_per_set + tile] = M;
+    }
+}
+
+// 16-byte loads: d % VEC == 0, 16-byte aligned rows, at most CPL chunks per lane.
+// Queries stay packed in registers (NQ x CPL chunks per lane); ROWS key rows per
+// wave are loaded before any of them is used.
+template <knn_dtype DT, int CPL, int NQ, int ROWS>
+__global__ __launch_bounds__(kDistThreads) void k_dist_vec(DistArgs a) {
+    constexpr int EB = Elem<DT>::BYTES;
+    constexpr int NW = kWavesPerDistBlock;
+    TileWork t;
+    if (!tile_work<NQ>(a, t)) return;
+
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    const int nchunks = static_cast<int>(a.d * EB / 16);
+    const int64_t row_bytes = a.d * EB;
+    const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
+
+    uint4 qv[NQ][CPL];
+#pragma unroll
+    for (int j = 0; j < NQ; ++j) {
+        const uint4 *qrow = reinterpret_cast<const uint4 *>(static_cast<const char *>(a.queries) + (t.qb + j) * row_bytes);
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) {
+            const int ch = lane + kWave * c;
+            qv[j][c] = (j < t.nq && ch < nchunks) ? qrow[ch] : zero;
+        }
+    }
+    float qq[NQ];
+#pragma unroll
+    for (int j = 0; j < NQ; ++j) {
+        float acc = 0.0f;
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) acc = dot_chunk<DT>(qv[j][c], qv[j][c], acc);
+        qq[j] = wave_allsum(acc);
+    }
+
+    float mn[NQ], mx[NQ];
+#pragma unroll
+    for (int j = 0; j < NQ; ++j) {
+        mn[j] = __builtin_huge_valf();
+        mx[j] = 0.0f;
+    }
+    const bool have_norms = a.key_sqnorms != nullptr;
+    const char *kset = static_cast<const char *>(a.keys) + t.k0 * row_bytes;
+
+    for (int64_t row = t.r0 + wave * ROWS; row < t.r1; row += NW * ROWS) {
+        uint4 kv[ROWS][CPL];
+#pragma unroll
+        for (int rr = 0; rr < ROWS; ++rr) {
+            const int64_t rw = row + rr;
+            const uint4 *krow = reinterpret_cast<const uint4 *>(kset + rw * row_bytes);
+#pragma unroll
+            for (int c = 0; c < CPL; ++c) {
+                const int ch = lane + kWave * c;
+                kv[rr][c] = (rw < t.r1 && ch < nchunks) ? krow[ch] : zero;
+            }
+        }
+#pragma unroll
+        for (int rr = 0; rr < ROWS; ++rr) {
+            const int64_t rw = row + rr;
+            float acc_k = 0.0f;
+            float acc_q[NQ];
+#pragma unroll
+            for (int j = 0; j < NQ; ++j) acc_q[j] = 0.0f;
+#pragma unroll
+            for (int c = 0; c < CPL; ++c) {
+                if (!have_norms) acc_k = dot_chunk<DT>(kv[rr][c], kv[rr][c], acc_k);
+#pragma unroll
+                for (int j = 0; j < NQ; ++j) acc_q[j] = dot_chunk<DT>(qv[j][c], kv[rr][c], acc_q[j]);
+            }
+            const float kk = have_norms ? ((rw < t.r1) ? a.key_sqnorms[t.k0 + rw] : 0.0f) : wave_allsum(acc_k);
+#pragma unroll
+            for (int j = 0; j < NQ; ++j) {
+                const float dot = wave_allsum(acc_q[j]);
+                const float dist = clamp_nonneg(fmaf(-2.0f, dot, qq[j] + kk));
+                if (rw < t.r1) {
+                    if (lane == j && j < t.nq) a.dist[(t.qb + j) * a.ld + rw] = dist;
+                    mn[j] = fminf(mn[j], dist);
+                    mx[j] = fmaxf(mx[j], dist);
+                }
+            }
+        }
+    }
+    if (a.tile_min != nullptr) write_tile_extrema<NQ>(a, t, mn, mx);
+}
+
+// --------------------------------------------------- element path (any d)
+
+// Same word/chunk layout and accumulation order as the vector path, with
+// element loads (elements past d read as 0): serves d that is not a multiple
+// of VEC, rows that are not 16-byte aligned and d above the vector path's
+// register budget.
+template <knn_dtype DT, int NQ>
+__global__ __launch_bounds__(kDistThreads) void k_dist_elem(DistArgs a) {
+    constexpr int EB = Elem<DT>::BYTES;
+    constexpr int PW = Elem<DT>::PER_WORD;
+    constexpr int NW = kWavesPerDistBlock;
+    TileWork t;
+    if (!tile_work<NQ>(a, t)) return;
+
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    const int64_t d = a.d;
+    const int64_t nwords = (d + PW - 1) / PW;
+    const int64_t nchunks = (nwords + 3) / 4;
+    const int64_t cpl = (nchunks + kWave - 1) / kWave;
+    const char *qbase = static_cast<const char *>(a.queries) + t.qb * d * EB;
+
+    float qq[NQ];
+#pragma unroll
+    for (int j = 0; j < NQ; ++j) {
+        float acc = 0.0f;
+        if (j < t.nq) {
+            const void *qrow = qbase + j * d * EB;
+            for (int64_t c = 0; c < cpl; ++c) {
+                const int64_t w0 = (lane + kWave * c) * 4;
+                for (int u = 0; u < 4; ++u) {
+                    const uint32_t w = load_word<DT>(qrow, w0 + u, d);
+                    acc = dot_word<DT>(w, w, acc);
+                }
+            }
+        }
+        qq[j] = wave_allsum(acc);
+    }
+
+    float mn[NQ], mx[NQ];
+#pragma unroll
+    for (int j = 0; j < NQ; ++j) {
+        mn[j] = __builtin_huge_valf();
+        mx[j] = 0.0f;
+    }
+    const bool have_norms = a.key_sqnorms != nullptr;
+    const char *kset = static_cast<const char *>(a.keys) + t.k0 * d * EB;
+
+    for (int64_t rw = t.r0 + wave; rw < t.r1; rw += NW) {
+        const void *krow = kset + rw * d * EB;
+        float acc_k = 0.0f;
+        float acc_q[NQ];
+#pragma unroll
+        for (int j = 0; j < NQ; ++j) acc_q[j] = 0.0f;
+        for (int64_t c = 0; c < cpl; ++c) {
+            const int64_t w0 = (lane + kWave * c) * 4;
+            for (int u = 0; u < 4; ++u) {
+                const uint32_t kw = load_word<DT>(krow, w0 + u, d);
+                if (!have_norms) acc_k = dot_word<DT>(kw, kw, acc_k);
+#pragma unroll
+                for (int j = 0; j < NQ; ++j) {
+                    const uint32_t qw = (j < t.nq) ? load_word<DT>(qbase + j * d * EB, w0 + u, d) : 0u;
+                    acc_q[j] = dot_word<DT>(qw, kw, acc_q[j]);
+                }
+            }
+        }
+        const float kk = have_norms ? a.key_sqnorms[t.k0 + rw] : wave_allsum(acc_k);
+#pragma unroll
+        for (int j = 0; j < NQ; ++j) {
+            const float dot = wave_allsum(acc_q[j]);
+            const float dist = clamp_nonneg(fmaf(-2.0f, dot, qq[j] + kk));
+            if (lane == j && j < t.nq) a.dist[(t.qb + j) * a.ld + rw] = dist;
+            mn[j] = fminf(mn[j], dist);
+            mx[j] = fmaxf(mx[j], dist);
+        }
+    }
+    if (a.tile_min != nullptr) write_tile_extrema<NQ>(a, t, mn, mx);
+}
+
+// ------------------------------------------------------------ key norms
+
+template <knn_dtype DT, int CPL>
+__global__ __launch_bounds__(kDistThreads) void k_sqnorm_vec(const void *keys, int64_t n, int64_t d, float *out) {
+    constexpr int EB = Elem<DT>::BYTES;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t wave_global = (static_cast<int64_t>(blockIdx.x) * kDistThreads + threadIdx.x) / kWave;
+    const int64_t nwaves = static_cast<int64_t>(gridDim.x) * (kDistThreads / kWave);
+    const int nchunks = static_cast<int>(d * EB / 16);
+    for (int64_t row = wave_global; row < n; row += nwaves) {
+        const uint4 *krow = reinterpret_cast<const uint4 *>(static_cast<const char *>(keys) + row * d * EB);
+        float acc = 0.0f;
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) {
+            const int ch = lane + kWave * c;
+            const uint4 v = (ch < nchunks) ? krow[ch] : make_uint4(0u, 0u, 0u, 0u);
+            acc = dot_chunk<DT>(v, v, acc);
+        }
+        acc = wave_allsum(acc);
+        if (lane == 0) out[row] = acc;
+    }
+}
+
+template <knn_dtype DT>
+__global__ __launch_bounds__(kDistThreads) void k_sqnorm_elem(const void *keys, int64_t n, int64_t d, float *out) {
+    constexpr int EB = Elem<DT>::BYTES;
+    constexpr int PW = Elem<DT>::PER_WORD;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t wave_global = (static_cast<int64_t>(blockIdx.x) * kDistThreads + threadIdx.x) / kWave;
+    const int64_t nwaves = static_cast<int64_t>(gridDim.x) * (kDistThreads / kWave);
+    const int64_t nwords = (d + PW - 1) / PW;
+    const int64_t nchunks = (nwords + 3) / 4;
+    const int64_t cpl = (nchunks + kWave - 1) / kWave;
+    for (int64_t row = wave_global; row < n; row += nwaves) {
+        const void *krow = static_cast<const char *>(keys) + row * d * EB;
+        float acc = 0.0f;
+        for (int64_t c = 0; c < cpl; ++c) {
+            const int64_t w0 = (lane + kWave * c) * 4;
+            for (int u = 0; u < 4; ++u) {
+                const uint32_t w = load_word<DT>(krow, w0 + u, d);
+                acc = dot_word<DT>(w, w, acc);
+            }
+        }
+        acc = wave_allsum(acc);
+        if (lane == 0) out[row] = acc;
+    }
+}
+
+// ------------------------------------------------------------ dispatch
+
+template <knn_dtype DT, int CPL, int NQ, int ROWS>
+hipError_t launch_vec(const DistArgs &a, dim3 grid, hipStream_t st) {
+    if constexpr (NQ * CPL <= kQueryRegChunks && ROWS * CPL <= kMaxCplVec) {
+        hipLaunchKernelGGL((k_dist_vec<DT, CPL, NQ, ROWS>), grid, dim3(kDistThreads), 0, st, a);
+        return hipGetLastError();
+    } else {
+        return hipErrorInvalidValue;
+    }
+}
+
+template <knn_dtype DT, int CPL, int NQ>
+hipError_t launch_vec_rows(int rows, const DistArgs &a, dim3 grid, hipStream_t st) {
+    return rows == 2 ? launch_vec<DT, CPL, NQ, 2>(a, grid, st) : launch_vec<DT, CPL, NQ, 1>(a, grid, st);
+}
+
+template <knn_dtype DT, int CPL>
+hipError_t launch_vec_nq(int nq, int rows, const DistArgs &a, dim3 grid, hipStream_t st) {
+    switch (nq) {
+    case 1: return launch_vec_rows<DT, CPL, 1>(rows, a, grid, st);
+    case 2: return launch_vec_rows<DT, CPL, 2>(rows, a, grid, st);
+    case 4: return launch_vec_rows<DT, CPL, 4>(rows, a, grid, st);
+    case 8: return launch_vec_rows<DT, CPL, 8>(rows, a, grid, st);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+template <knn_dtype DT>
+hipError_t launch_dist_dt(const DistPlan &p, const DistArgs &a, dim3 grid, hipStream_t st) {
+    if (!p.vec) {
+        switch (p.nq) {
+        case 1: hipLaunchKernelGGL((k_dist_elem<DT, 1>), grid, dim3(kDistThreads), 0, st, a); break;
+        case 2: hipLaunchKernelGGL((k_dist_elem<DT, 2>), grid, dim3(kDistThreads), 0, st, a); break;
+        case 4: hipLaunchKernelGGL((k_dist_elem<DT, 4>), grid, dim3(kDistThreads), 0, st, a); break;
+        case 8: hipLaunchKernelGGL((k_dist_elem<DT, 8>), grid, dim3(kDistThreads), 0, st, a); break;
+        default: return hipErrorInvalidValue;
+        }
+        return hipGetLastError();
+    }
+    switch (p.cpl) {
+    case 1: return launch_vec_nq<DT, 1>(p.nq, p.rows, a, grid, st);
+    case 2: return launch_vec_nq<DT, 2>(p.nq, p.rows, a, grid, st);
+    case 4: return launch_vec_nq<DT, 4>(p.nq, p.rows, a, grid, st);
+    case 8: return launch_vec_nq<DT, 8>(p.nq, p.rows, a, grid, st);
+    case 16: return launch_vec_nq<DT, 16>(p.nq, p.rows, a, grid, st);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+int pow2_at_least(int64_t x) {
+    int p = 1;
+    while (p < x) p <<= 1;
+    return p;
+}
+
+bool vector_path_ok(int64_t d, knn_dtype dtype, const void *queries, const void *keys) {
+    const int vec = vec_elems(dtype);
+    if (d % vec != 0) return false;
+    if ((d / vec + kWave - 1) / kWave > kMaxCplVec) return false;
+    if ((reinterpret_cast<uintptr_t>(queries) & 15u) || (reinterpret_cast<uintptr_t>(keys) & 15u)) return false;
+    return true;
+}
+
+}  // namespace
+
+DistPlan plan_distances(int64_t d, knn_dtype dtype, int64_t max_queries, const void *queries,
+                        const void *keys) {
+    DistPlan p{};
+    const int vec = vec_elems(dtype);
+    p.vec = vector_path_ok(d, dtype, queries, keys);
+    const int64_t mq = max_queries < 1 ? 1 : max_queries;
+    if (p.vec) {
+        p.cpl = pow2_at_least((d / vec + kWave - 1) / kWave);
+        int nq = 8;
+        while (nq > 1 && (nq * p.cpl > kQueryRegChunks || nq / 2 >= mq)) nq >>= 1;
+        p.nq = nq;
+        p.rows = (p.cpl <= kMaxCplVec / 2) ? 2 : 1;
+    } else {
+        p.cpl = 0;
+        int nq = 8;
+        while (nq > 1 && nq / 2 >= mq) nq >>= 1;
+        p.nq = nq;
+        p.rows = 1;
+    }
+    p.rows_per_tile = 0;  // set by the caller from the workspace layout
+    p.tiles_per_set = 0;
+    const int64_t groups = (mq + p.nq - 1) / p.nq;
+    p.groups = groups;
+    return p;
+}
+
+hipError_t launch_distances(const DistPlan &plan, knn_dtype dtype, const DistArgs &args, int64_t S,
+                            hipStream_t stream) {
+    const int64_t nblocks = S * plan.tiles_per_set;
+    if (nblocks > 0x7fffffffLL || plan.groups > 65535) return hipErrorInvalidConfiguration;
+    const dim3 grid(static_cast<unsigned>(nblocks), static_cast<unsigned>(plan.groups));
+    switch (dtype) {
+    case KNN_F32: return launch_dist_dt<KNN_F32>(plan, args, grid, stream);
+    case KNN_BF16: return launch_dist_dt<KNN_BF16>(plan, args, grid, stream);
+    case KNN_F16: return launch_dist_dt<KNN_F16>(plan, args, grid, stream);
+    }
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_key_sqnorms(const void *keys, int64_t n, int64_t d, knn_dtype dtype, float *out,
+                              hipStream_t stream) {
+    if (n == 0) return hipSuccess;
+    const int64_t waves_needed = n;
+    int64_t blocks = (waves_needed + kWavesPerDistBlock - 1) / kWavesPerDistBlock;
+    if (blocks > 65536) blocks = 65536;
+    const dim3 grid(static_cast<unsigned>(blocks));
+    const bool vec = vector_path_ok(d, dtype, keys, keys);
+    const int cpl = vec ? pow2_at_least((d / vec_elems(dtype) + kWave - 1) / kWave) : 0;
+#define KNN_SQN(DT)                                                                                 \
+    do {                                                                                            \
+        if (!vec) {                                                                                 \
+            hipLaunchKernelGGL((k_sqnorm_elem<DT>), grid, dim3(kDistThreads), 0, stream, keys, n, d, out); \
+        } else {                                                                                    \
+            switch (cpl) {                                                                          \
+            case 1: hipLaunchKernelGGL((k_sqnorm_vec<DT, 1>), grid, dim3(kDistThreads), 0, stream, keys, n, d, out); break; \
+            case 2: hipLaunchKernelGGL((k_sqnorm_vec<DT, 2>), grid, dim3(kDistThreads), 0, stream, keys, n, d, out); break; \
+            case 4: hipLaunchKernelGGL((k_sqnorm_vec<DT, 4>), grid, dim3(kDistThreads), 0, stream, keys, n, d, out); break; \
+            case 8: hipLaunchKernelGGL((k_sqnorm_vec<DT, 8>), grid, dim3(kDistThreads), 0, stream, keys, n, d, out); break; \
+            case 16: hipLaunchKernelGGL((k_sqnorm_vec<DT, 16>), grid, dim3(kDistThreads), 0, stream, keys, n, d, out); break; \
+            default: return hipErrorInvalidValue;                                                   \
+            }                                                                                       \
+        }                                                                                           \
+    } while (0)
+    switch (dtype) {
+    case KNN_F32: KNN_SQN(KNN_F32); break;
+    case KNN_BF16: KNN_SQN(KNN_BF16); break;
+    case KNN_F16: KNN_SQN(KNN_F16); break;
+    default: return hipErrorInvalidValue;
+    }
+#undef KNN_SQN
+    return hipGetLastError();
+}
+
+}  // namespace knnlm

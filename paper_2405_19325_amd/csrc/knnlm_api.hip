@@ -1,0 +1,360 @@
+// C ABI of the kNN-LM mixture step: host-side validation, workspace layout and
+// the launches of the three stages on the caller's stream.
+#include <math.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "knnlm.h"
+#include "knnlm_internal.h"
+
+namespace {
+
+using namespace knnlm;
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool valid_dtype(knn_dtype t) { return t == KNN_F32 || t == KNN_BF16 || t == KNN_F16; }
+
+// Key rows per distance workgroup: about 512 KiB of keys, fewer when the
+// launch would otherwise have under 2048 workgroups.  A multiple of 8 rows
+// (4 waves x up to 2 rows per iteration).  Depends on sizes only, so the
+// workspace size does not depend on pointer alignment.
+int tile_rows(int64_t d, knn_dtype dtype, int64_t S, int64_t max_keys) {
+    const int64_t step = 8;
+    const int64_t row_bytes = d * elem_bytes(dtype);
+    int64_t rpt = (512 * 1024) / (row_bytes > 0 ? row_bytes : 1);
+    if (rpt > 4096) rpt = 4096;
+    rpt = (rpt + step - 1) / step * step;
+    if (rpt < step) rpt = step;
+    while (rpt > step && S * ((max_keys + rpt - 1) / rpt) < 2048) rpt = (rpt / 2 + step - 1) / step * step;
+    return static_cast<int>(rpt);
+}
+
+struct Layout {
+    int rows_per_tile;
+    int64_t tiles_per_set;
+    int64_t ld;  // distance row stride = tiles_per_set * rows_per_tile
+    size_t off_dist, off_tmin, off_tmax, total;
+};
+
+Layout layout(int64_t B, int64_t d, int64_t S, int64_t max_keys, knn_dtype dtype) {
+    Layout L{};
+    L.rows_per_tile = tile_rows(d, dtype, S, max_keys);
+    L.tiles_per_set = (max_keys + L.rows_per_tile - 1) / L.rows_per_tile;
+    if (L.tiles_per_set < 1) L.tiles_per_set = 1;
+    L.ld = L.tiles_per_set * L.rows_per_tile;
+    L.off_dist = 0;
+    L.off_tmin = align_up(L.off_dist + sizeof(float) * static_cast<size_t>(B) * static_cast<size_t>(L.ld));
+    L.off_tmax = align_up(L.off_tmin + sizeof(float) * static_cast<size_t>(B) * static_cast<size_t>(L.tiles_per_set));
+    L.total = align_up(L.off_tmax + sizeof(float) * static_cast<size_t>(B) * static_cast<size_t>(L.tiles_per_set));
+    return L;
+}
+
+bool finite_pos(float x) { return isfinite(x) && x > 0.0f; }
+
+knn_status check_sizes(int64_t B, int64_t d, int64_t V, int64_t S, int64_t total_keys,
+                       int64_t min_keys, int64_t max_keys, int64_t max_queries, knn_dtype dtype,
+                       int32_t r, bool need_vocab) {
+    if (B < 1 || d < 1 || S < 1 || total_keys < 1 || max_queries < 1) return KNN_ERR_INVALID_ARG;
+    if (need_vocab && V < 1) return KNN_ERR_INVALID_ARG;
+    if (!valid_dtype(dtype)) return KNN_ERR_INVALID_ARG;
+    if (min_keys < 0 || max_keys < 1 || min_keys > max_keys || max_keys > total_keys || max_queries > B)
+        return KNN_ERR_INVALID_ARG;
+    if (r < 1) return KNN_ERR_INVALID_ARG;
+    if (B > 0x7fffffffLL || max_keys > 0x7fffffffLL) return KNN_ERR_UNSUPPORTED;
+    if (r > KNNLM_MAX_R) return KNN_ERR_UNSUPPORTED;
+    if (need_vocab && (V + kMixTile - 1) / kMixTile > 65535) return KNN_ERR_UNSUPPORTED;
+    if (d > (int64_t(1) << 40) / elem_bytes(dtype)) return KNN_ERR_UNSUPPORTED;
+    if (r > min_keys) return KNN_ERR_R_EXCEEDS_N;
+    const Layout L = layout(B, d, S, max_keys, dtype);
+    if (S * L.tiles_per_set > 0x7fffffffLL) return KNN_ERR_UNSUPPORTED;
+    if (max_queries > 65535) return KNN_ERR_UNSUPPORTED;  // query groups per set on grid.y
+    return KNN_OK;
+}
+
+knn_status check_scalars(float mu, float lambda) {
+    if (!finite_pos(mu)) return KNN_ERR_INVALID_ARG;
+    if (!(lambda >= 0.0f && lambda <= 1.0f)) return KNN_ERR_INVALID_ARG;
+    return KNN_OK;
+}
+
+knn_status status_of(hipError_t e) { return e == hipSuccess ? KNN_OK : KNN_ERR_HIP; }
+
+struct Call {
+    const void *queries;
+    const void *keys;
+    const float *key_sqnorms;
+    const int32_t *values;
+    const int64_t *key_offsets;
+    const int64_t *query_offsets;
+    const float *p_lm;
+    int64_t B, d, V, S, total_keys, min_keys, max_keys, max_queries;
+    knn_dtype dtype;
+    int32_t r;
+    float mu, lambda;
+    float *p_m;
+    int32_t *nbr_ids;
+    float *nbr_dists;
+    void *workspace;
+    size_t workspace_bytes;
+};
+
+knn_status validate_part(const Call &c, int part) {
+    knn_status st = check_sizes(c.B, c.d, c.V, c.S, c.total_keys, c.min_keys, c.max_keys, c.max_queries,
+                                c.dtype, c.r, part == 0 || part == KNN_PART_MIX);
+    if (st != KNN_OK) return st;
+    if (!c.key_offsets || !c.query_offsets) return KNN_ERR_INVALID_ARG;
+    const bool dist = part == 0 || part == KNN_PART_DISTANCES;
+    const bool sel = part == 0 || part == KNN_PART_SELECT;
+    const bool mix = part == 0 || part == KNN_PART_MIX;
+    if (dist && (!c.queries || !c.keys)) return KNN_ERR_INVALID_ARG;
+    if ((sel || mix) && (!c.nbr_ids || !c.nbr_dists)) return KNN_ERR_INVALID_ARG;
+    if (mix && (!c.values || !c.p_lm || !c.p_m)) return KNN_ERR_INVALID_ARG;
+    if (mix && (st = check_scalars(c.mu, c.lambda)) != KNN_OK) return st;
+    if (dist || sel) {
+        if (!c.workspace) return KNN_ERR_WORKSPACE;
+        if (reinterpret_cast<uintptr_t>(c.workspace) % kAlign) return KNN_ERR_WORKSPACE;
+        const Layout L = layout(c.B, c.d, c.S, c.max_keys, c.dtype);
+        if (c.workspace_bytes < L.total) return KNN_ERR_WORKSPACE;
+    }
+    return KNN_OK;
+}
+
+knn_status run_part(const Call &c, int part, hipStream_t stream) {
+    const Layout L = layout(c.B, c.d, c.S, c.max_keys, c.dtype);
+    char *ws = static_cast<char *>(c.workspace);
+    float *dist = ws ? reinterpret_cast<float *>(ws + L.off_dist) : nullptr;
+    float *tmin = ws ? reinterpret_cast<float *>(ws + L.off_tmin) : nullptr;
+    float *tmax = ws ? reinterpret_cast<float *>(ws + L.off_tmax) : nullptr;
+    if (part == KNN_PART_DISTANCES) {
+        DistPlan p = plan_distances(c.d, c.dtype, c.max_queries, c.queries, c.keys);
+        p.rows_per_tile = L.rows_per_tile;
+        p.tiles_per_set = L.tiles_per_set;
+        DistArgs a{};
+        a.queries = c.queries;
+        a.keys = c.keys;
+        a.key_sqnorms = c.key_sqnorms;
+        a.key_offsets = c.key_offsets;
+        a.query_offsets = c.query_offsets;
+        a.d = c.d;
+        a.ld = L.ld;
+        a.dist = dist;
+        a.tile_min = tmin;
+        a.tile_max = tmax;
+        a.tiles_per_set = L.tiles_per_set;
+        a.rows_per_tile = L.rows_per_tile;
+        return status_of(launch_distances(p, c.dtype, a, c.S, stream));
+    }
+    if (part == KNN_PART_SELECT) {
+        SelectArgs a{};
+        a.dist = dist;
+        a.tile_min = tmin;
+        a.tile_max = tmax;
+        a.key_offsets = c.key_offsets;
+        a.query_offsets = c.query_offsets;
+        a.S = c.S;
+        a.ld = L.ld;
+        a.tiles_per_set = L.tiles_per_set;
+        a.rows_per_tile = L.rows_per_tile;
+        a.r = c.r;
+        a.ids = c.nbr_ids;
+        a.dists = c.nbr_dists;
+        return status_of(launch_select(a, c.B, stream));
+    }
+    if (part == KNN_PART_MIX) {
+        MixArgs a{};
+        a.ids = c.nbr_ids;
+        a.dists = c.nbr_dists;
+        a.values = c.values;
+        a.key_offsets = c.key_offsets;
+        a.query_offsets = c.query_offsets;
+        a.p_lm = c.p_lm;
+        a.p_m = c.p_m;
+        a.S = c.S;
+        a.V = c.V;
+        a.r = c.r;
+        a.mu = c.mu;
+        a.lambda = c.lambda;
+        return status_of(launch_mix(a, c.B, stream));
+    }
+    return KNN_ERR_INVALID_ARG;
+}
+
+Call make_call(const void *queries, const void *keys, const float *key_sqnorms, const int32_t *values,
+               const int64_t *key_offsets, const int64_t *query_offsets, const float *p_lm, int64_t B,
+               int64_t d, int64_t V, int64_t S, int64_t total_keys, int64_t min_keys, int64_t max_keys,
+               int64_t max_queries, knn_dtype dtype, int32_t r, float mu, float lambda, float *p_m,
+               int32_t *nbr_ids, float *nbr_dists, void *workspace, size_t workspace_bytes) {
+    Call c;
+    c.queries = queries;
+    c.keys = keys;
+    c.key_sqnorms = key_sqnorms;
+    c.values = values;
+    c.key_offsets = key_offsets;
+    c.query_offsets = query_offsets;
+    c.p_lm = p_lm;
+    c.B = B;
+    c.d = d;
+    c.V = V;
+    c.S = S;
+    c.total_keys = total_keys;
+    c.min_keys = min_keys;
+    c.max_keys = max_keys;
+    c.max_queries = max_queries;
+    c.dtype = dtype;
+    c.r = r;
+    c.mu = mu;
+    c.lambda = lambda;
+    c.p_m = p_m;
+    c.nbr_ids = nbr_ids;
+    c.nbr_dists = nbr_dists;
+    c.workspace = workspace;
+    c.workspace_bytes = workspace_bytes;
+    return c;
+}
+
+}  // namespace
+
+extern "C" {
+
+knn_status knn_lm_mixture(const void *queries, const void *keys, const float *key_sqnorms,
+                          const int32_t *values, const int64_t *key_offsets,
+                          const int64_t *query_offsets, const float *p_lm, int64_t B, int64_t d,
+                          int64_t V, int64_t S, int64_t total_keys, int64_t min_keys_per_set,
+                          int64_t max_keys_per_set, int64_t max_queries_per_set, knn_dtype dtype,
+                          int32_t r, float mu, float lambda, float *p_m, int32_t *nbr_ids,
+                          float *nbr_dists, void *workspace, size_t workspace_bytes, void *stream) {
+    const Call c = make_call(queries, keys, key_sqnorms, values, key_offsets, query_offsets, p_lm, B, d, V, S,
+                             total_keys, min_keys_per_set, max_keys_per_set, max_queries_per_set, dtype, r, mu,
+                             lambda, p_m, nbr_ids, nbr_dists, workspace, workspace_bytes);
+    knn_status st = validate_part(c, 0);
+    if (st != KNN_OK) return st;
+    hipStream_t hs = static_cast<hipStream_t>(stream);
+    for (int part = KNN_PART_DISTANCES; part <= KNN_PART_MIX; ++part) {
+        st = run_part(c, part, hs);
+        if (st != KNN_OK) return st;
+    }
+    return KNN_OK;
+}
+
+knn_status knn_lm_mixture_part(knn_part part, const void *queries, const void *keys,
+                               const float *key_sqnorms, const int32_t *values,
+                               const int64_t *key_offsets, const int64_t *query_offsets,
+                               const float *p_lm, int64_t B, int64_t d, int64_t V, int64_t S,
+                               int64_t total_keys, int64_t min_keys_per_set,
+                               int64_t max_keys_per_set, int64_t max_queries_per_set,
+                               knn_dtype dtype, int32_t r, float mu, float lambda, float *p_m,
+                               int32_t *nbr_ids, float *nbr_dists, void *workspace,
+                               size_t workspace_bytes, void *stream) {
+    if (part != KNN_PART_DISTANCES && part != KNN_PART_SELECT && part != KNN_PART_MIX) return KNN_ERR_INVALID_ARG;
+    const Call c = make_call(queries, keys, key_sqnorms, values, key_offsets, query_offsets, p_lm, B, d, V, S,
+                             total_keys, min_keys_per_set, max_keys_per_set, max_queries_per_set, dtype, r, mu,
+                             lambda, p_m, nbr_ids, nbr_dists, workspace, workspace_bytes);
+    const knn_status st = validate_part(c, part);
+    if (st != KNN_OK) return st;
+    return run_part(c, part, static_cast<hipStream_t>(stream));
+}
+
+size_t knn_lm_mixture_workspace_size(int64_t B, int64_t d, int64_t V, int64_t S, int64_t total_keys,
+                                     int64_t min_keys_per_set, int64_t max_keys_per_set,
+                                     int64_t max_queries_per_set, knn_dtype dtype, int32_t r) {
+    if (check_sizes(B, d, V, S, total_keys, min_keys_per_set, max_keys_per_set, max_queries_per_set, dtype, r,
+                    true) != KNN_OK)
+        return 0;
+    return layout(B, d, S, max_keys_per_set, dtype).total;
+}
+
+knn_status knn_lm_mixture_validate(const void *queries, const void *keys, const int32_t *values,
+                                   const int64_t *key_offsets, const int64_t *query_offsets,
+                                   const float *p_lm, int64_t B, int64_t d, int64_t V, int64_t S,
+                                   int64_t total_keys, int64_t min_keys_per_set,
+                                   int64_t max_keys_per_set, int64_t max_queries_per_set,
+                                   knn_dtype dtype, int32_t r, float mu, float lambda,
+                                   const float *p_m, const int32_t *nbr_ids,
+                                   const float *nbr_dists, const void *workspace,
+                                   size_t workspace_bytes) {
+    const Call c = make_call(queries, keys, nullptr, values, key_offsets, query_offsets, p_lm, B, d, V, S,
+                             total_keys, min_keys_per_set, max_keys_per_set, max_queries_per_set, dtype, r, mu,
+                             lambda, const_cast<float *>(p_m), const_cast<int32_t *>(nbr_ids),
+                             const_cast<float *>(nbr_dists), const_cast<void *>(workspace), workspace_bytes);
+    return validate_part(c, 0);
+}
+
+knn_status knn_distances(const void *queries, const void *keys, const float *key_sqnorms,
+                         const int64_t *key_offsets, const int64_t *query_offsets, int64_t B,
+                         int64_t d, int64_t S, int64_t max_keys_per_set,
+                         int64_t max_queries_per_set, knn_dtype dtype, float *out, int64_t ld_out,
+                         void *stream) {
+    if (!queries || !keys || !key_offsets || !query_offsets || !out) return KNN_ERR_INVALID_ARG;
+    if (B < 1 || d < 1 || S < 1 || max_keys_per_set < 1 || max_queries_per_set < 1 || max_queries_per_set > B)
+        return KNN_ERR_INVALID_ARG;
+    if (!valid_dtype(dtype) || ld_out < max_keys_per_set) return KNN_ERR_INVALID_ARG;
+    if (B > 0x7fffffffLL || max_keys_per_set > 0x7fffffffLL || max_queries_per_set > 65535) return KNN_ERR_UNSUPPORTED;
+    DistPlan p = plan_distances(d, dtype, max_queries_per_set, queries, keys);
+    p.rows_per_tile = tile_rows(d, dtype, S, max_keys_per_set);
+    p.tiles_per_set = (max_keys_per_set + p.rows_per_tile - 1) / p.rows_per_tile;
+    if (S * p.tiles_per_set > 0x7fffffffLL || p.groups > 65535) return KNN_ERR_UNSUPPORTED;
+    DistArgs a{};
+    a.queries = queries;
+    a.keys = keys;
+    a.key_sqnorms = key_sqnorms;
+    a.key_offsets = key_offsets;
+    a.query_offsets = query_offsets;
+    a.d = d;
+    a.ld = ld_out;
+    a.dist = out;
+    a.tile_min = nullptr;
+    a.tile_max = nullptr;
+    a.tiles_per_set = p.tiles_per_set;
+    a.rows_per_tile = p.rows_per_tile;
+    return status_of(launch_distances(p, dtype, a, S, static_cast<hipStream_t>(stream)));
+}
+
+knn_status knn_key_sqnorms(const void *keys, int64_t n, int64_t d, knn_dtype dtype, float *out, void *stream) {
+    if (!keys || !out || n < 0 || d < 1 || !valid_dtype(dtype)) return KNN_ERR_INVALID_ARG;
+    return status_of(launch_key_sqnorms(keys, n, d, dtype, out, static_cast<hipStream_t>(stream)));
+}
+
+knn_status knn_mix(const int32_t *nbr_ids, const float *nbr_dists, const int32_t *values,
+                   const int64_t *key_offsets, const int64_t *query_offsets, const float *p_lm,
+                   int64_t B, int64_t V, int64_t S, int32_t r, float mu, float lambda, float *p_m,
+                   void *stream) {
+    if (!nbr_ids || !nbr_dists || !values || !key_offsets || !query_offsets || !p_lm || !p_m)
+        return KNN_ERR_INVALID_ARG;
+    if (B < 1 || V < 1 || S < 1 || r < 1) return KNN_ERR_INVALID_ARG;
+    if (r > KNNLM_MAX_R || B > 0x7fffffffLL || (V + kMixTile - 1) / kMixTile > 65535) return KNN_ERR_UNSUPPORTED;
+    const knn_status st = check_scalars(mu, lambda);
+    if (st != KNN_OK) return st;
+    MixArgs a{};
+    a.ids = nbr_ids;
+    a.dists = nbr_dists;
+    a.values = values;
+    a.key_offsets = key_offsets;
+    a.query_offsets = query_offsets;
+    a.p_lm = p_lm;
+    a.p_m = p_m;
+    a.S = S;
+    a.V = V;
+    a.r = r;
+    a.mu = mu;
+    a.lambda = lambda;
+    return status_of(launch_mix(a, B, static_cast<hipStream_t>(stream)));
+}
+
+const char *knn_status_string(knn_status status) {
+    switch (status) {
+    case KNN_OK: return "ok";
+    case KNN_ERR_INVALID_ARG: return "invalid argument";
+    case KNN_ERR_R_EXCEEDS_N: return "r exceeds the smallest key set";
+    case KNN_ERR_UNSUPPORTED: return "unsupported size or configuration";
+    case KNN_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+    case KNN_ERR_HIP: return "HIP launch failed";
+    }
+    return "unknown status";
+}
+
+int knn_abi_version(void) { return KNNLM_ABI_VERSION; }
+
+}  // extern "C"

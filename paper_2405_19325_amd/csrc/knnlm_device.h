@@ -1,0 +1,136 @@
+// Device helpers shared by the kernels: the dot-product word step and wave reductions.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "knnlm_internal.h"
+
+namespace knnlm {
+
+template <knn_dtype DT>
+struct Elem;
+template <>
+struct Elem<KNN_F32> {
+    static constexpr int VEC = 4;   // elements per 16-byte chunk
+    static constexpr int BYTES = 4;
+    static constexpr int PER_WORD = 1;  // elements per 32-bit word
+};
+template <>
+struct Elem<KNN_BF16> {
+    static constexpr int VEC = 8;
+    static constexpr int BYTES = 2;
+    static constexpr int PER_WORD = 2;
+};
+template <>
+struct Elem<KNN_F16> {
+    static constexpr int VEC = 8;
+    static constexpr int BYTES = 2;
+    static constexpr int PER_WORD = 2;
+};
+
+// acc + the products of one 32-bit word of q with the same word of k: two
+// packed 16-bit elements through the gfx950 dot2 instruction (fp32 accumulate),
+// or one fp32 element through an FMA.  Every dot product and squared norm in
+// the library is a chain of these calls over the words of a row, so equal
+// inputs give equal bits on every path.
+template <knn_dtype DT>
+__device__ __forceinline__ float dot_word(uint32_t q, uint32_t k, float acc);
+
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
+
+template <>
+__device__ __forceinline__ float dot_word<KNN_F32>(uint32_t q, uint32_t k, float acc) {
+    return fmaf(__uint_as_float(q), __uint_as_float(k), acc);
+}
+template <>
+__device__ __forceinline__ float dot_word<KNN_BF16>(uint32_t q, uint32_t k, float acc) {
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, q), __builtin_bit_cast(bf16x2_t, k), acc,
+                                           false);
+}
+template <>
+__device__ __forceinline__ float dot_word<KNN_F16>(uint32_t q, uint32_t k, float acc) {
+    return __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2_t, q), __builtin_bit_cast(f16x2_t, k), acc, false);
+}
+
+// The four words of a 16-byte chunk, in order.
+template <knn_dtype DT>
+__device__ __forceinline__ float dot_chunk(const uint4 q, const uint4 k, float acc) {
+    acc = dot_word<DT>(q.x, k.x, acc);
+    acc = dot_word<DT>(q.y, k.y, acc);
+    acc = dot_word<DT>(q.z, k.z, acc);
+    acc = dot_word<DT>(q.w, k.w, acc);
+    return acc;
+}
+
+// Word w of a row read with element loads (elements past d read as 0).
+template <knn_dtype DT>
+__device__ __forceinline__ uint32_t load_word(const void *row, int64_t w, int64_t d) {
+    if constexpr (DT == KNN_F32) {
+        return w < d ? __float_as_uint(static_cast<const float *>(row)[w]) : 0u;
+    } else {
+        const uint16_t *h = static_cast<const uint16_t *>(row);
+        const int64_t i = 2 * w;
+        const uint32_t lo = i < d ? h[i] : 0u;
+        const uint32_t hi = i + 1 < d ? h[i + 1] : 0u;
+        return lo | (hi << 16);
+    }
+}
+
+// Sum over the 64 lanes of a wave; every lane receives the same bits (each
+// butterfly step adds the same two operands in both partner lanes).
+__device__ __forceinline__ float wave_allsum(float v) {
+    v += __shfl_xor(v, 32);
+    v += __shfl_xor(v, 16);
+    v += __shfl_xor(v, 8);
+    v += __shfl_xor(v, 4);
+    v += __shfl_xor(v, 2);
+    v += __shfl_xor(v, 1);
+    return v;
+}
+
+__device__ __forceinline__ float wave_allmin(float v) {
+    for (int m = 32; m >= 1; m >>= 1) v = fminf(v, __shfl_xor(v, m));
+    return v;
+}
+
+__device__ __forceinline__ float wave_allmax(float v) {
+    for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m));
+    return v;
+}
+
+__device__ __forceinline__ uint32_t wave_allmin_u32(uint32_t v) {
+    for (int m = 32; m >= 1; m >>= 1) v = min(v, static_cast<uint32_t>(__shfl_xor(static_cast<int>(v), m)));
+    return v;
+}
+
+__device__ __forceinline__ uint32_t wave_allmax_u32(uint32_t v) {
+    for (int m = 32; m >= 1; m >>= 1) v = max(v, static_cast<uint32_t>(__shfl_xor(static_cast<int>(v), m)));
+    return v;
+}
+
+// Inclusive prefix sum over the lanes of a wave.
+__device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t v, int lane) {
+    for (int m = 1; m < 64; m <<= 1) {
+        uint32_t o = static_cast<uint32_t>(__shfl_up(static_cast<int>(v), m));
+        if (lane >= m) v += o;
+    }
+    return v;
+}
+
+// Distances are >= +0, so their fp32 bit patterns order like the values.
+__device__ __forceinline__ float clamp_nonneg(float x) { return x > 0.0f ? x : 0.0f; }
+
+// Set s owning query b: the s with query_offsets[s] <= b < query_offsets[s+1]
+// (the last such s when empty sets share an offset).
+__device__ __forceinline__ int64_t set_of_query(const int64_t *query_offsets, int64_t S, int64_t b) {
+    int64_t lo = 0, hi = S;  // invariant: qo[lo] <= b < qo[hi]
+    while (hi - lo > 1) {
+        const int64_t mid = (lo + hi) >> 1;
+        if (query_offsets[mid] <= b) lo = mid; else hi = mid;
+    }
+    return lo;
+}
+
+}  // namespace knnlm

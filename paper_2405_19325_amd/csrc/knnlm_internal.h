@@ -1,0 +1,90 @@
+// Internal interfaces between the C ABI (knnlm_api.hip) and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "knnlm.h"
+
+namespace knnlm {
+
+constexpr int kWave = 64;           // CDNA wavefront width
+constexpr int kDistThreads = 256;   // distance workgroup: 4 waves
+constexpr int kSelectThreads = 1024;
+constexpr int kSelectBinsLog2 = 11; // 2048-bin histogram per refinement pass
+constexpr int kSelectBins = 1 << kSelectBinsLog2;
+constexpr int kMixThreads = 256;
+constexpr int kMixTile = 4096;      // vocabulary entries per mix workgroup (16 KiB of LDS)
+constexpr int kMaxCplVec = 16;      // 16-byte chunks per lane on the vector path (d <= 1024*VEC)
+
+inline int elem_bytes(knn_dtype t) { return t == KNN_F32 ? 4 : 2; }
+inline int vec_elems(knn_dtype t) { return 16 / elem_bytes(t); }
+
+// How the distance kernel covers the (set, key tile, query group) space.
+struct DistPlan {
+    bool vec;               // 16-byte loads (d % VEC == 0, aligned rows) vs element loads
+    int cpl;                // chunks per lane (vector path), power of two <= kMaxCplVec
+    int nq;                 // queries per workgroup (1, 2, 4 or 8)
+    int rows;               // rows per wave iteration
+    int rows_per_tile;      // key rows per workgroup (from the workspace layout)
+    int64_t tiles_per_set;  // ceil(max_keys / rows_per_tile)
+    int64_t groups;         // ceil(max_queries / nq)
+};
+
+struct DistArgs {
+    const void *queries;
+    const void *keys;
+    const float *key_sqnorms;    // may be null
+    const int64_t *key_offsets;
+    const int64_t *query_offsets;
+    int64_t d;
+    int64_t ld;                  // row stride of dist (>= max keys per set)
+    float *dist;                 // [B, ld]
+    float *tile_min;             // [B, tiles_per_set] or null
+    float *tile_max;
+    int64_t tiles_per_set;
+    int rows_per_tile;
+};
+
+struct SelectArgs {
+    const float *dist;           // [B, ld]
+    const float *tile_min;       // [B, tiles_per_set] or null
+    const float *tile_max;
+    const int64_t *key_offsets;
+    const int64_t *query_offsets;
+    int64_t S;
+    int64_t ld;
+    int64_t tiles_per_set;
+    int rows_per_tile;
+    int r;
+    int32_t *ids;                // [B, r]
+    float *dists;                // [B, r]
+};
+
+struct MixArgs {
+    const int32_t *ids;          // [B, r]
+    const float *dists;          // [B, r]
+    const int32_t *values;
+    const int64_t *key_offsets;
+    const int64_t *query_offsets;
+    const float *p_lm;           // [B, V]
+    float *p_m;                  // [B, V]
+    int64_t S;
+    int64_t V;
+    int r;
+    float mu;
+    float lambda;
+};
+
+DistPlan plan_distances(int64_t d, knn_dtype dtype, int64_t max_queries, const void *queries,
+                        const void *keys);
+
+hipError_t launch_distances(const DistPlan &plan, knn_dtype dtype, const DistArgs &args, int64_t S,
+                            hipStream_t stream);
+hipError_t launch_key_sqnorms(const void *keys, int64_t n, int64_t d, knn_dtype dtype, float *out,
+                              hipStream_t stream);
+int select_capacity(int r);
+hipError_t launch_select(const SelectArgs &args, int64_t B, hipStream_t stream);
+hipError_t launch_mix(const MixArgs &args, int64_t B, hipStream_t stream);
+
+}  // namespace knnlm

@@ -1,0 +1,296 @@
+"""Parity of the HIP path (through the C ABI) against the CPU oracle on the GPU.
+
+Rules P2-P5 are in tests/parity.py.  Cases: the hand-worked cases, exact
+integer inputs (every distance exact, so ids, order and distances must match
+the oracle bit for bit), every element type and both load paths, ragged key
+sets, planted neighbours, degenerate shapes (r = 1, r = N, r = 4096, all keys
+equal, empty query groups), lambda = 1, precomputed key norms, the stage
+entry points, and the full-size workloads on sampled queries.
+"""
+import gc
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import parity
+from workloads import gen
+
+pytestmark = pytest.mark.gpu
+
+knn = pytest.importorskip("paper_2405_19325_amd")
+
+
+def _say(msg):
+    print(f"[gpu] {msg}", flush=True)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _device():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    knn.load()
+    yield
+    torch.cuda.synchronize()
+
+
+def _tensor_inputs(q, k, vals, p_lm, ko, qo, dtype):
+    dev = "cuda"
+    tq = torch.as_tensor(q).to(dev)
+    tk = torch.as_tensor(k).to(dev)
+    if dtype != torch.float32:
+        tq, tk = tq.to(dtype), tk.to(dtype)
+    return (tq.contiguous(), tk.contiguous(), torch.as_tensor(vals, dtype=torch.int32, device=dev),
+            torch.as_tensor(ko, dtype=torch.int64, device=dev), torch.as_tensor(qo, dtype=torch.int64, device=dev),
+            torch.as_tensor(p_lm, dtype=torch.float32, device=dev))
+
+
+def _run(w, key_sqnorms=None):
+    prob = knn.MixtureProblem(w.queries, w.keys, w.values, w.key_offsets, w.query_offsets, w.p_lm, w.r, w.mu,
+                              w.lam, key_sqnorms=key_sqnorms, key_offsets_host=w.key_offsets_host,
+                              query_offsets_host=w.query_offsets_host)
+    out = prob.run()
+    torch.cuda.synchronize()
+    return out
+
+
+def _free():
+    gc.collect()
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+# ------------------------------------------------------------------ hand cases
+
+@pytest.mark.parametrize("which", ["H-A", "H-B"])
+def test_hand_cases(golden_dir, which):
+    doc = json.load(open(os.path.join(golden_dir, "hand_cases.json")))[which]
+    for case in doc["cases"]:
+        _say(f"hand case {case['name']}")
+        tq, tk, tv, tko, tqo, tp = _tensor_inputs([doc["query"]], doc["keys"], doc["values"], [doc["p_lm"]],
+                                                  [0, len(doc["keys"])], [0, 1], torch.float32)
+        p_m, ids, dists = knn.mixture(tq.float(), tk.float(), tv, tko, tqo, tp, case["r"], case["mu"], doc["lam"])
+        torch.cuda.synchronize()
+        assert ids[0].tolist() == case["expect_ids"]
+        assert dists[0].tolist() == [float(x) for x in case["expect_dists"]]
+        pknn = [float(eval(e, {"__builtins__": {}}, {"exp": math.exp, "sqrt": math.sqrt})) for e in case["pknn_expr"]]
+        expect = [doc["lam"] * np.float32(p) + (1 - doc["lam"]) * x for p, x in zip(doc["p_lm"], pknn)]
+        np.testing.assert_allclose(p_m[0].cpu().numpy(), expect, rtol=0, atol=1e-6)
+
+
+# ------------------------------------------------------- exact-integer inputs
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16, torch.float16])
+@pytest.mark.parametrize("d,n,r", [(2, 50, 1), (3, 700, 7), (8, 3000, 64), (64, 5000, 1024), (64, 2100, 2100),
+                                   (24, 9000, 300)])
+def test_exact_integer_inputs_match_bitwise(dtype, d, n, r):
+    _say(f"exact integers dtype={dtype} d={d} n={n} r={r}")
+    rng = np.random.default_rng(d * 1000 + n)
+    B = 3
+    q = rng.integers(-4, 5, (B, d)).astype(np.float32)
+    k = rng.integers(-4, 5, (n, d)).astype(np.float32)
+    vals = rng.integers(0, 1000, n).astype(np.int32)
+    p_lm = np.full((B, 1000), 1e-3, np.float32)
+    tq, tk, tv, tko, tqo, tp = _tensor_inputs(q, k, vals, p_lm, [0, n], [0, B], dtype)
+    p_m, ids, dists = knn.mixture(tq, tk, tv, tko, tqo, tp, r, 0.05, 0.25)
+    torch.cuda.synchronize()
+    qh, dt = oracle.host_elements(tq)
+    kh, _ = oracle.host_elements(tk)
+    oids, odists = oracle.select(qh, kh, dt, np.array([0, n]), np.array([0, B]), r)
+    np.testing.assert_array_equal(ids.cpu().numpy(), oids)
+    np.testing.assert_array_equal(dists.cpu().numpy().astype(np.float64), odists)
+    pm_ref = oracle.mix(oids, odists, vals, np.array([0, n]), np.array([0, B]), p_lm, 0.05, 0.25)
+    np.testing.assert_allclose(p_m.cpu().numpy(), pm_ref, rtol=0, atol=1e-6)
+
+
+def test_all_keys_equal_ties_break_by_index():
+    _say("all keys equal")
+    n, d, r = 5000, 32, 1000
+    k = np.ones((n, d), np.float32)
+    q = np.zeros((2, d), np.float32)
+    vals = (np.arange(n) % 17).astype(np.int32)
+    p_lm = np.full((2, 17), 1 / 17, np.float32)
+    tq, tk, tv, tko, tqo, tp = _tensor_inputs(q, k, vals, p_lm, [0, n], [0, 2], torch.bfloat16)
+    p_m, ids, dists = knn.mixture(tq, tk, tv, tko, tqo, tp, r, 0.1, 0.5)
+    torch.cuda.synchronize()
+    assert ids.cpu().numpy().tolist() == [list(range(r))] * 2
+    assert torch.all(dists == 32.0)
+    counts = np.bincount(vals[:r], minlength=17) / r
+    expect = np.broadcast_to(0.5 * np.float32(1 / 17) + 0.5 * counts, (2, 17))
+    np.testing.assert_allclose(p_m.cpu().numpy(), expect, atol=1e-6)
+
+
+# ------------------------------------------------------------ small workloads
+
+SMALL = [
+    ("tiny-f32", gen.config("tiny"), 1, None),
+    ("decode-bf16-small", gen.scaled(gen.config("decode_7b"), n_keys=20000), 2, None),
+    ("ragged-bf16", gen.scaled(gen.config("ragged_batch"), B=12, S=7, n_keys=(1100, 5000, 3333, 2048, 2049, 1024, 7777),
+                                r=1024), 3, None),
+    ("multi-query-f16", gen.scaled(gen.config("specverify_static"), B=24, S=3, n_keys=(6000, 4000, 9000), d=1024,
+                                   query_mode="iid"), 6, None),
+    ("odd-d-bf16", gen.scaled(gen.config("decode_7b"), d=1000, n_keys=3001, B=2, r=200, mu=1 / math.sqrt(1000)), 7, None),
+    ("odd-d-f32", gen.scaled(gen.config("tiny"), d=37, n_keys=2999, B=5, r=33), 8, None),
+    ("d8192-bf16", gen.scaled(gen.config("decode_70b"), B=2, S=2, n_keys=6000), 4, None),
+    ("r1", gen.scaled(gen.config("decode_7b"), n_keys=5000, r=1), 9, None),
+    ("r4096", gen.scaled(gen.config("decode_7b"), n_keys=9000, r=4096, B=2), 10, None),
+    ("planted-bf16", gen.scaled(gen.config("decode_7b"), n_keys=30000, B=3, query_mode="planted"), 12, None),
+    ("empty-sets", gen.scaled(gen.config("decode_7b"), B=3, S=5, n_keys=(3000, 2000, 4000, 2500, 1500), d=512,
+                              r=256, mu=1 / math.sqrt(512)), 13, [0, 2, 0, 1, 0]),
+]
+
+
+def _make_small(spec, seed, qps):
+    if qps is None:
+        return gen.make(spec, seed, device="cuda")
+    # a workload whose sets own the given numbers of queries (some own none)
+    w = gen.make(spec.replace(B=sum(qps), S=len(qps)), seed, device="cuda")
+    qo = np.concatenate([[0], np.cumsum(qps)]).astype(np.int64)
+    w.query_offsets_host = qo
+    w.query_offsets = torch.as_tensor(qo, device="cuda")
+    return w
+
+
+@pytest.mark.parametrize("name,spec,seed,qps", SMALL, ids=[s[0] for s in SMALL])
+def test_small_workloads(name, spec, seed, qps):
+    _say(f"workload {name}")
+    w = _make_small(spec, seed, qps)
+    p_m, ids, dists = _run(w)
+    rep = parity.check_workload(w, p_m, ids, dists)
+    _say(f"{name}: {rep.summary()}")
+    assert rep.ok(), rep.failures[:5]
+    if spec.query_mode == "planted":
+        assert ids[:, 0].cpu().numpy().tolist() == w.planted_ids.tolist()
+
+
+def test_query_equal_to_key_gives_zero_distance():
+    _say("q == k")
+    spec = gen.scaled(gen.config("decode_7b"), n_keys=8000, B=4)
+    w = gen.make(spec, 21, device="cuda")
+    picks = [5, 4000, 7999, 123]
+    w.queries = w.keys[picks].clone()
+    for norms in (None, knn.key_sqnorms(w.keys)):
+        p_m, ids, dists = _run(w, key_sqnorms=norms)
+        assert ids[:, 0].cpu().tolist() == picks
+        assert torch.all(dists[:, 0] == 0.0)
+
+
+def test_lambda_one_returns_plm_bitwise():
+    _say("lambda = 1")
+    w = gen.make(gen.scaled(gen.config("decode_7b"), n_keys=6000, B=2, lam=1.0), 22, device="cuda")
+    p_m, _, _ = _run(w)
+    assert torch.equal(p_m, w.p_lm)
+
+
+def test_lambda_zero_is_pknn():
+    _say("lambda = 0")
+    w = gen.make(gen.scaled(gen.config("tiny"), n_keys=3000, lam=0.0), 23, device="cuda")
+    p_m, ids, dists = _run(w)
+    rep = parity.check_workload(w, p_m, ids, dists)
+    assert rep.ok(), rep.failures[:5]
+
+
+def test_precomputed_norms_give_identical_results():
+    _say("precomputed norms")
+    w = gen.make(gen.scaled(gen.config("ragged_batch"), B=4, S=4, n_keys=(3000, 5000, 2000, 4096)), 24, device="cuda")
+    _, ids0, d0 = _run(w)
+    ids0, d0 = ids0.clone(), d0.clone()
+    norms = knn.key_sqnorms(w.keys)
+    _, ids1, d1 = _run(w, key_sqnorms=norms)
+    assert torch.equal(ids0, ids1) and torch.equal(d0, d1)
+    ref = w.keys.float().pow(2).sum(1)
+    torch.testing.assert_close(norms, ref, rtol=1e-5, atol=1e-5)
+
+
+def test_element_path_matches_vector_path_bitwise():
+    """A key matrix that is not 16-byte aligned takes the element-load path; the
+    accumulation order is the same, so every output bit is the same."""
+    _say("element vs vector path")
+    w = gen.make(gen.scaled(gen.config("decode_7b"), n_keys=5000, B=2, d=512, mu=1 / math.sqrt(512)), 25, device="cuda")
+    _, ids0, d0 = _run(w)
+    ids0, d0 = ids0.clone(), d0.clone()
+    buf = torch.empty(w.keys.numel() + 1, dtype=w.keys.dtype, device="cuda")
+    shifted = buf[1:].view(w.keys.shape)
+    shifted.copy_(w.keys)
+    assert shifted.data_ptr() % 16 != 0
+    w.keys = shifted
+    _, ids1, d1 = _run(w)
+    assert torch.equal(ids0, ids1) and torch.equal(d0, d1)
+
+
+def test_stages_equal_whole_call_and_repeat_deterministically():
+    _say("stages vs whole call")
+    w = gen.make(gen.scaled(gen.config("ragged_batch"), B=6, S=3, n_keys=(4000, 6000, 3000)), 26, device="cuda")
+    prob = knn.MixtureProblem(w.queries, w.keys, w.values, w.key_offsets, w.query_offsets, w.p_lm, w.r, w.mu,
+                              w.lam, key_offsets_host=w.key_offsets_host, query_offsets_host=w.query_offsets_host)
+    prob.run()
+    torch.cuda.synchronize()
+    ids0, d0, pm0 = prob.ids.clone(), prob.dists.clone(), prob.p_m.clone()
+    for part in ("distances", "select", "mix"):
+        prob.run_part(part)
+    torch.cuda.synchronize()
+    assert torch.equal(ids0, prob.ids) and torch.equal(d0, prob.dists)
+    torch.testing.assert_close(pm0, prob.p_m, rtol=0, atol=1e-7)
+
+
+def test_distance_matrix_entry_point():
+    _say("knn_distances")
+    w = gen.make(gen.scaled(gen.config("ragged_batch"), B=5, S=2, n_keys=(1000, 1500), d=256, mu=1 / 16), 27,
+                 device="cuda")
+    D = knn.distances(w.queries, w.keys, w.key_offsets, w.query_offsets, key_offsets_host=w.key_offsets_host,
+                      query_offsets_host=w.query_offsets_host).cpu().numpy()
+    ko, qo = w.key_offsets_host, w.query_offsets_host
+    for s in range(2):
+        kh, dt = oracle.host_elements(w.keys[ko[s]:ko[s + 1]])
+        qh, _ = oracle.host_elements(w.queries[qo[s]:qo[s + 1]])
+        ref = oracle.sqdist(qh, kh, dt)
+        got = D[qo[s]:qo[s + 1], :ko[s + 1] - ko[s]]
+        np.testing.assert_allclose(got, ref, rtol=1e-5, atol=2e-4)
+        assert np.all(np.isnan(D[qo[s]:qo[s + 1], ko[s + 1] - ko[s]:]))
+
+
+def test_mix_entry_point():
+    _say("knn_mix")
+    rng = np.random.default_rng(28)
+    B, n, r, V = 3, 500, 100, 9000
+    ids = np.stack([rng.permutation(n)[:r] for _ in range(B)]).astype(np.int32)
+    dists = rng.uniform(10, 20, (B, r)).astype(np.float32)
+    vals = rng.integers(0, V, n).astype(np.int32)
+    p_lm = rng.dirichlet(np.ones(V), B).astype(np.float32)
+    ko, qo = np.array([0, n]), np.array([0, B])
+    dev = "cuda"
+    out = knn.mix(torch.as_tensor(ids, device=dev), torch.as_tensor(dists, device=dev),
+                  torch.as_tensor(vals, device=dev), torch.as_tensor(ko, device=dev), torch.as_tensor(qo, device=dev),
+                  torch.as_tensor(p_lm, device=dev), 0.3, 0.4)
+    ref = oracle.mix(ids, dists.astype(np.float64), vals, ko, qo, p_lm, 0.3, 0.4)
+    np.testing.assert_allclose(out.cpu().numpy(), ref, rtol=0, atol=1e-6)
+
+
+# -------------------------------------------------------- full-size workloads
+
+FULL = [("decode_7b", None), ("ragged_batch", [0, 17, 40, 63]), ("decode_70b", [0, 9]),
+        ("specverify_seq", [0, 31, 127]), ("specverify_static", [0, 77])]
+
+
+@pytest.mark.parametrize("name,sample", FULL, ids=[f[0] for f in FULL])
+def test_full_size_workloads(name, sample):
+    _free()
+    _say(f"full workload {name}: generating")
+    w = gen.make(gen.config(name), gen.CONFIG_SEEDS[name], device="cuda")
+    _say(f"full workload {name}: running")
+    p_m, ids, dists = _run(w)
+    _say(f"full workload {name}: oracle on {sample if sample is not None else 'all'} queries")
+    rep = parity.check_workload(w, p_m, ids, dists, sample=sample)
+    _say(f"{name}: {rep.summary()}")
+    # properties that hold for every query
+    pm64 = p_m.double()
+    torch.testing.assert_close(pm64.sum(1), w.lam * w.p_lm.double().sum(1) + (1 - w.lam), rtol=0, atol=1e-5)
+    assert torch.all(dists[:, 1:] >= dists[:, :-1])
+    assert int(ids.min()) >= 0
+    assert rep.ok(), rep.failures[:5]
+    del w, p_m, ids, dists
+    _free()

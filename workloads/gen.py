@@ -246,3 +246,17 @@ def config(name: str) -> Spec:
 
 def scaled(spec: Spec, **overrides) -> Spec:
     return spec.replace(**overrides)
+
+
+def extra_queries(spec: Spec, seed: int, n: int, device="cpu") -> torch.Tensor:
+    """n further query rows drawn like the workload's i.i.d. queries (sub-stream +700)."""
+    return _draw_normal_rows(n, spec.d, spec.key_scale, DTYPES[spec.dtype], torch.device(device),
+                             _gen(torch.device(device), seed + 700))
+
+
+def second_key_copy(spec: Spec, seed: int, device="cpu") -> torch.Tensor:
+    """Another key matrix of the same shape and law (sub-stream +800), used to rotate
+    buffers so that repeated timed calls cannot be served from the 256 MB last-level cache."""
+    sizes = _set_sizes(spec, seed)
+    return _draw_normal_rows(int(sum(sizes)), spec.d, spec.key_scale, DTYPES[spec.dtype], torch.device(device),
+                             _gen(torch.device(device), seed + 800))
