@@ -67,11 +67,13 @@ typedef enum {
 /* Element type of queries and keys. */
 typedef enum { KNN_F32 = 0, KNN_BF16 = 1, KNN_F16 = 2 } knn_dtype;
 
-/* Stages of knn_lm_mixture, runnable one at a time by knn_lm_mixture_part(). */
+/* Stages of knn_lm_mixture, runnable one at a time by knn_lm_mixture_part().
+ * knn_lm_mixture itself runs KNN_PART_DISTANCES then KNN_PART_SELECT_MIX. */
 typedef enum {
     KNN_PART_DISTANCES = 1, /* squared distances of every query to its set (into the workspace) */
     KNN_PART_SELECT = 2,    /* top-r per query: nbr_ids, nbr_dists */
-    KNN_PART_MIX = 3        /* softmax over mu*s, scatter onto values, lambda-mix: p_m */
+    KNN_PART_MIX = 3,       /* softmax over mu*s, scatter onto values, lambda-mix: p_m */
+    KNN_PART_SELECT_MIX = 4 /* SELECT and MIX in one launch */
 } knn_part;
 
 /*
@@ -111,11 +113,13 @@ knn_status knn_lm_mixture(const void *queries, const void *keys, const float *ke
 
 /*
  * knn_lm_mixture_part -- one stage of knn_lm_mixture with the same arguments.
- * Calling KNN_PART_DISTANCES, KNN_PART_SELECT, KNN_PART_MIX in that order on
- * one stream with one workspace is exactly knn_lm_mixture.  Pointers a stage
- * does not use may be NULL (DISTANCES: values, p_lm, p_m, nbr_ids, nbr_dists;
- * SELECT: queries, keys, key_sqnorms, values, p_lm, p_m; MIX: queries, keys,
- * key_sqnorms, workspace).
+ * KNN_PART_DISTANCES followed by either KNN_PART_SELECT_MIX or KNN_PART_SELECT
+ * then KNN_PART_MIX, on one stream with one workspace, computes what
+ * knn_lm_mixture computes (neighbours and distances bit for bit; p_m up to
+ * the order of float additions in the scatter).  Pointers a stage does not
+ * use may be NULL (DISTANCES: values, p_lm, p_m, nbr_ids, nbr_dists; SELECT:
+ * queries, keys, key_sqnorms, values, p_lm, p_m; MIX: queries, keys,
+ * key_sqnorms, workspace; SELECT_MIX: queries, keys, key_sqnorms).
  */
 knn_status knn_lm_mixture_part(knn_part part, const void *queries, const void *keys,
                                const float *key_sqnorms, const int32_t *values,

@@ -128,7 +128,7 @@ class MixtureProblem:
         return self.p_m, self.ids, self.dists
 
     def run_part(self, part: str, stream=None):
-        """One stage ("distances", "select", "mix") of knn_lm_mixture on this problem's workspace."""
+        """One stage ("distances", "select", "mix", "select_mix") of knn_lm_mixture on this problem's workspace."""
         _lib.check("knn_lm_mixture_part", load().knn_lm_mixture_part(PARTS[part], *self._args(stream)))
 
 

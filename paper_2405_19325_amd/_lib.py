@@ -24,7 +24,7 @@ KNN_OK = 0
 STATUS_NAMES = {0: "KNN_OK", 1: "KNN_ERR_INVALID_ARG", 2: "KNN_ERR_R_EXCEEDS_N", 3: "KNN_ERR_UNSUPPORTED",
                 4: "KNN_ERR_WORKSPACE", 5: "KNN_ERR_HIP"}
 DTYPES = {"f32": 0, "bf16": 1, "f16": 2}
-PARTS = {"distances": 1, "select": 2, "mix": 3}
+PARTS = {"distances": 1, "select": 2, "mix": 3, "select_mix": 4}
 
 _MIX_ARGS = [P, P, P, P, P, P, P, I64, I64, I64, I64, I64, I64, I64, I64, I, I32, F, F, P, P, P, P, SZ, P]
 

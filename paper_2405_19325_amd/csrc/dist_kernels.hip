@@ -11,7 +11,7 @@
 // 16-byte chunks of four words; lane l of a wave accumulates chunks l, l+64,
 // l+128, ... word by word into one fp32 accumulator (v_dot2_f32_bf16 /
 // v_dot2_f32_f16 for 16-bit elements, FMA for fp32); the 64 lane partials are
-// then summed by a butterfly that leaves the same bits in every lane.
+// then summed by a fixed reduction tree that leaves the same bits in every lane.
 // ||q||^2, ||k||^2 and q.k all use this order, so q == k gives exactly 0.
 #include "knnlm_device.h"
 #include "knnlm_internal.h"
@@ -105,15 +105,6 @@ __global__ __launch_bounds__(kDistThreads) void k_dist_vec(DistArgs a) {
             qv[j][c] = (j < t.nq && ch < nchunks) ? qrow[ch] : zero;
         }
     }
-    float qq[NQ];
-#pragma unroll
-    for (int j = 0; j < NQ; ++j) {
-        float acc = 0.0f;
-#pragma unroll
-        for (int c = 0; c < CPL; ++c) acc = dot_chunk<DT>(qv[j][c], qv[j][c], acc);
-        qq[j] = wave_allsum(acc);
-    }
-
     float mn[NQ], mx[NQ];
 #pragma unroll
     for (int j = 0; j < NQ; ++j) {
@@ -123,16 +114,40 @@ __global__ __launch_bounds__(kDistThreads) void k_dist_vec(DistArgs a) {
     const bool have_norms = a.key_sqnorms != nullptr;
     const char *kset = static_cast<const char *>(a.keys) + t.k0 * row_bytes;
 
-    for (int64_t row = t.r0 + wave * ROWS; row < t.r1; row += NW * ROWS) {
-        uint4 kv[ROWS][CPL];
+    // Software pipeline: the loads of a wave's next ROWS rows are in flight
+    // while the current rows are reduced.
+    constexpr int64_t kStep = static_cast<int64_t>(NW) * ROWS;
+    uint4 kv[ROWS][CPL];
+    int64_t row = t.r0 + wave * ROWS;
+#pragma unroll
+    for (int rr = 0; rr < ROWS; ++rr) {
+        const int64_t rw = row + rr;
+        const uint4 *krow = reinterpret_cast<const uint4 *>(kset + rw * row_bytes);
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) {
+            const int ch = lane + kWave * c;
+            kv[rr][c] = (rw < t.r1 && ch < nchunks) ? load_stream(krow + ch) : zero;
+        }
+    }
+    // ||q||^2 after the first key loads are issued, so they overlap the query's latency.
+    float qq[NQ];
+#pragma unroll
+    for (int j = 0; j < NQ; ++j) {
+        float acc = 0.0f;
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) acc = dot_chunk<DT>(qv[j][c], qv[j][c], acc);
+        qq[j] = wave_allsum(acc);
+    }
+    for (; row < t.r1; row += kStep) {
+        uint4 kn[ROWS][CPL];
 #pragma unroll
         for (int rr = 0; rr < ROWS; ++rr) {
-            const int64_t rw = row + rr;
+            const int64_t rw = row + kStep + rr;
             const uint4 *krow = reinterpret_cast<const uint4 *>(kset + rw * row_bytes);
 #pragma unroll
             for (int c = 0; c < CPL; ++c) {
                 const int ch = lane + kWave * c;
-                kv[rr][c] = (rw < t.r1 && ch < nchunks) ? krow[ch] : zero;
+                kn[rr][c] = (rw < t.r1 && ch < nchunks) ? load_stream(krow + ch) : zero;
             }
         }
 #pragma unroll
@@ -160,6 +175,10 @@ __global__ __launch_bounds__(kDistThreads) void k_dist_vec(DistArgs a) {
                 }
             }
         }
+#pragma unroll
+        for (int rr = 0; rr < ROWS; ++rr)
+#pragma unroll
+            for (int c = 0; c < CPL; ++c) kv[rr][c] = kn[rr][c];
     }
     if (a.tile_min != nullptr) write_tile_extrema<NQ>(a, t, mn, mx);
 }
@@ -368,7 +387,7 @@ DistPlan plan_distances(int64_t d, knn_dtype dtype, int64_t max_queries, const v
         int nq = 8;
         while (nq > 1 && (nq * p.cpl > kQueryRegChunks || nq / 2 >= mq)) nq >>= 1;
         p.nq = nq;
-        p.rows = (p.cpl <= kMaxCplVec / 2) ? 2 : 1;
+        p.rows = 1;  // one row per wave iteration, the next one already loading (measured best)
     } else {
         p.cpl = 0;
         int nq = 8;

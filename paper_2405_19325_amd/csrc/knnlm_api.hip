@@ -17,18 +17,19 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 bool valid_dtype(knn_dtype t) { return t == KNN_F32 || t == KNN_BF16 || t == KNN_F16; }
 
-// Key rows per distance workgroup: about 512 KiB of keys, fewer when the
-// launch would otherwise have under 2048 workgroups.  A multiple of 8 rows
-// (4 waves x up to 2 rows per iteration).  Depends on sizes only, so the
-// workspace size does not depend on pointer alignment.
+// Key rows per distance workgroup: about 1 MiB of keys, fewer when the launch
+// would otherwise have under 512 workgroups (two per CU: measured best for
+// the streaming kernel).  A multiple of 8 rows (4 waves x up to 2 rows per
+// iteration).  Depends on sizes only, so the workspace size does not depend on
+// pointer alignment.
 int tile_rows(int64_t d, knn_dtype dtype, int64_t S, int64_t max_keys) {
     const int64_t step = 8;
     const int64_t row_bytes = d * elem_bytes(dtype);
-    int64_t rpt = (512 * 1024) / (row_bytes > 0 ? row_bytes : 1);
+    int64_t rpt = (1024 * 1024) / (row_bytes > 0 ? row_bytes : 1);
     if (rpt > 4096) rpt = 4096;
     rpt = (rpt + step - 1) / step * step;
     if (rpt < step) rpt = step;
-    while (rpt > step && S * ((max_keys + rpt - 1) / rpt) < 2048) rpt = (rpt / 2 + step - 1) / step * step;
+    while (rpt > step && S * ((max_keys + rpt - 1) / rpt) < 512) rpt = (rpt / 2 + step - 1) / step * step;
     return static_cast<int>(rpt);
 }
 
@@ -65,7 +66,7 @@ knn_status check_sizes(int64_t B, int64_t d, int64_t V, int64_t S, int64_t total
     if (r < 1) return KNN_ERR_INVALID_ARG;
     if (B > 0x7fffffffLL || max_keys > 0x7fffffffLL) return KNN_ERR_UNSUPPORTED;
     if (r > KNNLM_MAX_R) return KNN_ERR_UNSUPPORTED;
-    if (need_vocab && (V + kMixTile - 1) / kMixTile > 65535) return KNN_ERR_UNSUPPORTED;
+    if (need_vocab && V > 0x7fffffffLL) return KNN_ERR_UNSUPPORTED;
     if (d > (int64_t(1) << 40) / elem_bytes(dtype)) return KNN_ERR_UNSUPPORTED;
     if (r > min_keys) return KNN_ERR_R_EXCEEDS_N;
     const Layout L = layout(B, d, S, max_keys, dtype);
@@ -103,12 +104,12 @@ struct Call {
 
 knn_status validate_part(const Call &c, int part) {
     knn_status st = check_sizes(c.B, c.d, c.V, c.S, c.total_keys, c.min_keys, c.max_keys, c.max_queries,
-                                c.dtype, c.r, part == 0 || part == KNN_PART_MIX);
+                                c.dtype, c.r, part == 0 || part == KNN_PART_MIX || part == KNN_PART_SELECT_MIX);
     if (st != KNN_OK) return st;
     if (!c.key_offsets || !c.query_offsets) return KNN_ERR_INVALID_ARG;
     const bool dist = part == 0 || part == KNN_PART_DISTANCES;
-    const bool sel = part == 0 || part == KNN_PART_SELECT;
-    const bool mix = part == 0 || part == KNN_PART_MIX;
+    const bool sel = part == 0 || part == KNN_PART_SELECT || part == KNN_PART_SELECT_MIX;
+    const bool mix = part == 0 || part == KNN_PART_MIX || part == KNN_PART_SELECT_MIX;
     if (dist && (!c.queries || !c.keys)) return KNN_ERR_INVALID_ARG;
     if ((sel || mix) && (!c.nbr_ids || !c.nbr_dists)) return KNN_ERR_INVALID_ARG;
     if (mix && (!c.values || !c.p_lm || !c.p_m)) return KNN_ERR_INVALID_ARG;
@@ -120,6 +121,23 @@ knn_status validate_part(const Call &c, int part) {
         if (c.workspace_bytes < L.total) return KNN_ERR_WORKSPACE;
     }
     return KNN_OK;
+}
+
+MixArgs mix_args(const Call &c) {
+    MixArgs a{};
+    a.ids = c.nbr_ids;
+    a.dists = c.nbr_dists;
+    a.values = c.values;
+    a.key_offsets = c.key_offsets;
+    a.query_offsets = c.query_offsets;
+    a.p_lm = c.p_lm;
+    a.p_m = c.p_m;
+    a.S = c.S;
+    a.V = c.V;
+    a.r = c.r;
+    a.mu = c.mu;
+    a.lambda = c.lambda;
+    return a;
 }
 
 knn_status run_part(const Call &c, int part, hipStream_t stream) {
@@ -147,7 +165,7 @@ knn_status run_part(const Call &c, int part, hipStream_t stream) {
         a.rows_per_tile = L.rows_per_tile;
         return status_of(launch_distances(p, c.dtype, a, c.S, stream));
     }
-    if (part == KNN_PART_SELECT) {
+    if (part == KNN_PART_SELECT || part == KNN_PART_SELECT_MIX) {
         SelectArgs a{};
         a.dist = dist;
         a.tile_min = tmin;
@@ -161,24 +179,10 @@ knn_status run_part(const Call &c, int part, hipStream_t stream) {
         a.r = c.r;
         a.ids = c.nbr_ids;
         a.dists = c.nbr_dists;
-        return status_of(launch_select(a, c.B, stream));
+        if (part == KNN_PART_SELECT) return status_of(launch_select(a, c.B, stream));
+        return status_of(launch_select_mix(a, mix_args(c), c.B, stream));
     }
-    if (part == KNN_PART_MIX) {
-        MixArgs a{};
-        a.ids = c.nbr_ids;
-        a.dists = c.nbr_dists;
-        a.values = c.values;
-        a.key_offsets = c.key_offsets;
-        a.query_offsets = c.query_offsets;
-        a.p_lm = c.p_lm;
-        a.p_m = c.p_m;
-        a.S = c.S;
-        a.V = c.V;
-        a.r = c.r;
-        a.mu = c.mu;
-        a.lambda = c.lambda;
-        return status_of(launch_mix(a, c.B, stream));
-    }
+    if (part == KNN_PART_MIX) return status_of(launch_mix(mix_args(c), c.B, stream));
     return KNN_ERR_INVALID_ARG;
 }
 
@@ -232,11 +236,9 @@ knn_status knn_lm_mixture(const void *queries, const void *keys, const float *ke
     knn_status st = validate_part(c, 0);
     if (st != KNN_OK) return st;
     hipStream_t hs = static_cast<hipStream_t>(stream);
-    for (int part = KNN_PART_DISTANCES; part <= KNN_PART_MIX; ++part) {
-        st = run_part(c, part, hs);
-        if (st != KNN_OK) return st;
-    }
-    return KNN_OK;
+    st = run_part(c, KNN_PART_DISTANCES, hs);
+    if (st != KNN_OK) return st;
+    return run_part(c, KNN_PART_SELECT_MIX, hs);
 }
 
 knn_status knn_lm_mixture_part(knn_part part, const void *queries, const void *keys,
@@ -248,7 +250,8 @@ knn_status knn_lm_mixture_part(knn_part part, const void *queries, const void *k
                                knn_dtype dtype, int32_t r, float mu, float lambda, float *p_m,
                                int32_t *nbr_ids, float *nbr_dists, void *workspace,
                                size_t workspace_bytes, void *stream) {
-    if (part != KNN_PART_DISTANCES && part != KNN_PART_SELECT && part != KNN_PART_MIX) return KNN_ERR_INVALID_ARG;
+    if (part != KNN_PART_DISTANCES && part != KNN_PART_SELECT && part != KNN_PART_MIX && part != KNN_PART_SELECT_MIX)
+        return KNN_ERR_INVALID_ARG;
     const Call c = make_call(queries, keys, key_sqnorms, values, key_offsets, query_offsets, p_lm, B, d, V, S,
                              total_keys, min_keys_per_set, max_keys_per_set, max_queries_per_set, dtype, r, mu,
                              lambda, p_m, nbr_ids, nbr_dists, workspace, workspace_bytes);
@@ -324,7 +327,7 @@ knn_status knn_mix(const int32_t *nbr_ids, const float *nbr_dists, const int32_t
     if (!nbr_ids || !nbr_dists || !values || !key_offsets || !query_offsets || !p_lm || !p_m)
         return KNN_ERR_INVALID_ARG;
     if (B < 1 || V < 1 || S < 1 || r < 1) return KNN_ERR_INVALID_ARG;
-    if (r > KNNLM_MAX_R || B > 0x7fffffffLL || (V + kMixTile - 1) / kMixTile > 65535) return KNN_ERR_UNSUPPORTED;
+    if (r > KNNLM_MAX_R || B > 0x7fffffffLL || V > 0x7fffffffLL) return KNN_ERR_UNSUPPORTED;
     const knn_status st = check_scalars(mu, lambda);
     if (st != KNN_OK) return st;
     MixArgs a{};

@@ -54,6 +54,14 @@ __device__ __forceinline__ float dot_word<KNN_F16>(uint32_t q, uint32_t k, float
     return __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2_t, q), __builtin_bit_cast(f16x2_t, k), acc, false);
 }
 
+// Streaming 16-byte load: every key byte is read exactly once, so the load
+// carries the non-temporal hint and does not displace reusable cache lines.
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 load_stream(const uint4 *p) {
+    const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 // The four words of a 16-byte chunk, in order.
 template <knn_dtype DT>
 __device__ __forceinline__ float dot_chunk(const uint4 q, const uint4 k, float acc) {
@@ -78,16 +86,26 @@ __device__ __forceinline__ uint32_t load_word(const void *row, int64_t w, int64_
     }
 }
 
-// Sum over the 64 lanes of a wave; every lane receives the same bits (each
-// butterfly step adds the same two operands in both partner lanes).
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xf, 0xf, false));
+}
+
+// Sum over the 64 lanes of a wave; every lane receives the same bits.  Within
+// each 16-lane row, DPP exchanges (xor 1, xor 2, half-row mirror, row mirror)
+// add partner lanes -- both partners add the same two operands, so the whole
+// row ends with one value -- then the four row sums are read out to scalar
+// registers and added as (r0 + r1) + (r2 + r3).  No LDS round trips.
 __device__ __forceinline__ float wave_allsum(float v) {
-    v += __shfl_xor(v, 32);
-    v += __shfl_xor(v, 16);
-    v += __shfl_xor(v, 8);
-    v += __shfl_xor(v, 4);
-    v += __shfl_xor(v, 2);
-    v += __shfl_xor(v, 1);
-    return v;
+    v += dpp_f32<0xB1>(v);   // quad_perm [1,0,3,2]
+    v += dpp_f32<0x4E>(v);   // quad_perm [2,3,0,1]
+    v += dpp_f32<0x141>(v);  // row_half_mirror
+    v += dpp_f32<0x140>(v);  // row_mirror
+    const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+    const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+    const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+    const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+    return (r0 + r1) + (r2 + r3);
 }
 
 __device__ __forceinline__ float wave_allmin(float v) {

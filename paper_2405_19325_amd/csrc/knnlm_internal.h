@@ -13,8 +13,6 @@ constexpr int kDistThreads = 256;   // distance workgroup: 4 waves
 constexpr int kSelectThreads = 1024;
 constexpr int kSelectBinsLog2 = 11; // 2048-bin histogram per refinement pass
 constexpr int kSelectBins = 1 << kSelectBinsLog2;
-constexpr int kMixThreads = 256;
-constexpr int kMixTile = 4096;      // vocabulary entries per mix workgroup (16 KiB of LDS)
 constexpr int kMaxCplVec = 16;      // 16-byte chunks per lane on the vector path (d <= 1024*VEC)
 
 inline int elem_bytes(knn_dtype t) { return t == KNN_F32 ? 4 : 2; }
@@ -85,6 +83,7 @@ hipError_t launch_key_sqnorms(const void *keys, int64_t n, int64_t d, knn_dtype 
                               hipStream_t stream);
 int select_capacity(int r);
 hipError_t launch_select(const SelectArgs &args, int64_t B, hipStream_t stream);
+hipError_t launch_select_mix(const SelectArgs &args, const MixArgs &mix, int64_t B, hipStream_t stream);
 hipError_t launch_mix(const MixArgs &args, int64_t B, hipStream_t stream);
 
 }  // namespace knnlm

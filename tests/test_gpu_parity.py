@@ -230,11 +230,14 @@ def test_stages_equal_whole_call_and_repeat_deterministically():
     prob.run()
     torch.cuda.synchronize()
     ids0, d0, pm0 = prob.ids.clone(), prob.dists.clone(), prob.p_m.clone()
-    for part in ("distances", "select", "mix"):
-        prob.run_part(part)
-    torch.cuda.synchronize()
-    assert torch.equal(ids0, prob.ids) and torch.equal(d0, prob.dists)
-    torch.testing.assert_close(pm0, prob.p_m, rtol=0, atol=1e-7)
+    for parts in (("distances", "select", "mix"), ("distances", "select_mix")):
+        prob.ids.zero_()
+        prob.p_m.zero_()
+        for part in parts:
+            prob.run_part(part)
+        torch.cuda.synchronize()
+        assert torch.equal(ids0, prob.ids) and torch.equal(d0, prob.dists)
+        torch.testing.assert_close(pm0, prob.p_m, rtol=0, atol=1e-7)
 
 
 def test_distance_matrix_entry_point():
