@@ -108,33 +108,57 @@ __device__ __forceinline__ float wave_allsum(float v) {
     return (r0 + r1) + (r2 + r3);
 }
 
-__device__ __forceinline__ float wave_allmin(float v) {
-    for (int m = 32; m >= 1; m >>= 1) v = fminf(v, __shfl_xor(v, m));
-    return v;
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t old, uint32_t v) {
+    return static_cast<uint32_t>(
+        __builtin_amdgcn_update_dpp(static_cast<int>(old), static_cast<int>(v), CTRL, 0xf, 0xf, false));
 }
 
-__device__ __forceinline__ float wave_allmax(float v) {
-    for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m));
-    return v;
+__device__ __forceinline__ uint32_t readlane_u32(uint32_t v, int lane) {
+    return static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(v), lane));
+}
+
+// min / max over the 64 lanes (every lane gets the result): DPP exchanges
+// within each 16-lane row, then the four row results via readlane.
+__device__ __forceinline__ float wave_allmin(float v) {
+    v = fminf(v, dpp_f32<0xB1>(v));
+    v = fminf(v, dpp_f32<0x4E>(v));
+    v = fminf(v, dpp_f32<0x141>(v));
+    v = fminf(v, dpp_f32<0x140>(v));
+    const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+    const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+    const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+    const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+    return fminf(fminf(r0, r1), fminf(r2, r3));
 }
 
 __device__ __forceinline__ uint32_t wave_allmin_u32(uint32_t v) {
-    for (int m = 32; m >= 1; m >>= 1) v = min(v, static_cast<uint32_t>(__shfl_xor(static_cast<int>(v), m)));
-    return v;
+    v = min(v, dpp_u32<0xB1>(v, v));
+    v = min(v, dpp_u32<0x4E>(v, v));
+    v = min(v, dpp_u32<0x141>(v, v));
+    v = min(v, dpp_u32<0x140>(v, v));
+    return min(min(readlane_u32(v, 0), readlane_u32(v, 16)), min(readlane_u32(v, 32), readlane_u32(v, 48)));
 }
 
 __device__ __forceinline__ uint32_t wave_allmax_u32(uint32_t v) {
-    for (int m = 32; m >= 1; m >>= 1) v = max(v, static_cast<uint32_t>(__shfl_xor(static_cast<int>(v), m)));
-    return v;
+    v = max(v, dpp_u32<0xB1>(v, v));
+    v = max(v, dpp_u32<0x4E>(v, v));
+    v = max(v, dpp_u32<0x141>(v, v));
+    v = max(v, dpp_u32<0x140>(v, v));
+    return max(max(readlane_u32(v, 0), readlane_u32(v, 16)), max(readlane_u32(v, 32), readlane_u32(v, 48)));
 }
 
-// Inclusive prefix sum over the lanes of a wave.
+// Inclusive prefix sum over the lanes of a wave: DPP row shifts by 1, 2, 4, 8
+// (lanes without a source add 0) scan each 16-lane row; the totals of the rows
+// below are then added from readlane.
 __device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t v, int lane) {
-    for (int m = 1; m < 64; m <<= 1) {
-        uint32_t o = static_cast<uint32_t>(__shfl_up(static_cast<int>(v), m));
-        if (lane >= m) v += o;
-    }
-    return v;
+    v += dpp_u32<0x111>(0u, v);  // row_shr:1
+    v += dpp_u32<0x112>(0u, v);  // row_shr:2
+    v += dpp_u32<0x114>(0u, v);  // row_shr:4
+    v += dpp_u32<0x118>(0u, v);  // row_shr:8
+    const uint32_t r0 = readlane_u32(v, 15), r1 = readlane_u32(v, 31), r2 = readlane_u32(v, 47);
+    const int row = lane >> 4;
+    return v + (row >= 1 ? r0 : 0u) + (row >= 2 ? r1 : 0u) + (row >= 3 ? r2 : 0u);
 }
 
 // Distances are >= +0, so their fp32 bit patterns order like the values.

@@ -8,25 +8,34 @@
 //
 // One 1024-thread workgroup per query.  Key i is ordered by (bits(d_i), i):
 // distances are >= +0, so their fp32 bit patterns order like the values, and
-// the index makes every key distinct.  A radix refinement narrows a range
-// known to hold the r-th smallest key -- first on the distance bits, then, if
-// a single distance value remains, on the key index -- with 2048-bin LDS
-// histograms until every key before the range's end fits in LDS; those keys
-// are compacted as 64-bit (bits << 32 | i) words, bitonic-sorted, and the
-// first r are the answer.
-// The range starts from the per-tile extrema the distance stage leaves, so one
-// histogram pass usually suffices.  Every pass streams the distance row in
-// 16 Ki-key batches (four 16-byte loads per thread), the next batch loading
-// while the current one is processed.
+// the index makes every key distinct.  Selection is a radix refinement: a
+// range known to hold the r-th smallest key is narrowed with 2048-bin LDS
+// histograms -- first on the distance bits, then, if a single distance value
+// remains, on the key index -- starting from the per-tile min/max the distance
+// stage leaves.
+//
+// Fast path (rows of at most 64 Ki keys, r <= 1024): the whole distance row is
+// read once into registers (sixteen 16-byte loads per thread, all in flight
+// together).  A histogram of 1024 keys sampled across the row picks a
+// threshold that keeps, with overwhelming probability, between r and 4096 keys;
+// one pass compacts them into LDS, and a bucket sort on their distance bits
+// orders them; the first r are pi.  If the sample misjudges the count, the
+// general path below takes over for that query, so the answer never depends on
+// the sample.
+//
+// General path: every pass streams the distance row in 16 Ki-key batches with
+// the next batch prefetched; the keys before the end of the final range (at
+// most CAP) are compacted and bitonic-sorted in LDS.
 //
 // Mixture (eq. non-parametric and eq. kNN-LM), when p_m is given: the softmax
 // of mu * s over the r neighbours (the largest mu * s, i.e. the smallest
 // distance, is subtracted first), scattered onto the neighbours' value tokens
-// in 8 Ki-entry LDS tiles of the vocabulary with LDS float atomics (tokens no
-// neighbour carries get 0; duplicates accumulate), then
-// p_M = fmaf(lambda, p_LM, acc * ((1 - lambda) / Z)), so lambda = 1 returns p_LM
-// bit for bit.  The order of the LDS atomics is not fixed, so p_kNN may differ
-// between runs in the last bits.
+// in LDS vocabulary tiles with LDS float atomics (tokens no neighbour carries
+// get 0; duplicates accumulate), then p_M = fmaf(lambda, p_LM, acc * ((1 -
+// lambda) / Z)), so lambda = 1 returns p_LM bit for bit.  The order of the LDS
+// atomics is not fixed, so p_kNN may differ between runs in the last bits.
+#include <math.h>
+
 #include "knnlm_device.h"
 #include "knnlm_internal.h"
 
@@ -34,16 +43,30 @@ namespace knnlm {
 
 namespace {
 
-constexpr int kNumWaves = kSelectThreads / kWave;
-constexpr int kU = 4;                                             // 16-byte loads per thread per batch
-constexpr int64_t kBatch = static_cast<int64_t>(kSelectThreads) * 4 * kU;  // keys per batch (16384)
-constexpr int kVocabTile = 8192;                                  // vocabulary entries per LDS tile
+constexpr int kT = kSelectThreads;                          // 1024 threads
+constexpr int kNumWaves = kT / kWave;
+constexpr int kPer = (KNNLM_MAX_R + kT - 1) / kT;            // neighbours per thread, general path
+constexpr int kU = 4;                                       // 16-byte loads per thread per streamed batch
+constexpr int64_t kBatch = static_cast<int64_t>(kT) * 4 * kU;  // keys per streamed batch (16384)
+constexpr int kFastU = 16;                                  // fast path: the whole row in registers
+constexpr int64_t kFastMaxN = static_cast<int64_t>(kT) * 4 * kFastU;  // 65536
+constexpr int kFastCap = 4096;                              // candidates the fast path keeps in LDS
+constexpr int kVocabTile = 8192;                            // mixture tile, general path
+constexpr int kVocabTileFast = 32768;                       // mixture tile, fast path (128 KiB)
 
-__device__ __forceinline__ uint64_t sort_key(uint32_t dbits, int64_t i) {
-    return (static_cast<uint64_t>(dbits) << 32) | static_cast<uint32_t>(i);
+struct Shared {
+    uint32_t red_u[2][kNumWaves];
+    uint32_t wave_tot[kNumWaves];
+    float red_f[kNumWaves];
+    uint32_t lo, hi, below, cnt, found, total;
+    float dmin;
+};
+
+__device__ __forceinline__ uint64_t sort_key(uint32_t dbits, uint32_t i) {
+    return (static_cast<uint64_t>(dbits) << 32) | i;
 }
 
-// Exclusive prefix sum of one value per thread over the 1024-thread block.
+// Exclusive prefix sum of one value per thread over the block.
 __device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t *wave_tot) {
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
@@ -74,44 +97,6 @@ __device__ __forceinline__ float block_sum(float v, float *red) {
     return t;
 }
 
-// Batch `b` of a distance row: thread t holds keys (u * 1024 + t) * 4 + e of
-// the batch, e < 4, for u < kU.  Keys past N are never used.
-__device__ __forceinline__ void load_batch(const float *drow, int64_t N, int64_t b, uint4 (&v)[kU]) {
-    const int64_t base = b * kBatch;
-#pragma unroll
-    for (int u = 0; u < kU; ++u) {
-        const int64_t i = base + (static_cast<int64_t>(u) * kSelectThreads + threadIdx.x) * 4;
-        v[u] = (i < N) ? *reinterpret_cast<const uint4 *>(drow + i) : make_uint4(0u, 0u, 0u, 0u);
-    }
-}
-
-// Position of element (u, e) of this thread inside its batch, relative to the
-// thread's first element: keys of a batch are at base + u * 4096 + e with
-// base = batch start + 4 * threadIdx.x, and the key is valid iff this offset
-// is below limit = N - base.
-// Prefetch batch bb + 1 (zeros past the last batch).
-__device__ __forceinline__ void next_batch(const float *drow, int64_t N, int32_t bb, int64_t nbatch, uint4 (&nx)[kU]) {
-    if (bb + 1 < nbatch) {
-        load_batch(drow, N, bb + 1, nx);
-    } else {
-#pragma unroll
-        for (int u = 0; u < kU; ++u) nx[u] = make_uint4(0u, 0u, 0u, 0u);
-    }
-}
-
-__device__ __forceinline__ void advance(uint4 (&v)[kU], const uint4 (&nx)[kU]) {
-#pragma unroll
-    for (int u = 0; u < kU; ++u) v[u] = nx[u];
-}
-
-__device__ __forceinline__ int32_t elem_off(int u, int e) { return u * kSelectThreads * 4 + e; }
-
-__device__ __forceinline__ uint32_t lane_word(const uint4 &v, int e) {
-    return e == 0 ? v.x : e == 1 ? v.y : e == 2 ? v.z : v.w;
-}
-
-constexpr int kPer = (KNNLM_MAX_R + kSelectThreads - 1) / kSelectThreads;  // neighbours per thread
-
 __device__ __forceinline__ float block_min(float v, float *red) {
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
@@ -125,240 +110,94 @@ __device__ __forceinline__ float block_min(float v, float *red) {
     return t;
 }
 
-// p_M row b: the weights wj (unnormalised softmax terms, sum z) are
-// scatter-added onto their tokens tok (-1: none) one vocabulary tile at a time
-// in LDS, and each tile of p_LM is mixed and written with 16-byte accesses.
-__device__ __forceinline__ void mix_row(const float (&wj)[kPer], const int32_t (&tok)[kPer], float z,
-                                        const MixArgs &m, int64_t b, float *acc) {
-    const int tid = threadIdx.x;
-    const float lam = m.lambda;
-    const float scale = (1.0f - lam) / z;
-    const float *plm = m.p_lm + b * m.V;
-    float *pm = m.p_m + b * m.V;
-    const bool vec4 = (m.V % 4 == 0) && ((reinterpret_cast<uintptr_t>(plm) | reinterpret_cast<uintptr_t>(pm)) & 15u) == 0;
-    for (int64_t v0 = 0; v0 < m.V; v0 += kVocabTile) {
-        const int64_t nv = (m.V - v0 < kVocabTile) ? m.V - v0 : kVocabTile;
-        for (int i = tid; i < kVocabTile; i += kSelectThreads) acc[i] = 0.0f;
-        __syncthreads();
+// min and max of the per-thread values over the block (every thread gets both).
+__device__ __forceinline__ void block_minmax_u32(uint32_t &mn, uint32_t &mx, Shared &sh) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    mn = wave_allmin_u32(mn);
+    mx = wave_allmax_u32(mx);
+    if (lane == 0) {
+        sh.red_u[0][wave] = mn;
+        sh.red_u[1][wave] = mx;
+    }
+    __syncthreads();
+    mn = sh.red_u[0][0];
+    mx = sh.red_u[1][0];
 #pragma unroll
-        for (int q = 0; q < kPer; ++q)
-            if (tok[q] >= v0 && tok[q] < v0 + nv) atomicAdd(&acc[tok[q] - v0], wj[q]);
-        __syncthreads();
-        if (vec4) {
-            const float4 *src = reinterpret_cast<const float4 *>(plm + v0);
-            float4 *dst = reinterpret_cast<float4 *>(pm + v0);
-            for (int64_t i = tid; i < nv / 4; i += kSelectThreads) {
-                const float4 p = src[i];
-                float4 o;
-                o.x = fmaf(lam, p.x, acc[4 * i + 0] * scale);
-                o.y = fmaf(lam, p.y, acc[4 * i + 1] * scale);
-                o.z = fmaf(lam, p.z, acc[4 * i + 2] * scale);
-                o.w = fmaf(lam, p.w, acc[4 * i + 3] * scale);
-                dst[i] = o;
-            }
-        } else {
-            for (int64_t i = tid; i < nv; i += kSelectThreads) pm[v0 + i] = fmaf(lam, plm[v0 + i], acc[i] * scale);
-        }
-        __syncthreads();
+    for (int w = 1; w < kNumWaves; ++w) {
+        mn = min(mn, sh.red_u[0][w]);
+        mx = max(mx, sh.red_u[1][w]);
+    }
+    __syncthreads();
+}
+
+// Range of a query's distance bits from the distance stage's per-tile extrema.
+__device__ __forceinline__ void row_range(const SelectArgs &a, int64_t b, int64_t N, uint32_t &bmin, uint32_t &bmax,
+                                          Shared &sh) {
+    bmin = 0xffffffffu;
+    bmax = 0u;
+    const int64_t ntiles = (N + a.rows_per_tile - 1) / a.rows_per_tile;
+    for (int64_t t = threadIdx.x; t < ntiles; t += kT) {
+        bmin = min(bmin, __float_as_uint(a.tile_min[b * a.tiles_per_set + t]));
+        bmax = max(bmax, __float_as_uint(a.tile_max[b * a.tiles_per_set + t]));
+    }
+    block_minmax_u32(bmin, bmax, sh);
+    if (N == 0) {
+        bmin = 0u;
+        bmax = 0u;
     }
 }
 
-template <int CAP, bool MIX>
-__global__ __launch_bounds__(kSelectThreads) void k_select(SelectArgs a, MixArgs m) {
-    __shared__ uint32_t hist[kSelectBins];
-    __shared__ uint64_t cand[CAP];
-    __shared__ float acc[MIX ? kVocabTile : 1];
-    __shared__ uint32_t red_u[2][kNumWaves];
-    __shared__ uint32_t wave_tot[kNumWaves];
-    __shared__ float red_f[kNumWaves];
-    __shared__ uint32_t sh_lo, sh_hi, sh_below, sh_cnt, sh_found, sh_fix;
+__device__ __forceinline__ uint32_t lane_word(const uint4 &v, int e) {
+    return e == 0 ? v.x : e == 1 ? v.y : e == 2 ? v.z : v.w;
+}
 
+// Element (u, e) of a thread's registers sits at key index base + u * 4096 + e.
+__device__ __forceinline__ int32_t elem_off(int u, int e) { return u * kT * 4 + e; }
+
+// Given the histogram of the keys inside the current range, move the range to
+// the bin holding the need-th of them.  Thread t owns bins 2t and 2t+1.
+__device__ __forceinline__ void pick_bin(const uint32_t *hist, uint32_t need, int shift, Shared &sh) {
     const int tid = threadIdx.x;
-    const int lane = tid & (kWave - 1);
-    const int wave = tid / kWave;
-    const int64_t b = blockIdx.x;
-    const int64_t s = set_of_query(a.query_offsets, a.S, b);
-    const int64_t k0 = a.key_offsets[s];
-    int64_t N = a.key_offsets[s + 1] - k0;
-    if (N > a.ld) N = a.ld;
-    const float *drow = a.dist + b * a.ld;
-    const uint32_t r_eff = static_cast<uint32_t>(N < a.r ? N : a.r);
-    const int64_t nbatch = (N + kBatch - 1) / kBatch;
-
-    // Range of the keys from the per-tile extrema (or one pass over the row).
-    uint32_t bmin = 0xffffffffu, bmax = 0u;
-    uint4 v[kU], nx[kU];
-    if (a.tile_min != nullptr) {
-        const int64_t ntiles = (N + a.rows_per_tile - 1) / a.rows_per_tile;
-        for (int64_t t = tid; t < ntiles; t += kSelectThreads) {
-            bmin = min(bmin, __float_as_uint(a.tile_min[b * a.tiles_per_set + t]));
-            bmax = max(bmax, __float_as_uint(a.tile_max[b * a.tiles_per_set + t]));
-        }
-    } else {
-        load_batch(drow, N, 0, v);
-        for (int32_t bb = 0; bb < nbatch; ++bb) {
-            next_batch(drow, N, bb, nbatch, nx);
-            const int32_t limit = static_cast<int32_t>(N) - (bb * static_cast<int32_t>(kBatch) + 4 * tid);
-#pragma unroll
-            for (int u = 0; u < kU; ++u)
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    if (elem_off(u, e) < limit) {
-                        bmin = min(bmin, lane_word(v[u], e));
-                        bmax = max(bmax, lane_word(v[u], e));
-                    }
-            advance(v, nx);
-        }
+    const uint32_t c0 = hist[2 * tid], c1 = hist[2 * tid + 1];
+    const uint32_t lo = sh.lo, hi = sh.hi;
+    const uint32_t excl = block_excl_scan(c0 + c1, sh.wave_tot);
+    int j = -1;
+    uint32_t before = 0, cj = 0;
+    if (excl < need && excl + c0 >= need) {
+        j = 2 * tid; before = excl; cj = c0;
+    } else if (excl + c0 < need && excl + c0 + c1 >= need) {
+        j = 2 * tid + 1; before = excl + c0; cj = c1;
     }
-    bmin = wave_allmin_u32(bmin);
-    bmax = wave_allmax_u32(bmax);
-    if (lane == 0) {
-        red_u[0][wave] = bmin;
-        red_u[1][wave] = bmax;
+    if (j >= 0) {
+        const uint32_t nlo = lo + (static_cast<uint32_t>(j) << shift);
+        const uint64_t nhi = static_cast<uint64_t>(nlo) + (1ull << shift);
+        sh.hi = nhi < hi ? static_cast<uint32_t>(nhi) : hi;
+        sh.lo = nlo;
+        sh.below += before;
+        sh.cnt = cj;
+        sh.found = 1u;
     }
     __syncthreads();
-    if (tid == 0) {
-        uint32_t mn = red_u[0][0], mx = red_u[1][0];
-        for (int w = 1; w < kNumWaves; ++w) {
-            mn = min(mn, red_u[0][w]);
-            mx = max(mx, red_u[1][w]);
-        }
-        if (N == 0) { mn = 0u; mx = 0u; }
-        sh_lo = mn;
-        sh_hi = mx + 1u;  // distances are >= +0, so mx < 0x80000000
-        sh_below = 0u;
-        sh_cnt = static_cast<uint32_t>(N);
-        sh_fix = 0u;
-    }
-    __syncthreads();
-    // The candidate range is [lo, hi) on distance bits while fix == 0; once it
-    // holds a single distance value fv, it becomes [lo, hi) on key indices
-    // among the keys at exactly fv (fix == 1).  `below` counts the keys known
-    // to precede the range, `cnt` the keys inside it.
-    uint32_t lo = sh_lo, hi = sh_hi, fv = 0u, fix = 0u;
-    uint32_t below = sh_below, cnt = sh_cnt;
+}
 
-    // Refinement: keep the range holding the r-th smallest key.  Each pass
-    // shrinks it by 2^10 at least (or switches to the index regime), so a few
-    // passes always suffice; the cap and the found flag only guard against
-    // inconsistent inputs.
-    for (int pass = 0; pass < 12 && below + cnt > static_cast<uint32_t>(CAP); ++pass) {
-        if (fix == 0u && hi - lo == 1u) {  // one distance value left: order by index
-            fix = 1u;
-            fv = lo;
-            lo = 0u;
-            hi = static_cast<uint32_t>(N);
-        }
-        const uint32_t w = hi - lo;  // >= 2 here
-        const int nbits = 32 - __clz(static_cast<int>(w - 1u));
-        const int shift = nbits > kSelectBinsLog2 ? nbits - kSelectBinsLog2 : 0;
-        for (int i = tid; i < kSelectBins; i += kSelectThreads) hist[i] = 0u;
-        if (tid == 0) sh_found = 0u;
-        __syncthreads();
-        load_batch(drow, N, 0, v);
-        for (int32_t bb = 0; bb < nbatch; ++bb) {
-            next_batch(drow, N, bb, nbatch, nx);
-            const int32_t base = bb * static_cast<int32_t>(kBatch) + 4 * tid;
-            const int32_t limit = static_cast<int32_t>(N) - base;
-            if (!fix) {
-#pragma unroll
-                for (int u = 0; u < kU; ++u)
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const uint32_t off = lane_word(v[u], e) - lo;
-                        if (elem_off(u, e) < limit && off < w) atomicAdd(&hist[off >> shift], 1u);
-                    }
-            } else {
-#pragma unroll
-                for (int u = 0; u < kU; ++u)
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const uint32_t off = static_cast<uint32_t>(base + elem_off(u, e)) - lo;
-                        if (elem_off(u, e) < limit && off < w && lane_word(v[u], e) == fv)
-                            atomicAdd(&hist[off >> shift], 1u);
-                    }
-            }
-            advance(v, nx);
-        }
-        __syncthreads();
-        // thread t owns bins 2t and 2t+1
-        const uint32_t c0 = hist[2 * tid], c1 = hist[2 * tid + 1];
-        const uint32_t excl = block_excl_scan(c0 + c1, wave_tot);
-        const uint32_t need = r_eff - below;  // >= 1
-        int j = -1;
-        uint32_t before = 0, cj = 0;
-        if (excl < need && excl + c0 >= need) {
-            j = 2 * tid; before = excl; cj = c0;
-        } else if (excl + c0 < need && excl + c0 + c1 >= need) {
-            j = 2 * tid + 1; before = excl + c0; cj = c1;
-        }
-        if (j >= 0) {
-            const uint32_t nlo = lo + (static_cast<uint32_t>(j) << shift);
-            const uint64_t nhi = static_cast<uint64_t>(nlo) + (1ull << shift);
-            sh_lo = nlo;
-            sh_hi = nhi < hi ? static_cast<uint32_t>(nhi) : hi;
-            sh_below = below + before;
-            sh_cnt = cj;
-            sh_found = 1u;
-        }
-        __syncthreads();
-        const bool found = sh_found != 0u;
-        lo = sh_lo; hi = sh_hi; below = sh_below; cnt = sh_cnt;
-        __syncthreads();
-        if (!found) break;
-    }
+__device__ __forceinline__ int range_shift(uint32_t w) {
+    const int nbits = 32 - __clz(static_cast<int>(w - 1u));
+    return nbits > kSelectBinsLog2 ? nbits - kSelectBinsLog2 : 0;
+}
 
-    // Compaction of every key before the end of the range (below + cnt <= CAP
-    // of them), at offsets from a block scan of the per-thread counts.
-    uint32_t written = 0;
-    load_batch(drow, N, 0, v);
-    for (int32_t bb = 0; bb < nbatch; ++bb) {
-        next_batch(drow, N, bb, nbatch, nx);
-        const int32_t base = bb * static_cast<int32_t>(kBatch) + 4 * tid;
-        const int32_t limit = static_cast<int32_t>(N) - base;
-        // a key is taken iff it precedes the end of the range
-        const uint32_t end_bits = fix ? fv : hi;
-        const uint32_t end_idx = fix ? hi : 0u;  // at bits == fv: indices below hi (none outside fix)
-        uint32_t c = 0;
-#pragma unroll
-        for (int u = 0; u < kU; ++u)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const uint32_t bits = lane_word(v[u], e);
-                const uint32_t i = static_cast<uint32_t>(base + elem_off(u, e));
-                const bool take = bits < end_bits || (bits == end_bits && i < end_idx);
-                c += (elem_off(u, e) < limit && take) ? 1u : 0u;
-            }
-        uint32_t pos = written + block_excl_scan(c, wave_tot);
-#pragma unroll
-        for (int u = 0; u < kU; ++u)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const uint32_t bits = lane_word(v[u], e);
-                const uint32_t i = static_cast<uint32_t>(base + elem_off(u, e));
-                const bool take = bits < end_bits || (bits == end_bits && i < end_idx);
-                if (elem_off(u, e) < limit && take) {
-                    if (pos < static_cast<uint32_t>(CAP)) cand[pos] = sort_key(bits, i);
-                    ++pos;
-                }
-            }
-        // total written so far: the last thread's end offset
-        if (tid == kSelectThreads - 1) red_u[0][0] = pos;
-        __syncthreads();
-        written = red_u[0][0];
-        __syncthreads();
-        advance(v, nx);
-    }
-    const uint32_t n = written < static_cast<uint32_t>(CAP) ? written : static_cast<uint32_t>(CAP);
-    uint32_t P = 1;
-    while (P < n) P <<= 1;
-    for (uint32_t i = n + tid; i < P; i += kSelectThreads) cand[i] = ~0ull;
-    __syncthreads();
+// Is key (bits, i) before the end of the range?  In the distance regime the
+// range ends at bits == hi; in the index regime (fix) it ends at (fv, hi).
+__device__ __forceinline__ bool before_end(uint32_t bits, uint32_t i, bool fix, uint32_t fv, uint32_t hi) {
+    return fix ? (bits < fv || (bits == fv && i < hi)) : bits < hi;
+}
 
-    // Bitonic sort of cand[0, P), ascending.
+// Ascending bitonic sort of cand[0, P) in LDS (P a power of two).
+__device__ __forceinline__ void lds_bitonic(uint64_t *cand, uint32_t P) {
+    const uint32_t tid = threadIdx.x;
     for (uint32_t k = 2; k <= P; k <<= 1) {
         for (uint32_t jj = k >> 1; jj > 0; jj >>= 1) {
-            for (uint32_t t = tid; t < P / 2; t += kSelectThreads) {
+            for (uint32_t t = tid; t < P / 2; t += kT) {
                 const uint32_t i = ((t & ~(jj - 1)) << 1) | (t & (jj - 1));
                 const uint32_t p = i | jj;
                 const uint64_t x = cand[i], y = cand[p];
@@ -371,10 +210,268 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(SelectArgs a, MixArgs
             __syncthreads();
         }
     }
+}
+
+// Ascending sort of the n <= PER * 1024 keys in cand[0, n), in place, by
+// buckets of their distance bits over [lo, lo + w): each key takes a slot in
+// its bucket with an LDS atomic, a block scan turns bucket sizes into bucket
+// starts, the keys are scattered to tmp, and each key's final place is its
+// bucket start plus its rank among the (few) keys of its bucket.  A bucket
+// holding many equal distances only costs time, never order.
+template <int PER>
+__device__ __forceinline__ void bucket_sort(uint64_t *cand, uint32_t n, uint32_t lo, uint32_t w, uint32_t *count,
+                                            uint32_t *start, uint64_t *tmp, Shared &sh) {
+    const int tid = threadIdx.x;
+    const int shift = range_shift(w > 1u ? w : 2u);
+    for (int i = tid; i < kSelectBins; i += kT) count[i] = 0u;
+    __syncthreads();
+    uint64_t key[PER];
+    uint32_t bin[PER], slot[PER];
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+        const uint32_t j = static_cast<uint32_t>(q * kT + tid);
+        key[q] = j < n ? cand[j] : ~0ull;
+        bin[q] = j < n ? ((static_cast<uint32_t>(key[q] >> 32) - lo) >> shift) : 0u;
+        if (bin[q] >= static_cast<uint32_t>(kSelectBins)) bin[q] = kSelectBins - 1;  // never for consistent input
+        slot[q] = j < n ? atomicAdd(&count[bin[q]], 1u) : 0u;
+    }
+    __syncthreads();
+    const uint32_t c0 = count[2 * tid], c1 = count[2 * tid + 1];
+    const uint32_t excl = block_excl_scan(c0 + c1, sh.wave_tot);
+    start[2 * tid] = excl;
+    start[2 * tid + 1] = excl + c0;
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < PER; ++q)
+        if (q * kT + tid < static_cast<int>(n)) tmp[start[bin[q]] + slot[q]] = key[q];
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+        if (q * kT + tid < static_cast<int>(n)) {
+            const uint32_t b0 = start[bin[q]], nb = count[bin[q]];
+            uint32_t rank = 0;
+            for (uint32_t i = 0; i < nb; ++i) rank += tmp[b0 + i] < key[q] ? 1u : 0u;
+            cand[b0 + rank] = key[q];
+        }
+    }
+    __syncthreads();
+}
+
+// ------------------------------------------------------------ general path
+
+__device__ __forceinline__ void load_batch(const float *drow, int64_t N, int64_t bb, uint4 (&v)[kU]) {
+    const int64_t base = bb * kBatch;
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+        const int64_t i = base + (static_cast<int64_t>(u) * kT + threadIdx.x) * 4;
+        v[u] = (i < N) ? *reinterpret_cast<const uint4 *>(drow + i) : make_uint4(0u, 0u, 0u, 0u);
+    }
+}
+
+__device__ __forceinline__ void next_batch(const float *drow, int64_t N, int64_t bb, int64_t nbatch, uint4 (&nx)[kU]) {
+    if (bb + 1 < nbatch) {
+        load_batch(drow, N, bb + 1, nx);
+    } else {
+#pragma unroll
+        for (int u = 0; u < kU; ++u) nx[u] = make_uint4(0u, 0u, 0u, 0u);
+    }
+}
+
+__device__ __forceinline__ void advance(uint4 (&v)[kU], const uint4 (&nx)[kU]) {
+#pragma unroll
+    for (int u = 0; u < kU; ++u) v[u] = nx[u];
+}
+
+// Select over a streamed row: on return cand[0, n) holds, sorted ascending,
+// every key before the end of the final range (n >= r_eff, n <= CAP); returns n.
+template <int CAP>
+__device__ uint32_t select_stream(const float *drow, int64_t N, uint32_t r_eff, uint32_t bmin, uint32_t bmax,
+                                  uint64_t *cand, uint32_t *hist, Shared &sh) {
+    const int tid = threadIdx.x;
+    const int64_t nbatch = (N + kBatch - 1) / kBatch;
+    uint4 v[kU], nx[kU];
+    if (tid == 0) {
+        sh.lo = bmin;
+        sh.hi = bmax + 1u;  // distances are >= +0, so bmax < 0x80000000
+        sh.below = 0u;
+        sh.cnt = static_cast<uint32_t>(N);
+    }
+    __syncthreads();
+    uint32_t lo = sh.lo, hi = sh.hi, below = sh.below, cnt = sh.cnt, fv = 0u;
+    bool fix = false;
+    for (int pass = 0; pass < 12 && below + cnt > static_cast<uint32_t>(CAP); ++pass) {
+        if (!fix && hi - lo == 1u) {  // one distance value left: order by index
+            fix = true;
+            fv = lo;
+            lo = 0u;
+            hi = static_cast<uint32_t>(N);
+        }
+        const uint32_t w = hi - lo;
+        const int shift = range_shift(w);
+        for (int i = tid; i < kSelectBins; i += kT) hist[i] = 0u;
+        if (tid == 0) { sh.found = 0u; sh.lo = lo; sh.hi = hi; }
+        __syncthreads();
+        load_batch(drow, N, 0, v);
+        for (int32_t bb = 0; bb < nbatch; ++bb) {
+            next_batch(drow, N, bb, nbatch, nx);
+            const int32_t base = bb * static_cast<int32_t>(kBatch) + 4 * tid;
+            const int32_t limit = static_cast<int32_t>(N) - base;
+#pragma unroll
+            for (int u = 0; u < kU; ++u)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const uint32_t bits = lane_word(v[u], e);
+                    const uint32_t off = (fix ? static_cast<uint32_t>(base + elem_off(u, e)) : bits) - lo;
+                    if (elem_off(u, e) < limit && off < w && (!fix || bits == fv)) atomicAdd(&hist[off >> shift], 1u);
+                }
+            advance(v, nx);
+        }
+        __syncthreads();
+        pick_bin(hist, r_eff - below, shift, sh);
+        const bool found = sh.found != 0u;
+        lo = sh.lo; hi = sh.hi; below = sh.below; cnt = sh.cnt;
+        __syncthreads();
+        if (!found) break;
+    }
+
+    // Compaction of every key before the end of the range.
+    uint32_t written = 0;
+    load_batch(drow, N, 0, v);
+    for (int32_t bb = 0; bb < nbatch; ++bb) {
+        next_batch(drow, N, bb, nbatch, nx);
+        const int32_t base = bb * static_cast<int32_t>(kBatch) + 4 * tid;
+        const int32_t limit = static_cast<int32_t>(N) - base;
+        uint32_t c = 0;
+#pragma unroll
+        for (int u = 0; u < kU; ++u)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const uint32_t i = static_cast<uint32_t>(base + elem_off(u, e));
+                c += (elem_off(u, e) < limit && before_end(lane_word(v[u], e), i, fix, fv, hi)) ? 1u : 0u;
+            }
+        uint32_t pos = written + block_excl_scan(c, sh.wave_tot);
+#pragma unroll
+        for (int u = 0; u < kU; ++u)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const uint32_t bits = lane_word(v[u], e);
+                const uint32_t i = static_cast<uint32_t>(base + elem_off(u, e));
+                if (elem_off(u, e) < limit && before_end(bits, i, fix, fv, hi)) {
+                    if (pos < static_cast<uint32_t>(CAP)) cand[pos] = sort_key(bits, i);
+                    ++pos;
+                }
+            }
+        if (tid == kT - 1) sh.total = pos;  // the last thread's end offset
+        __syncthreads();
+        written = sh.total;
+        __syncthreads();
+        advance(v, nx);
+    }
+    const uint32_t n = written < static_cast<uint32_t>(CAP) ? written : static_cast<uint32_t>(CAP);
+    uint32_t P = 1;
+    while (P < n) P <<= 1;
+    for (uint32_t i = n + tid; i < P; i += kT) cand[i] = ~0ull;
+    __syncthreads();
+    lds_bitonic(cand, P);
+    return n;
+}
+
+// ------------------------------------------------------------------ mixture
+
+__device__ __forceinline__ bool mix_vec4(const MixArgs &m, int64_t b) {
+    return (m.V % 4 == 0) &&
+           ((reinterpret_cast<uintptr_t>(m.p_lm + b * m.V) | reinterpret_cast<uintptr_t>(m.p_m + b * m.V)) & 15u) == 0;
+}
+
+// This thread's float4s of the p_LM tile starting at v0 (16-byte path only).
+template <int NV4>
+__device__ __forceinline__ void mix_prefetch(const MixArgs &m, int64_t b, int64_t v0, float4 (&pre)[NV4]) {
+    const int64_t nv = (m.V - v0 < static_cast<int64_t>(NV4) * 4 * kT) ? m.V - v0 : static_cast<int64_t>(NV4) * 4 * kT;
+    const bool vec4 = mix_vec4(m, b);
+    const float4 *src = reinterpret_cast<const float4 *>(m.p_lm + b * m.V + v0);
+#pragma unroll
+    for (int q = 0; q < NV4; ++q) {
+        const int64_t i = static_cast<int64_t>(q) * kT + threadIdx.x;
+        pre[q] = (vec4 && i < nv / 4) ? src[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+}
+
+// p_M row b: weights wj (unnormalised softmax terms, sum z) are scatter-added
+// onto their tokens tok (-1: none) one vocabulary tile of TILE entries at a
+// time in LDS; each tile's p_LM slice sits in registers (prefetched by the
+// caller for the first tile when `first` is given) and is mixed with 16-byte
+// accesses.
+template <int PER, int TILE>
+__device__ __forceinline__ void mix_row(const float (&wj)[PER], const int32_t (&tok)[PER], float z, const MixArgs &m,
+                                        int64_t b, float *acc, const float4 (*first)[TILE / 4 / kT] = nullptr) {
+    constexpr int kV4 = TILE / 4 / kT;  // float4 per thread per tile
+    const int tid = threadIdx.x;
+    const float lam = m.lambda;
+    const float scale = (1.0f - lam) / z;
+    const float *plm = m.p_lm + b * m.V;
+    float *pm = m.p_m + b * m.V;
+    const bool vec4 = mix_vec4(m, b);
+    for (int64_t v0 = 0; v0 < m.V; v0 += TILE) {
+        const int64_t nv = (m.V - v0 < TILE) ? m.V - v0 : TILE;
+        float4 pre[kV4];
+        if (v0 == 0 && first != nullptr) {
+#pragma unroll
+            for (int q = 0; q < kV4; ++q) pre[q] = (*first)[q];
+        } else {
+            mix_prefetch(m, b, v0, pre);
+        }
+        for (int i = tid; i < TILE / 4; i += kT) reinterpret_cast<float4 *>(acc)[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+        __syncthreads();
+#pragma unroll
+        for (int q = 0; q < PER; ++q)
+            if (tok[q] >= v0 && tok[q] < v0 + nv) atomicAdd(&acc[tok[q] - v0], wj[q]);
+        __syncthreads();
+        if (vec4) {
+            float4 *dst = reinterpret_cast<float4 *>(pm + v0);
+#pragma unroll
+            for (int q = 0; q < kV4; ++q) {
+                const int64_t i = static_cast<int64_t>(q) * kT + tid;
+                if (i < nv / 4) {
+                    const float4 a4 = reinterpret_cast<const float4 *>(acc)[i];
+                    float4 o;
+                    o.x = fmaf(lam, pre[q].x, a4.x * scale);
+                    o.y = fmaf(lam, pre[q].y, a4.y * scale);
+                    o.z = fmaf(lam, pre[q].z, a4.z * scale);
+                    o.w = fmaf(lam, pre[q].w, a4.w * scale);
+                    dst[i] = o;
+                }
+            }
+        } else {
+            for (int64_t i = tid; i < nv; i += kT) pm[v0 + i] = fmaf(lam, plm[v0 + i], acc[i] * scale);
+        }
+        __syncthreads();
+    }
+}
+
+// ------------------------------------------------------------------ kernels
+
+// General path: any row length, r <= KNNLM_MAX_R.
+template <int CAP, bool MIX>
+__global__ __launch_bounds__(kT) void k_select(SelectArgs a, MixArgs m) {
+    __shared__ uint32_t hist[kSelectBins];
+    __shared__ uint64_t cand[CAP];
+    __shared__ __align__(16) float acc[MIX ? kVocabTile : 4];
+    __shared__ Shared sh;
+
+    const int tid = threadIdx.x;
+    const int64_t b = blockIdx.x;
+    const int64_t s = set_of_query(a.query_offsets, a.S, b);
+    const int64_t k0 = a.key_offsets[s];
+    int64_t N = a.key_offsets[s + 1] - k0;
+    if (N > a.ld) N = a.ld;
+    const uint32_t r_eff = static_cast<uint32_t>(N < a.r ? N : a.r);
+    uint32_t bmin, bmax;
+    row_range(a, b, N, bmin, bmax, sh);
+    const uint32_t n = select_stream<CAP>(a.dist + b * a.ld, N, r_eff, bmin, bmax, cand, hist, sh);
 
     int32_t *out_ids = a.ids + b * a.r;
     float *out_d = a.dists + b * a.r;
-    for (int j = tid; j < a.r; j += kSelectThreads) {
+    for (int j = tid; j < a.r; j += kT) {
         if (static_cast<uint32_t>(j) < r_eff && static_cast<uint32_t>(j) < n) {
             const uint64_t key = cand[j];
             out_ids[j] = static_cast<int32_t>(key & 0xffffffffu);
@@ -384,35 +481,155 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(SelectArgs a, MixArgs
             out_d[j] = __builtin_huge_valf();
         }
     }
-    if (!MIX) return;
-
-    // ---- mixture over the r neighbours now sorted in cand[0, r_eff)
-    const uint32_t rn = r_eff < n ? r_eff : n;
-    const float dmin = rn > 0 ? __uint_as_float(static_cast<uint32_t>(cand[0] >> 32)) : 0.0f;
-    float wj[kPer];
-    int32_t tok[kPer];
-    float zpart = 0.0f;
+    if constexpr (MIX) {
+        const uint32_t rn = r_eff < n ? r_eff : n;
+        const float dmin = rn > 0 ? __uint_as_float(static_cast<uint32_t>(cand[0] >> 32)) : 0.0f;
+        float wj[kPer];
+        int32_t tok[kPer];
+        float zpart = 0.0f;
 #pragma unroll
-    for (int q = 0; q < kPer; ++q) {
-        const uint32_t j = static_cast<uint32_t>(q * kSelectThreads + tid);
-        tok[q] = -1;
-        wj[q] = 0.0f;
-        if (j < rn) {
-            const uint64_t key = cand[j];
-            const int32_t id = static_cast<int32_t>(key & 0xffffffffu);
-            const float dj = __uint_as_float(static_cast<uint32_t>(key >> 32));
-            wj[q] = expf(-m.mu * (dj - dmin));
-            zpart += wj[q];
-            tok[q] = m.values[k0 + id];
+        for (int q = 0; q < kPer; ++q) {
+            const uint32_t j = static_cast<uint32_t>(q * kT + tid);
+            tok[q] = -1;
+            wj[q] = 0.0f;
+            if (j < rn) {
+                const uint64_t key = cand[j];
+                wj[q] = expf(-m.mu * (__uint_as_float(static_cast<uint32_t>(key >> 32)) - dmin));
+                zpart += wj[q];
+                tok[q] = m.values[k0 + static_cast<int32_t>(key & 0xffffffffu)];
+            }
+        }
+        const float z = block_sum(zpart, sh.red_f);
+        mix_row<kPer, kVocabTile>(wj, tok, z, m, b, acc);
+    }
+}
+
+// Fast path: rows of at most kFastMaxN keys (ld <= kFastMaxN), r <= 1024.
+template <bool MIX>
+__global__ __launch_bounds__(kT) void k_select_fast(SelectArgs a, MixArgs m) {
+    constexpr int kSelBytes = 2 * kFastCap * 8 + 2 * kSelectBins * 4;
+    constexpr int kSmem = (MIX && kVocabTileFast * 4 > kSelBytes) ? kVocabTileFast * 4 : kSelBytes;
+    constexpr int kPre = MIX ? kVocabTileFast / 4 / kT : 1;
+    __shared__ __align__(16) unsigned char smem[kSmem];
+    __shared__ Shared sh;
+    uint64_t *cand = reinterpret_cast<uint64_t *>(smem);                                   // [kFastCap]
+    uint64_t *tmp = reinterpret_cast<uint64_t *>(smem + kFastCap * 8);                     // [kFastCap]
+    uint32_t *hist = reinterpret_cast<uint32_t *>(smem + 2 * kFastCap * 8);                // [2 * kSelectBins]
+    float *acc = reinterpret_cast<float *>(smem);  // mixture phase, after the keys are in registers
+
+    const int tid = threadIdx.x;
+    const int64_t b = blockIdx.x;
+    const int64_t s = set_of_query(a.query_offsets, a.S, b);
+    const int64_t k0 = a.key_offsets[s];
+    int64_t N = a.key_offsets[s + 1] - k0;
+    if (N > a.ld) N = a.ld;
+    if (N > kFastMaxN) N = kFastMaxN;  // the host launches this kernel only when ld <= kFastMaxN
+    const uint32_t r_eff = static_cast<uint32_t>(N < a.r ? N : a.r);
+    const float *drow = a.dist + b * a.ld;
+
+    // The whole row into registers: element (u, e) is key 4 * tid + u * 4096 + e.
+    uint4 v[kFastU];
+#pragma unroll
+    for (int u = 0; u < kFastU; ++u) {
+        const int64_t i = (static_cast<int64_t>(u) * kT + tid) * 4;
+        v[u] = (i < N) ? *reinterpret_cast<const uint4 *>(drow + i) : make_uint4(0u, 0u, 0u, 0u);
+    }
+    const int32_t limit = static_cast<int32_t>(N) - 4 * tid;
+    uint32_t bmin, bmax;
+    row_range(a, b, N, bmin, bmax, sh);
+
+    // Threshold on the distance bits: every key if they fit, else from a
+    // histogram of one key per thread, sampled across the whole row.
+    uint32_t thr = bmax + 1u;
+    if (N > kFastCap) {
+        const int us = tid & (kFastU - 1), es = (tid >> 4) & 3;
+        uint32_t sbits = 0u;
+#pragma unroll
+        for (int u = 0; u < kFastU; ++u)
+            if (u == us) sbits = lane_word(v[u], es);
+        const bool sval = elem_off(us, es) < limit;
+        for (int i = tid; i < kSelectBins; i += kT) hist[i] = 0u;
+        __syncthreads();
+        const uint32_t w = bmax + 1u - bmin;
+        const int shift = range_shift(w);
+        if (sval && sbits - bmin < w) atomicAdd(&hist[(sbits - bmin) >> shift], 1u);
+        const uint64_t votes = __ballot(sval);  // every lane votes
+        if ((tid & (kWave - 1)) == 0) sh.red_u[0][tid / kWave] = static_cast<uint32_t>(__popcll(votes));
+        __syncthreads();
+        uint32_t ns = 0;
+#pragma unroll
+        for (int wv = 0; wv < kNumWaves; ++wv) ns += sh.red_u[0][wv];
+        // Sample rank aiming at about r + 4 sd + 4 samples' worth of keys: the
+        // count of keys below the threshold then lies in [r, kFastCap] with
+        // overwhelming probability; otherwise the general path runs.
+        const float k0f = ceilf(static_cast<float>(r_eff) * static_cast<float>(ns) / static_cast<float>(N));
+        const uint32_t ks = static_cast<uint32_t>(k0f + ceilf(4.0f * sqrtf(k0f)) + 4.0f);
+        if (ks < ns) {
+            if (tid == 0) { sh.lo = bmin; sh.hi = bmax + 1u; sh.below = 0u; sh.cnt = ns; }
+            __syncthreads();
+            pick_bin(hist, ks, shift, sh);
+            thr = sh.hi;  // bin end: at least ks samples lie below it
+            __syncthreads();
         }
     }
-    const float z = block_sum(zpart, red_f);
-    mix_row(wj, tok, z, m, b, acc);
+
+    // One compaction pass of the keys below the threshold.
+    uint32_t c = 0;
+#pragma unroll
+    for (int u = 0; u < kFastU; ++u)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) c += (elem_off(u, e) < limit && lane_word(v[u], e) < thr) ? 1u : 0u;
+    uint32_t pos = block_excl_scan(c, sh.wave_tot);
+    if (tid == kT - 1) sh.total = pos + c;
+    __syncthreads();
+    const uint32_t C = sh.total;
+    const bool fast = C >= r_eff && C <= static_cast<uint32_t>(kFastCap);
+    if (c > 0 && pos + c <= static_cast<uint32_t>(kFastCap)) {
+#pragma unroll
+        for (int u = 0; u < kFastU; ++u)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if (elem_off(u, e) < limit && lane_word(v[u], e) < thr)
+                    cand[pos++] = sort_key(lane_word(v[u], e), static_cast<uint32_t>(4 * tid + elem_off(u, e)));
+    }
+    __syncthreads();
+    uint64_t x = ~0ull;
+    if (fast) {
+        // Sort every candidate (all keys below the threshold); the first r are pi.
+        bucket_sort<kFastCap / kT>(cand, C, bmin, thr - bmin, hist, hist + kSelectBins, tmp, sh);
+        x = static_cast<uint32_t>(tid) < r_eff ? cand[tid] : ~0ull;
+    } else {
+        // The sample misjudged the count: select over the streamed row.
+        const uint32_t n = select_stream<kFastCap>(drow, N, r_eff, bmin, bmax, cand, hist, sh);
+        x = (static_cast<uint32_t>(tid) < r_eff && static_cast<uint32_t>(tid) < n) ? cand[tid] : ~0ull;
+    }
+    __syncthreads();
+
+    // Start fetching this query's p_LM row while the neighbours are written out.
+    float4 pre[kPre];
+    if constexpr (MIX) mix_prefetch(m, b, 0, pre);
+
+    // Thread t holds the t-th nearest key (t < r_eff).
+    if (tid < a.r) {
+        const bool ok = static_cast<uint32_t>(tid) < r_eff;
+        a.ids[b * a.r + tid] = ok ? static_cast<int32_t>(x & 0xffffffffu) : -1;
+        a.dists[b * a.r + tid] = ok ? __uint_as_float(static_cast<uint32_t>(x >> 32)) : __builtin_huge_valf();
+    }
+    if constexpr (MIX) {
+        const bool ok = static_cast<uint32_t>(tid) < r_eff;
+        int32_t tok[1] = {ok ? m.values[k0 + static_cast<int32_t>(x & 0xffffffffu)] : -1};
+        const float dj = __uint_as_float(static_cast<uint32_t>(x >> 32));
+        if (tid == 0) sh.dmin = ok ? dj : 0.0f;
+        __syncthreads();
+        float wj[1] = {ok ? expf(-m.mu * (dj - sh.dmin)) : 0.0f};
+        const float z = block_sum(wj[0], sh.red_f);
+        mix_row<1, kVocabTileFast>(wj, tok, z, m, b, acc, &pre);
+    }
 }
 
 // Standalone mixture on caller-given neighbours (any order): one workgroup per query.
-__global__ __launch_bounds__(kSelectThreads) void k_mix(MixArgs m) {
-    __shared__ float acc[kVocabTile];
+__global__ __launch_bounds__(kT) void k_mix(MixArgs m) {
+    __shared__ __align__(16) float acc[kVocabTile];
     __shared__ float red_f[kNumWaves];
     const int tid = threadIdx.x;
     const int64_t b = blockIdx.x;
@@ -424,7 +641,7 @@ __global__ __launch_bounds__(kSelectThreads) void k_mix(MixArgs m) {
     float dmin = __builtin_huge_valf();
 #pragma unroll
     for (int q = 0; q < kPer; ++q) {
-        const int j = q * kSelectThreads + tid;
+        const int j = q * kT + tid;
         dj[q] = j < m.r ? m.dists[b * m.r + j] : __builtin_huge_valf();
         id[q] = j < m.r ? m.ids[b * m.r + j] : -1;
         dmin = fminf(dmin, dj[q]);
@@ -435,32 +652,32 @@ __global__ __launch_bounds__(kSelectThreads) void k_mix(MixArgs m) {
     float zpart = 0.0f;
 #pragma unroll
     for (int q = 0; q < kPer; ++q) {
-        const int j = q * kSelectThreads + tid;
+        const int j = q * kT + tid;
         wj[q] = j < m.r ? expf(-m.mu * (dj[q] - dmin)) : 0.0f;
         zpart += wj[q];
         tok[q] = (j < m.r && id[q] >= 0 && id[q] < N) ? m.values[k0 + id[q]] : -1;
     }
     const float z = block_sum(zpart, red_f);
-    mix_row(wj, tok, z, m, b, acc);
-}
-
-template <int CAP, bool MIX>
-hipError_t launch_cap(const SelectArgs &a, const MixArgs &m, dim3 grid, hipStream_t st) {
-    hipLaunchKernelGGL((k_select<CAP, MIX>), grid, dim3(kSelectThreads), 0, st, a, m);
-    return hipGetLastError();
+    mix_row<kPer, kVocabTile>(wj, tok, z, m, b, acc);
 }
 
 template <bool MIX>
 hipError_t launch_sel(const SelectArgs &a, const MixArgs &m, int64_t B, hipStream_t st) {
     if (B == 0) return hipSuccess;
     if (B > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-    const dim3 grid(static_cast<unsigned>(B));
+    if (a.tile_min == nullptr || a.tile_max == nullptr) return hipErrorInvalidValue;
+    const dim3 grid(static_cast<unsigned>(B)), block(kT);
+    if (a.ld <= kFastMaxN && a.r <= kT) {
+        hipLaunchKernelGGL((k_select_fast<MIX>), grid, block, 0, st, a, m);
+        return hipGetLastError();
+    }
     switch (select_capacity(a.r)) {
-    case 2048: return launch_cap<2048, MIX>(a, m, grid, st);
-    case 4096: return launch_cap<4096, MIX>(a, m, grid, st);
-    case 8192: return launch_cap<8192, MIX>(a, m, grid, st);
+    case 2048: hipLaunchKernelGGL((k_select<2048, MIX>), grid, block, 0, st, a, m); break;
+    case 4096: hipLaunchKernelGGL((k_select<4096, MIX>), grid, block, 0, st, a, m); break;
+    case 8192: hipLaunchKernelGGL((k_select<8192, MIX>), grid, block, 0, st, a, m); break;
     default: return hipErrorInvalidValue;
     }
+    return hipGetLastError();
 }
 
 }  // namespace
@@ -485,7 +702,7 @@ hipError_t launch_select_mix(const SelectArgs &args, const MixArgs &mix, int64_t
 hipError_t launch_mix(const MixArgs &args, int64_t B, hipStream_t stream) {
     if (B == 0) return hipSuccess;
     if (B > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL(k_mix, dim3(static_cast<unsigned>(B)), dim3(kSelectThreads), 0, stream, args);
+    hipLaunchKernelGGL(k_mix, dim3(static_cast<unsigned>(B)), dim3(kT), 0, stream, args);
     return hipGetLastError();
 }
 
