@@ -297,3 +297,25 @@ def test_full_size_workloads(name, sample):
     assert rep.ok(), rep.failures[:5]
     del w, p_m, ids, dists
     _free()
+
+
+def test_adversarial_row_takes_the_streamed_path():
+    """Keys at the positions the fast path samples are far away and every other
+    key sits on the query: the sampled threshold then keeps more than the LDS
+    capacity, the general streamed path takes over, and the answer (ties broken
+    by index) is still exact."""
+    _say("adversarial sample")
+    n, d, r = 65536, 16, 1000
+    t = np.arange(1024)
+    sampled = ((t & 15) * 4096 + 4 * t + ((t >> 4) & 3))
+    k = np.zeros((n, d), np.float32)
+    k[sampled] = 3.0
+    q = np.zeros((1, d), np.float32)
+    vals = (np.arange(n) % 50).astype(np.int32)
+    p_lm = np.full((1, 50), 0.02, np.float32)
+    tq, tk, tv, tko, tqo, tp = _tensor_inputs(q, k, vals, p_lm, [0, n], [0, 1], torch.bfloat16)
+    p_m, ids, dists = knn.mixture(tq, tk, tv, tko, tqo, tp, r, 0.1, 0.5)
+    torch.cuda.synchronize()
+    expect = np.setdiff1d(np.arange(n), sampled)[:r]
+    assert ids[0].cpu().numpy().tolist() == expect.tolist()
+    assert torch.all(dists == 0.0)
