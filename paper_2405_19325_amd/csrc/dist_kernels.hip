@@ -376,12 +376,44 @@ bool vector_path_ok(int64_t d, knn_dtype dtype, const void *queries, const void 
 
 }  // namespace
 
+bool mfma_shape(int64_t d, knn_dtype dtype, int64_t max_queries) {
+    return (dtype == KNN_BF16 || dtype == KNN_F16) && d % 8 == 0 && max_queries >= kMfmaMinQueries;
+}
+
+// Key rows per distance workgroup.  Streaming path: about 1 MiB of keys, fewer
+// when the launch would otherwise have under 512 workgroups (two per CU,
+// measured best).  Matrix-core path: one 256-key pass.  A multiple of 8 rows.
+// Depends on sizes only, so the workspace size does not depend on pointers.
+int dist_tile_rows(int64_t d, knn_dtype dtype, int64_t S, int64_t max_keys, int64_t max_queries) {
+    if (mfma_shape(d, dtype, max_queries)) return mfma_keys_per_pass();
+    const int64_t step = 8;
+    const int64_t row_bytes = d * elem_bytes(dtype);
+    int64_t rpt = (1024 * 1024) / (row_bytes > 0 ? row_bytes : 1);
+    if (rpt > 4096) rpt = 4096;
+    rpt = (rpt + step - 1) / step * step;
+    if (rpt < step) rpt = step;
+    while (rpt > step && S * ((max_keys + rpt - 1) / rpt) < 512) rpt = (rpt / 2 + step - 1) / step * step;
+    return static_cast<int>(rpt);
+}
+
 DistPlan plan_distances(int64_t d, knn_dtype dtype, int64_t max_queries, const void *queries,
                         const void *keys) {
     DistPlan p{};
     const int vec = vec_elems(dtype);
     p.vec = vector_path_ok(d, dtype, queries, keys);
     const int64_t mq = max_queries < 1 ? 1 : max_queries;
+    p.mfma = p.vec && mfma_shape(d, dtype, max_queries);
+    if (p.mfma) {
+        const int64_t per = mq < 128 ? mq : 128;
+        int blocks = 1;
+        while (blocks * 16 < per) blocks <<= 1;
+        p.mq = blocks;
+        p.cpl = 0;
+        p.nq = blocks * 16;
+        p.rows = 1;
+        p.groups = (mq + p.nq - 1) / p.nq;
+        return p;
+    }
     if (p.vec) {
         p.cpl = pow2_at_least((d / vec + kWave - 1) / kWave);
         int nq = 8;
@@ -404,6 +436,7 @@ DistPlan plan_distances(int64_t d, knn_dtype dtype, int64_t max_queries, const v
 
 hipError_t launch_distances(const DistPlan &plan, knn_dtype dtype, const DistArgs &args, int64_t S,
                             hipStream_t stream) {
+    if (plan.mfma) return launch_distances_mfma(plan.mq, dtype, args, S, plan.groups, stream);
     const int64_t nblocks = S * plan.tiles_per_set;
     if (nblocks > 0x7fffffffLL || plan.groups > 65535) return hipErrorInvalidConfiguration;
     const dim3 grid(static_cast<unsigned>(nblocks), static_cast<unsigned>(plan.groups));

@@ -17,22 +17,6 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 bool valid_dtype(knn_dtype t) { return t == KNN_F32 || t == KNN_BF16 || t == KNN_F16; }
 
-// Key rows per distance workgroup: about 1 MiB of keys, fewer when the launch
-// would otherwise have under 512 workgroups (two per CU: measured best for
-// the streaming kernel).  A multiple of 8 rows (4 waves x up to 2 rows per
-// iteration).  Depends on sizes only, so the workspace size does not depend on
-// pointer alignment.
-int tile_rows(int64_t d, knn_dtype dtype, int64_t S, int64_t max_keys) {
-    const int64_t step = 8;
-    const int64_t row_bytes = d * elem_bytes(dtype);
-    int64_t rpt = (1024 * 1024) / (row_bytes > 0 ? row_bytes : 1);
-    if (rpt > 4096) rpt = 4096;
-    rpt = (rpt + step - 1) / step * step;
-    if (rpt < step) rpt = step;
-    while (rpt > step && S * ((max_keys + rpt - 1) / rpt) < 512) rpt = (rpt / 2 + step - 1) / step * step;
-    return static_cast<int>(rpt);
-}
-
 struct Layout {
     int rows_per_tile;
     int64_t tiles_per_set;
@@ -40,9 +24,9 @@ struct Layout {
     size_t off_dist, off_tmin, off_tmax, total;
 };
 
-Layout layout(int64_t B, int64_t d, int64_t S, int64_t max_keys, knn_dtype dtype) {
+Layout layout(int64_t B, int64_t d, int64_t S, int64_t max_keys, int64_t max_queries, knn_dtype dtype) {
     Layout L{};
-    L.rows_per_tile = tile_rows(d, dtype, S, max_keys);
+    L.rows_per_tile = dist_tile_rows(d, dtype, S, max_keys, max_queries);
     L.tiles_per_set = (max_keys + L.rows_per_tile - 1) / L.rows_per_tile;
     if (L.tiles_per_set < 1) L.tiles_per_set = 1;
     L.ld = L.tiles_per_set * L.rows_per_tile;
@@ -69,7 +53,7 @@ knn_status check_sizes(int64_t B, int64_t d, int64_t V, int64_t S, int64_t total
     if (need_vocab && V > 0x7fffffffLL) return KNN_ERR_UNSUPPORTED;
     if (d > (int64_t(1) << 40) / elem_bytes(dtype)) return KNN_ERR_UNSUPPORTED;
     if (r > min_keys) return KNN_ERR_R_EXCEEDS_N;
-    const Layout L = layout(B, d, S, max_keys, dtype);
+    const Layout L = layout(B, d, S, max_keys, max_queries, dtype);
     if (S * L.tiles_per_set > 0x7fffffffLL) return KNN_ERR_UNSUPPORTED;
     if (max_queries > 65535) return KNN_ERR_UNSUPPORTED;  // query groups per set on grid.y
     return KNN_OK;
@@ -117,7 +101,7 @@ knn_status validate_part(const Call &c, int part) {
     if (dist || sel) {
         if (!c.workspace) return KNN_ERR_WORKSPACE;
         if (reinterpret_cast<uintptr_t>(c.workspace) % kAlign) return KNN_ERR_WORKSPACE;
-        const Layout L = layout(c.B, c.d, c.S, c.max_keys, c.dtype);
+        const Layout L = layout(c.B, c.d, c.S, c.max_keys, c.max_queries, c.dtype);
         if (c.workspace_bytes < L.total) return KNN_ERR_WORKSPACE;
     }
     return KNN_OK;
@@ -141,7 +125,7 @@ MixArgs mix_args(const Call &c) {
 }
 
 knn_status run_part(const Call &c, int part, hipStream_t stream) {
-    const Layout L = layout(c.B, c.d, c.S, c.max_keys, c.dtype);
+    const Layout L = layout(c.B, c.d, c.S, c.max_keys, c.max_queries, c.dtype);
     char *ws = static_cast<char *>(c.workspace);
     float *dist = ws ? reinterpret_cast<float *>(ws + L.off_dist) : nullptr;
     float *tmin = ws ? reinterpret_cast<float *>(ws + L.off_tmin) : nullptr;
@@ -266,7 +250,7 @@ size_t knn_lm_mixture_workspace_size(int64_t B, int64_t d, int64_t V, int64_t S,
     if (check_sizes(B, d, V, S, total_keys, min_keys_per_set, max_keys_per_set, max_queries_per_set, dtype, r,
                     true) != KNN_OK)
         return 0;
-    return layout(B, d, S, max_keys_per_set, dtype).total;
+    return layout(B, d, S, max_keys_per_set, max_queries_per_set, dtype).total;
 }
 
 knn_status knn_lm_mixture_validate(const void *queries, const void *keys, const int32_t *values,
@@ -296,7 +280,7 @@ knn_status knn_distances(const void *queries, const void *keys, const float *key
     if (!valid_dtype(dtype) || ld_out < max_keys_per_set) return KNN_ERR_INVALID_ARG;
     if (B > 0x7fffffffLL || max_keys_per_set > 0x7fffffffLL || max_queries_per_set > 65535) return KNN_ERR_UNSUPPORTED;
     DistPlan p = plan_distances(d, dtype, max_queries_per_set, queries, keys);
-    p.rows_per_tile = tile_rows(d, dtype, S, max_keys_per_set);
+    p.rows_per_tile = dist_tile_rows(d, dtype, S, max_keys_per_set, max_queries_per_set);
     p.tiles_per_set = (max_keys_per_set + p.rows_per_tile - 1) / p.rows_per_tile;
     if (S * p.tiles_per_set > 0x7fffffffLL || p.groups > 65535) return KNN_ERR_UNSUPPORTED;
     DistArgs a{};

@@ -20,6 +20,8 @@ inline int vec_elems(knn_dtype t) { return 16 / elem_bytes(t); }
 
 // How the distance kernel covers the (set, key tile, query group) space.
 struct DistPlan {
+    bool mfma;              // query batches: q.k on the matrix cores (16-bit elements, >= 16 queries per set)
+    int mq;                 // MFMA path: 16-query blocks per workgroup (1, 2, 4 or 8)
     bool vec;               // 16-byte loads (d % VEC == 0, aligned rows) vs element loads
     int cpl;                // chunks per lane (vector path), power of two <= kMaxCplVec
     int nq;                 // queries per workgroup (1, 2, 4 or 8)
@@ -77,8 +79,17 @@ struct MixArgs {
 DistPlan plan_distances(int64_t d, knn_dtype dtype, int64_t max_queries, const void *queries,
                         const void *keys);
 
+// The matrix-core path serves 16-bit keys with d % 8 == 0 when at least this
+// many queries share a key set.
+constexpr int kMfmaMinQueries = 16;
+bool mfma_shape(int64_t d, knn_dtype dtype, int64_t max_queries);
+int mfma_keys_per_pass();
+int dist_tile_rows(int64_t d, knn_dtype dtype, int64_t S, int64_t max_keys, int64_t max_queries);
+
 hipError_t launch_distances(const DistPlan &plan, knn_dtype dtype, const DistArgs &args, int64_t S,
                             hipStream_t stream);
+hipError_t launch_distances_mfma(int mq, knn_dtype dtype, const DistArgs &args, int64_t S, int64_t groups,
+                                 hipStream_t stream);
 hipError_t launch_key_sqnorms(const void *keys, int64_t n, int64_t d, knn_dtype dtype, float *out,
                               hipStream_t stream);
 int select_capacity(int r);

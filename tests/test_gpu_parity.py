@@ -319,3 +319,51 @@ def test_adversarial_row_takes_the_streamed_path():
     expect = np.setdiff1d(np.arange(n), sampled)[:r]
     assert ids[0].cpu().numpy().tolist() == expect.tolist()
     assert torch.all(dists == 0.0)
+
+
+# ------------------------------------------------- matrix-core (query batch) path
+
+MFMA = [
+    ("mfma-16q-bf16", gen.scaled(gen.config("specverify_seq"), B=16, S=1, n_keys=5000, d=1024,
+                                 mu=1 / 32), 31),
+    ("mfma-40q-2sets-f16-d1000", gen.scaled(gen.config("specverify_static"), B=80, S=2, n_keys=(3000, 4500), d=1000,
+                                            query_mode="iid", mu=1 / math.sqrt(1000)), 32),
+    ("mfma-130q-bf16-groups", gen.scaled(gen.config("specverify_seq"), B=130, S=1, n_keys=3001, d=256, mu=1 / 16,
+                                         r=700), 33),
+    ("mfma-ragged-sets", gen.scaled(gen.config("specverify_seq"), B=51, S=3, n_keys=(2048, 1300, 4100), d=512,
+                                    mu=1 / math.sqrt(512), r=512), 34),
+    ("mfma-d8192", gen.scaled(gen.config("specverify_seq"), B=16, S=1, n_keys=1500, r=256), 35),
+]
+
+
+@pytest.mark.parametrize("name,spec,seed", MFMA, ids=[m[0] for m in MFMA])
+def test_matrix_core_workloads(name, spec, seed):
+    _say(f"workload {name}")
+    w = gen.make(spec, seed, device="cuda")
+    p_m, ids, dists = _run(w)
+    rep = parity.check_workload(w, p_m, ids, dists)
+    _say(f"{name}: {rep.summary()}")
+    assert rep.ok(), rep.failures[:5]
+    norms = knn.key_sqnorms(w.keys)
+    p_m2, ids2, dists2 = _run(w, key_sqnorms=norms)
+    rep2 = parity.check_workload(w, p_m2, ids2, dists2)
+    assert rep2.ok(), rep2.failures[:5]
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float16])
+def test_matrix_core_exact_integers(dtype):
+    _say(f"matrix-core exact integers {dtype}")
+    rng = np.random.default_rng(41)
+    B, n, d, r = 37, 3000, 64, 300
+    q = rng.integers(-4, 5, (B, d)).astype(np.float32)
+    k = rng.integers(-4, 5, (n, d)).astype(np.float32)
+    vals = rng.integers(0, 500, n).astype(np.int32)
+    p_lm = np.full((B, 500), 1 / 500, np.float32)
+    tq, tk, tv, tko, tqo, tp = _tensor_inputs(q, k, vals, p_lm, [0, n], [0, B], dtype)
+    p_m, ids, dists = knn.mixture(tq, tk, tv, tko, tqo, tp, r, 0.05, 0.25)
+    torch.cuda.synchronize()
+    qh, dt = oracle.host_elements(tq)
+    kh, _ = oracle.host_elements(tk)
+    oids, odists = oracle.select(qh, kh, dt, np.array([0, n]), np.array([0, B]), r)
+    np.testing.assert_array_equal(ids.cpu().numpy(), oids)
+    np.testing.assert_array_equal(dists.cpu().numpy().astype(np.float64), odists)
