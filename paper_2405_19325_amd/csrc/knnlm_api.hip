@@ -21,10 +21,11 @@ struct Layout {
     int rows_per_tile;
     int64_t tiles_per_set;
     int64_t ld;  // distance row stride = tiles_per_set * rows_per_tile
-    size_t off_dist, off_tmin, off_tmax, total;
+    int split_parts;  // > 0: the select runs split over parts (candidate lists and counts below)
+    size_t off_dist, off_tmin, off_tmax, off_cand, off_count, off_thr, total;
 };
 
-Layout layout(int64_t B, int64_t d, int64_t S, int64_t max_keys, int64_t max_queries, knn_dtype dtype) {
+Layout layout(int64_t B, int64_t d, int64_t S, int64_t max_keys, int64_t max_queries, knn_dtype dtype, int32_t r) {
     Layout L{};
     L.rows_per_tile = dist_tile_rows(d, dtype, S, max_keys, max_queries);
     L.tiles_per_set = (max_keys + L.rows_per_tile - 1) / L.rows_per_tile;
@@ -33,7 +34,12 @@ Layout layout(int64_t B, int64_t d, int64_t S, int64_t max_keys, int64_t max_que
     L.off_dist = 0;
     L.off_tmin = align_up(L.off_dist + sizeof(float) * static_cast<size_t>(B) * static_cast<size_t>(L.ld));
     L.off_tmax = align_up(L.off_tmin + sizeof(float) * static_cast<size_t>(B) * static_cast<size_t>(L.tiles_per_set));
-    L.total = align_up(L.off_tmax + sizeof(float) * static_cast<size_t>(B) * static_cast<size_t>(L.tiles_per_set));
+    L.off_cand = align_up(L.off_tmax + sizeof(float) * static_cast<size_t>(B) * static_cast<size_t>(L.tiles_per_set));
+    L.split_parts = select_split_parts(B, L.ld, r);
+    const size_t np = static_cast<size_t>(L.split_parts) * static_cast<size_t>(B);  // 0 unless split
+    L.off_count = align_up(L.off_cand + sizeof(uint64_t) * kSplitKeys * np);
+    L.off_thr = align_up(L.off_count + sizeof(uint32_t) * np);
+    L.total = align_up(L.off_thr + (L.split_parts > 0 ? sizeof(uint32_t) * static_cast<size_t>(B) : 0));
     return L;
 }
 
@@ -53,7 +59,7 @@ knn_status check_sizes(int64_t B, int64_t d, int64_t V, int64_t S, int64_t total
     if (need_vocab && V > 0x7fffffffLL) return KNN_ERR_UNSUPPORTED;
     if (d > (int64_t(1) << 40) / elem_bytes(dtype)) return KNN_ERR_UNSUPPORTED;
     if (r > min_keys) return KNN_ERR_R_EXCEEDS_N;
-    const Layout L = layout(B, d, S, max_keys, max_queries, dtype);
+    const Layout L = layout(B, d, S, max_keys, max_queries, dtype, r);
     if (S * L.tiles_per_set > 0x7fffffffLL) return KNN_ERR_UNSUPPORTED;
     if (max_queries > 65535) return KNN_ERR_UNSUPPORTED;  // query groups per set on grid.y
     return KNN_OK;
@@ -101,7 +107,7 @@ knn_status validate_part(const Call &c, int part) {
     if (dist || sel) {
         if (!c.workspace) return KNN_ERR_WORKSPACE;
         if (reinterpret_cast<uintptr_t>(c.workspace) % kAlign) return KNN_ERR_WORKSPACE;
-        const Layout L = layout(c.B, c.d, c.S, c.max_keys, c.max_queries, c.dtype);
+        const Layout L = layout(c.B, c.d, c.S, c.max_keys, c.max_queries, c.dtype, c.r);
         if (c.workspace_bytes < L.total) return KNN_ERR_WORKSPACE;
     }
     return KNN_OK;
@@ -125,11 +131,14 @@ MixArgs mix_args(const Call &c) {
 }
 
 knn_status run_part(const Call &c, int part, hipStream_t stream) {
-    const Layout L = layout(c.B, c.d, c.S, c.max_keys, c.max_queries, c.dtype);
+    const Layout L = layout(c.B, c.d, c.S, c.max_keys, c.max_queries, c.dtype, c.r);
     char *ws = static_cast<char *>(c.workspace);
     float *dist = ws ? reinterpret_cast<float *>(ws + L.off_dist) : nullptr;
     float *tmin = ws ? reinterpret_cast<float *>(ws + L.off_tmin) : nullptr;
     float *tmax = ws ? reinterpret_cast<float *>(ws + L.off_tmax) : nullptr;
+    uint64_t *cand = (ws && L.split_parts > 0) ? reinterpret_cast<uint64_t *>(ws + L.off_cand) : nullptr;
+    uint32_t *part_count = (ws && L.split_parts > 0) ? reinterpret_cast<uint32_t *>(ws + L.off_count) : nullptr;
+    uint32_t *part_thr = (ws && L.split_parts > 0) ? reinterpret_cast<uint32_t *>(ws + L.off_thr) : nullptr;
     if (part == KNN_PART_DISTANCES) {
         DistPlan p = plan_distances(c.d, c.dtype, c.max_queries, c.queries, c.keys);
         p.rows_per_tile = L.rows_per_tile;
@@ -163,6 +172,9 @@ knn_status run_part(const Call &c, int part, hipStream_t stream) {
         a.r = c.r;
         a.ids = c.nbr_ids;
         a.dists = c.nbr_dists;
+        a.cand = cand;
+        a.part_count = part_count;
+        a.part_thr = part_thr;
         if (part == KNN_PART_SELECT) return status_of(launch_select(a, c.B, stream));
         return status_of(launch_select_mix(a, mix_args(c), c.B, stream));
     }
@@ -250,7 +262,7 @@ size_t knn_lm_mixture_workspace_size(int64_t B, int64_t d, int64_t V, int64_t S,
     if (check_sizes(B, d, V, S, total_keys, min_keys_per_set, max_keys_per_set, max_queries_per_set, dtype, r,
                     true) != KNN_OK)
         return 0;
-    return layout(B, d, S, max_keys_per_set, max_queries_per_set, dtype).total;
+    return layout(B, d, S, max_keys_per_set, max_queries_per_set, dtype, r).total;
 }
 
 knn_status knn_lm_mixture_validate(const void *queries, const void *keys, const int32_t *values,

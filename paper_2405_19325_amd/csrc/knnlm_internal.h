@@ -59,6 +59,9 @@ struct SelectArgs {
     int r;
     int32_t *ids;                // [B, r]
     float *dists;                // [B, r]
+    uint64_t *cand;              // split select: [B, parts, kSplitKeys] candidate keys, or null
+    uint32_t *part_count;        // split select: [B, parts] candidates per part
+    uint32_t *part_thr;          // split select: [B] threshold on the distance bits
 };
 
 struct MixArgs {
@@ -93,6 +96,16 @@ hipError_t launch_distances_mfma(int mq, knn_dtype dtype, const DistArgs &args, 
 hipError_t launch_key_sqnorms(const void *keys, int64_t n, int64_t d, knn_dtype dtype, float *out,
                               hipStream_t stream);
 int select_capacity(int r);
+// Split select: rows of at most kSplitMaxN keys are cut into parts of
+// kSplitKeys keys, one workgroup each, when r <= kSplitMaxR and the parts of
+// all queries fit in one pass of the chip.  Returns the parts per query, or 0
+// when a query's row is selected by a single workgroup.
+constexpr int kSplitKeys = 4096;
+constexpr int kSplitCap = 4096;
+constexpr int64_t kSplitMaxN = 65536;
+constexpr int kSplitMaxR = 1024;
+constexpr int64_t kSplitMaxBlocks = 256;
+int select_split_parts(int64_t B, int64_t ld, int r);
 hipError_t launch_select(const SelectArgs &args, int64_t B, hipStream_t stream);
 hipError_t launch_select_mix(const SelectArgs &args, const MixArgs &mix, int64_t B, hipStream_t stream);
 hipError_t launch_mix(const MixArgs &args, int64_t B, hipStream_t stream);

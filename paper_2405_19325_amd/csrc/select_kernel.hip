@@ -218,13 +218,28 @@ __device__ __forceinline__ void lds_bitonic(uint64_t *cand, uint32_t P) {
 // starts, the keys are scattered to tmp, and each key's final place is its
 // bucket start plus its rank among the (few) keys of its bucket.  A bucket
 // holding many equal distances only costs time, never order.
-template <int PER>
+struct NoHook {
+    __device__ void operator()() const {}
+};
+
+// Ascending sort of the n <= PER * 1024 keys in cand[0, n), in place, by
+// buckets of their distance bits over [lo, lo + w): each key takes a slot in
+// its bucket with an LDS atomic, a block scan turns bucket sizes into bucket
+// starts, the keys are scattered to tmp, and each key's final place is its
+// bucket start plus its rank among the (few) keys of its bucket.  A bucket
+// holding many equal distances only costs time, never order.  With ZEROED the
+// caller has cleared count[] and ordered that with a barrier.  `mid` runs
+// between the scan and the scatter (callers issue loads there that the rest
+// of the sort hides).
+template <int PER, bool ZEROED = false, typename Hook = NoHook>
 __device__ __forceinline__ void bucket_sort(uint64_t *cand, uint32_t n, uint32_t lo, uint32_t w, uint32_t *count,
-                                            uint32_t *start, uint64_t *tmp, Shared &sh) {
+                                            uint32_t *start, uint64_t *tmp, Shared &sh, Hook mid = Hook()) {
     const int tid = threadIdx.x;
     const int shift = range_shift(w > 1u ? w : 2u);
-    for (int i = tid; i < kSelectBins; i += kT) count[i] = 0u;
-    __syncthreads();
+    if (!ZEROED) {
+        for (int i = tid; i < kSelectBins; i += kT) count[i] = 0u;
+        __syncthreads();
+    }
     uint64_t key[PER];
     uint32_t bin[PER], slot[PER];
 #pragma unroll
@@ -240,19 +255,33 @@ __device__ __forceinline__ void bucket_sort(uint64_t *cand, uint32_t n, uint32_t
     const uint32_t excl = block_excl_scan(c0 + c1, sh.wave_tot);
     start[2 * tid] = excl;
     start[2 * tid + 1] = excl + c0;
+    mid();
     __syncthreads();
 #pragma unroll
     for (int q = 0; q < PER; ++q)
         if (q * kT + tid < static_cast<int>(n)) tmp[start[bin[q]] + slot[q]] = key[q];
     __syncthreads();
+    // Rank within the bucket: its first four entries are compared at once
+    // (reads past the bucket are discarded), a longer bucket goes on in a loop.
+    uint32_t b0[PER], nb[PER], rank[PER];
 #pragma unroll
     for (int q = 0; q < PER; ++q) {
-        if (q * kT + tid < static_cast<int>(n)) {
-            const uint32_t b0 = start[bin[q]], nb = count[bin[q]];
-            uint32_t rank = 0;
-            for (uint32_t i = 0; i < nb; ++i) rank += tmp[b0 + i] < key[q] ? 1u : 0u;
-            cand[b0 + rank] = key[q];
+        b0[q] = start[bin[q]];
+        nb[q] = count[bin[q]];
+        rank[q] = 0u;
+    }
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+#pragma unroll
+        for (uint32_t i = 0; i < 4; ++i) {
+            const uint32_t at = b0[q] + i < static_cast<uint32_t>(PER * kT) ? b0[q] + i : PER * kT - 1;
+            rank[q] += (i < nb[q] && tmp[at] < key[q]) ? 1u : 0u;
         }
+    }
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+        for (uint32_t i = 4; i < nb[q]; ++i) rank[q] += tmp[b0[q] + i] < key[q] ? 1u : 0u;
+        if (q * kT + tid < static_cast<int>(n)) cand[b0[q] + rank[q]] = key[q];
     }
     __syncthreads();
 }
@@ -627,6 +656,314 @@ __global__ __launch_bounds__(kT) void k_select_fast(SelectArgs a, MixArgs m) {
     }
 }
 
+// Split path: rows of at most kSplitMaxN keys, r <= kSplitMaxR, few queries.
+// Query b's row is cut into `parts` parts of kSplitKeys keys so that one query
+// keeps many CUs busy; two kernels, and no atomics or fences between
+// workgroups (the kernel boundary orders them).
+//
+// Parts kernel (blockIdx.x = b * parts + part): every part of query b reads
+// the same kSplitSamples keys sampled across the row (1024 runs of 4
+// consecutive keys, one run every N / 1024) and takes as threshold the end of the histogram bin, over the
+// samples' own range, that holds the ks-th smallest of them, ks aiming at
+// about r + 4 sd + 4 samples' worth of keys; it writes its keys below the
+// threshold to its own list (distance bits << 32 | key index << 12) and their
+// count, and part 0 records the threshold.  With mixing, each part also
+// writes its slice of the dense term of p_M: lambda * p_LM is what
+// fmaf(lambda, p_LM, acc * scale) gives wherever no neighbour carries the
+// token.  The part's keys and samples are requested before the row length is
+// known (as if the row filled the stride) and corrected after.
+constexpr int kSplitSamples = 4 * kT;
+
+template <bool MIX>
+__global__ __launch_bounds__(kT) void k_select_parts(SelectArgs a, MixArgs m, int parts) {
+    __shared__ uint32_t hist[kSelectBins];
+    __shared__ Shared sh;
+    const int tid = threadIdx.x;
+    const int64_t b = blockIdx.x / parts;
+    const int part = static_cast<int>(blockIdx.x - b * parts);
+    const float *drow = a.dist + b * a.ld;
+    const int64_t ld = a.ld < kSplitMaxN ? a.ld : kSplitMaxN;  // the host launches this kernel only when ld <= kSplitMaxN
+
+    // Requests first: the part's keys (4 per thread), 4 samples per thread for
+    // a full row, and the first float4 of the part's p_LM slice.
+    const int64_t i0 = static_cast<int64_t>(part) * kSplitKeys + 4 * tid;
+    uint4 v = make_uint4(~0u, ~0u, ~0u, ~0u);
+    if (i0 < ld) v = *reinterpret_cast<const uint4 *>(drow + i0);
+    // samples: 4 consecutive keys per thread, 1024 runs spread across the row
+    // (a run starts at a multiple of 4 at most N - 4, so it stays in the row)
+    uint4 sv = *reinterpret_cast<const uint4 *>(drow + (((static_cast<uint64_t>(tid) * static_cast<uint64_t>(ld)) >> 10) & ~3ull));
+    int64_t v0 = 0, nv = 0;
+    bool vec4 = false;
+    float4 pl4 = make_float4(0.f, 0.f, 0.f, 0.f);
+    if constexpr (MIX) {
+        const int64_t slice = ((m.V + parts - 1) / parts + 3) / 4 * 4;
+        v0 = static_cast<int64_t>(part) * slice;
+        nv = m.V - v0 < slice ? m.V - v0 : slice;
+        if (nv < 0) nv = 0;
+        vec4 = mix_vec4(m, b);
+        if (vec4 && tid < nv / 4) pl4 = reinterpret_cast<const float4 *>(m.p_lm + b * m.V + v0)[tid];
+    }
+    const int64_t s = set_of_query(a.query_offsets, a.S, b);
+    const int64_t k0 = a.key_offsets[s];
+    int64_t N = a.key_offsets[s + 1] - k0;
+    if (N > ld) N = ld;
+    const uint32_t r_eff = static_cast<uint32_t>(N < a.r ? N : a.r);
+    const bool sampled = N > kSplitCap;
+    // words past the row end read as all-ones, above any threshold
+    if (i0 >= N) v = make_uint4(~0u, ~0u, ~0u, ~0u);
+    if (i0 + 1 >= N) v.y = ~0u;
+    if (i0 + 2 >= N) v.z = ~0u;
+    if (i0 + 3 >= N) v.w = ~0u;
+    if (sampled && N != ld)  // a shorter row: sample it again
+        sv = *reinterpret_cast<const uint4 *>(drow + (((static_cast<uint64_t>(tid) * static_cast<uint64_t>(N)) >> 10) & ~3ull));
+    const uint32_t sb[4] = {sv.x, sv.y, sv.z, sv.w};
+
+    uint32_t thr = ~0u;  // a row that fits: every key
+    if (sampled) {
+        // distances are >= +0 and never NaN: bits <= 0x7f800000
+        uint32_t smin = min(min(sb[0], sb[1]), min(sb[2], sb[3]));
+        uint32_t smax = max(max(sb[0], sb[1]), max(sb[2], sb[3]));
+        block_minmax_u32(smin, smax, sh);
+        for (int i = tid; i < kSelectBins; i += kT) hist[i] = 0u;
+        __syncthreads();
+        const uint32_t w = smax + 1u - smin;
+        const int shift = range_shift(w);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) atomicAdd(&hist[(sb[u] - smin) >> shift], 1u);
+        const float k0f = ceilf(static_cast<float>(r_eff) * static_cast<float>(kSplitSamples) / static_cast<float>(N));
+        const uint32_t ks = static_cast<uint32_t>(k0f + ceilf(4.0f * sqrtf(k0f)) + 4.0f);
+        if (tid == 0) { sh.lo = smin; sh.hi = smax + 1u; sh.below = 0u; sh.cnt = kSplitSamples; }
+        __syncthreads();
+        if (ks < static_cast<uint32_t>(kSplitSamples)) {
+            pick_bin(hist, ks, shift, sh);
+            thr = sh.hi;  // at least ks samples lie below it
+        }
+    }
+
+    uint32_t c = 0;
+    c += v.x < thr ? 1u : 0u;
+    c += v.y < thr ? 1u : 0u;
+    c += v.z < thr ? 1u : 0u;
+    c += v.w < thr ? 1u : 0u;
+    uint32_t pos = block_excl_scan(c, sh.wave_tot);
+    const int64_t bp = b * parts + part;
+    if (tid == kT - 1) a.part_count[bp] = pos + c;
+    if (part == 0 && tid == 0) a.part_thr[b] = thr;
+    uint64_t *list = a.cand + bp * kSplitKeys;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const uint32_t bits = lane_word(v, e);
+        if (bits < thr)
+            list[pos++] = (static_cast<uint64_t>(bits) << 32) | (static_cast<uint64_t>(static_cast<uint32_t>(i0) + e) << 12);
+    }
+    if constexpr (MIX) {
+        const float lam = m.lambda;
+        float *pm = m.p_m + b * m.V + v0;
+        const float *plm = m.p_lm + b * m.V + v0;
+        if (vec4) {
+            for (int64_t i = tid; i < nv / 4; i += kT) {
+                const float4 x = i == tid ? pl4 : reinterpret_cast<const float4 *>(plm)[i];
+                reinterpret_cast<float4 *>(pm)[i] =
+                    make_float4(fmaf(lam, x.x, 0.0f), fmaf(lam, x.y, 0.0f), fmaf(lam, x.z, 0.0f), fmaf(lam, x.w, 0.0f));
+            }
+        } else {
+            for (int64_t i = tid; i < nv; i += kT) pm[i] = fmaf(lam, plm[i], 0.0f);
+        }
+    }
+}
+
+// Finish kernel (one workgroup per query).  It loads the part counts together
+// with the first kSplitCap / parts entries of every list, gathers the
+// candidates into LDS (the rest of a longer list afterwards), and bucket-sorts
+// them on their distance bits; the neighbours' tokens and p_LM values load
+// meanwhile.  Then it writes pi; with mixing, each neighbour adds its
+// unnormalised weight to its token's entry of an LDS hash table (as many slots
+// as twice the largest r, so probes stay short) while the block sums the
+// weights, and the tokens' p_M entries are written.  If the sample misjudged
+// the count (fewer than r candidates, or more than kSplitCap) it selects over
+// the whole row instead.  In LDS a candidate carries its slot (< 4096) in the
+// low 12 bits, below the key index, which it cannot reorder since indices are
+// distinct; the slot names where its token and p_LM value were staged.
+constexpr int kHashBits = 11;
+constexpr int kHashSlots = 1 << kHashBits;
+static_assert(kHashSlots >= 2 * kSplitMaxR, "the mixture hash needs twice as many slots as tokens");
+
+template <int PER, bool MIX>
+__device__ __forceinline__ void finish_sort(uint64_t *cand, uint32_t total, uint32_t lo, uint32_t thr, uint32_t *hist,
+                                            uint64_t *tmp, Shared &sh, const bool (&valid)[4], const int32_t (&tv)[4],
+                                            float (&pv)[4], const float *plm_row, int64_t V) {
+    auto prefetch_plm = [&] {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const bool in = MIX && valid[q] && tv[q] >= 0 && tv[q] < V;
+            pv[q] = MIX ? plm_row[in ? tv[q] : 0] : 0.0f;
+        }
+    };
+    bucket_sort<PER, true>(cand, total, lo, thr - lo, hist, hist + kSelectBins, tmp, sh, prefetch_plm);
+}
+
+template <bool MIX>
+__global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, int parts) {
+    constexpr int PER = kSplitCap / kT;
+    __shared__ uint64_t cand[kSplitCap];
+    __shared__ uint64_t tmp[kSplitCap];
+    __shared__ uint32_t hist[2 * kSelectBins];
+    __shared__ int32_t tok_of[MIX ? kSplitCap : 1];
+    __shared__ float plm_of[MIX ? kSplitCap : 1];
+    __shared__ int32_t hkey[MIX ? kHashSlots : 1];
+    __shared__ float hval[MIX ? kHashSlots : 1];
+    __shared__ Shared sh;
+    __shared__ uint32_t part_off[kWave + 1];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & (kWave - 1);
+    const int64_t b = blockIdx.x;
+    const uint64_t *lists = a.cand + b * parts * kSplitKeys;
+
+    // Counts, threshold and the first `win` entries of every list, all in flight together.
+    const uint32_t win = static_cast<uint32_t>(kSplitCap / parts);
+    const uint32_t cnt = (tid < kWave && lane < parts) ? a.part_count[b * parts + lane] : 0u;
+    const uint32_t thr = a.part_thr[b];
+    uint64_t key[PER];
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+        const uint32_t e = static_cast<uint32_t>(q * kT + tid);
+        const uint32_t p = e / win;
+        key[q] = p < static_cast<uint32_t>(parts) ? lists[p * kSplitKeys + (e - p * win)] : ~0ull;
+    }
+    const int64_t s = set_of_query(a.query_offsets, a.S, b);
+    const int64_t k0 = a.key_offsets[s];
+    int64_t N = a.key_offsets[s + 1] - k0;
+    if (N > a.ld) N = a.ld;
+    if (N > kSplitMaxN) N = kSplitMaxN;
+    const uint32_t r_eff = static_cast<uint32_t>(N < a.r ? N : a.r);
+    // LDS to clear while the loads are in flight: bucket counts, hash table.
+    for (int i = tid; i < kSelectBins; i += kT) hist[i] = 0u;
+    if constexpr (MIX) {
+        for (int i = tid; i < kHashSlots; i += kT) {
+            hkey[i] = -1;
+            hval[i] = 0.0f;
+        }
+    }
+    if (tid < kWave) {  // list starts, and whether any list is longer than its window
+        const uint32_t incl = wave_incl_scan_u32(cnt, lane);
+        if (lane < parts) part_off[lane] = incl - cnt;
+        if (lane == parts - 1) part_off[parts] = incl;
+        const uint32_t longest = wave_allmax_u32(cnt);
+        if (lane == 0) sh.found = longest > win ? 1u : 0u;
+    }
+    __syncthreads();
+    const uint32_t total = part_off[parts];
+    const bool fast = total >= r_eff && total <= static_cast<uint32_t>(kSplitCap);
+
+    uint64_t x = ~0ull;
+    uint32_t id = 0;
+    int32_t tok = -1;
+    float plm_t = 0.0f;
+    const bool ok = static_cast<uint32_t>(tid) < r_eff;
+    const float *plm_row = m.p_lm + b * m.V;
+    if (fast) {
+        uint32_t slot[PER];
+        bool valid[PER];
+        uint32_t lo = ~0u;
+#pragma unroll
+        for (int q = 0; q < PER; ++q) {
+            const uint32_t e = static_cast<uint32_t>(q * kT + tid);
+            const uint32_t p = e / win;
+            const uint32_t pc = p < static_cast<uint32_t>(parts) ? p : static_cast<uint32_t>(parts - 1);
+            const uint32_t i = e - p * win;
+            const uint32_t start = part_off[pc], end = part_off[pc + 1];
+            valid[q] = p < static_cast<uint32_t>(parts) && i < end - start;
+            slot[q] = start + i;
+            if (valid[q]) cand[slot[q]] = key[q] | slot[q];
+            lo = valid[q] ? min(lo, static_cast<uint32_t>(key[q] >> 32)) : lo;
+        }
+        // Tokens: unconditional loads (an invalid entry reads key 0's), so
+        // that nothing waits for them before the sort needs them.
+        int32_t tv[PER];
+#pragma unroll
+        for (int q = 0; q < PER; ++q)
+            tv[q] = MIX ? m.values[k0 + (valid[q] ? (static_cast<uint32_t>(key[q]) >> 12) : 0u)] : -1;
+        if (sh.found != 0u) {  // longer lists: the rest, one part after another (rare)
+            for (int p = 0; p < parts; ++p) {
+                const uint32_t n_p = part_off[p + 1] - part_off[p];
+                for (uint32_t i = win + tid; i < n_p; i += kT) {
+                    const uint64_t k = lists[p * kSplitKeys + i];
+                    const uint32_t sl = part_off[p] + i;
+                    cand[sl] = k | sl;
+                    if constexpr (MIX) {
+                        const int32_t t = m.values[k0 + (static_cast<uint32_t>(k) >> 12)];
+                        tok_of[sl] = t;
+                        plm_of[sl] = (t >= 0 && t < m.V) ? plm_row[t] : 0.0f;
+                    }
+                    lo = min(lo, static_cast<uint32_t>(k >> 32));
+                }
+            }
+        }
+        uint32_t hi_unused = 0u;
+        block_minmax_u32(lo, hi_unused, sh);  // also orders the LDS writes before the sort
+        float pv[PER];
+        if (total <= static_cast<uint32_t>(kSplitCap / 2))
+            finish_sort<PER / 2, MIX>(cand, total, lo, thr, hist, tmp, sh, valid, tv, pv, plm_row, m.V);
+        else
+            finish_sort<PER, MIX>(cand, total, lo, thr, hist, tmp, sh, valid, tv, pv, plm_row, m.V);
+        if constexpr (MIX) {
+#pragma unroll
+            for (int q = 0; q < PER; ++q)
+                if (valid[q]) {
+                    tok_of[slot[q]] = tv[q];
+                    plm_of[slot[q]] = pv[q];
+                }
+            __syncthreads();
+        }
+        x = ok ? cand[tid] : ~0ull;
+        id = static_cast<uint32_t>(x) >> 12;
+        if (MIX && ok) {
+            const uint32_t sl = static_cast<uint32_t>(x) & (kSplitCap - 1);
+            tok = tok_of[sl];
+            plm_t = plm_of[sl];
+        }
+    } else {
+        // The sample misjudged the count: select over the whole row.
+        uint32_t bmin, bmax;
+        row_range(a, b, N, bmin, bmax, sh);
+        const uint32_t n = select_stream<kSplitCap>(a.dist + b * a.ld, N, r_eff, bmin, bmax, cand, hist, sh);
+        x = (ok && static_cast<uint32_t>(tid) < n) ? cand[tid] : ~0ull;
+        id = static_cast<uint32_t>(x);
+        if (MIX && ok) {
+            tok = m.values[k0 + id];
+            plm_t = (tok >= 0 && tok < m.V) ? plm_row[tok] : 0.0f;
+        }
+    }
+    if (tok < 0 || tok >= m.V) tok = -1;  // tokens outside [0, V) carry no mass
+    const float d0 = __uint_as_float(static_cast<uint32_t>(cand[0] >> 32));  // the nearest distance
+    if (tid < a.r) {
+        a.ids[b * a.r + tid] = ok ? static_cast<int32_t>(id) : -1;
+        a.dists[b * a.r + tid] = ok ? __uint_as_float(static_cast<uint32_t>(x >> 32)) : __builtin_huge_valf();
+    }
+    if constexpr (MIX) {
+        const float dj = __uint_as_float(static_cast<uint32_t>(x >> 32));
+        const float wj = ok ? expf(-m.mu * (dj - d0)) : 0.0f;
+        // Token -> slot by linear probing from a multiplicative hash; at most
+        // r <= kHashSlots / 2 distinct tokens, so a free slot always exists.
+        uint32_t h = 0;
+        if (tok >= 0) {
+            h = (static_cast<uint32_t>(tok) * 2654435761u) >> (32 - kHashBits);
+            for (;;) {
+                const int32_t old = atomicCAS(&hkey[h], -1, tok);
+                if (old == -1 || old == tok) break;
+                h = (h + 1u) & (kHashSlots - 1);
+            }
+            atomicAdd(&hval[h], wj);
+        }
+        const float z = block_sum(wj, sh.red_f);  // its barriers also complete the additions
+        const float lam = m.lambda;
+        const float scale = (1.0f - lam) / z;
+        // Duplicate tokens write the same value.
+        if (tok >= 0) m.p_m[b * m.V + tok] = fmaf(lam, plm_t, hval[h] * scale);
+    }
+}
+
 // Standalone mixture on caller-given neighbours (any order): one workgroup per query.
 __global__ __launch_bounds__(kT) void k_mix(MixArgs m) {
     __shared__ __align__(16) float acc[kVocabTile];
@@ -667,6 +1004,15 @@ hipError_t launch_sel(const SelectArgs &a, const MixArgs &m, int64_t B, hipStrea
     if (B > 0x7fffffffLL) return hipErrorInvalidConfiguration;
     if (a.tile_min == nullptr || a.tile_max == nullptr) return hipErrorInvalidValue;
     const dim3 grid(static_cast<unsigned>(B)), block(kT);
+    const int parts = select_split_parts(B, a.ld, a.r);
+    if (parts > 0) {
+        if (a.cand == nullptr || a.part_count == nullptr || a.part_thr == nullptr) return hipErrorInvalidValue;
+        hipLaunchKernelGGL((k_select_parts<MIX>), dim3(static_cast<unsigned>(B * parts)), block, 0, st, a, m, parts);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL((k_select_finish<MIX>), grid, block, 0, st, a, m, parts);
+        return hipGetLastError();
+    }
     if (a.ld <= kFastMaxN && a.r <= kT) {
         hipLaunchKernelGGL((k_select_fast<MIX>), grid, block, 0, st, a, m);
         return hipGetLastError();
@@ -681,6 +1027,12 @@ hipError_t launch_sel(const SelectArgs &a, const MixArgs &m, int64_t B, hipStrea
 }
 
 }  // namespace
+
+int select_split_parts(int64_t B, int64_t ld, int r) {
+    if (B < 1 || ld < 1 || ld > kSplitMaxN || r > kSplitMaxR) return 0;
+    const int64_t parts = (ld + kSplitKeys - 1) / kSplitKeys;
+    return B * parts <= kSplitMaxBlocks ? static_cast<int>(parts) : 0;
+}
 
 int select_capacity(int r) {
     int p = 1;

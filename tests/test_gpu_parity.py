@@ -299,26 +299,63 @@ def test_full_size_workloads(name, sample):
     _free()
 
 
-def test_adversarial_row_takes_the_streamed_path():
-    """Keys at the positions the fast path samples are far away and every other
-    key sits on the query: the sampled threshold then keeps more than the LDS
-    capacity, the general streamed path takes over, and the answer (ties broken
-    by index) is still exact."""
-    _say("adversarial sample")
-    n, d, r = 65536, 16, 1000
+def test_split_and_one_workgroup_select_agree():
+    """The same queries through the split select (few queries: a 64K-key row
+    over 16 workgroups) and the one-workgroup select (20 queries): the same
+    neighbours and distances bit for bit, p_M within the rounding of the LDS
+    atomics.  fp32 keys keep both batches on the streaming distance kernel,
+    whose per-query arithmetic does not depend on the batch."""
+    _say("split vs one-workgroup select")
+    w = gen.make(gen.scaled(gen.config("decode_7b"), B=20, n_keys=65536, d=256, dtype="f32", mu=1 / 16), 29,
+                 device="cuda")
+    _, ids20, d20 = _run(w)
+    p20 = _run(w)[0].clone()
+    ids20, d20 = ids20.clone(), d20.clone()
+    qo = np.array([0, 3], np.int64)
+    prob = knn.MixtureProblem(w.queries[:3].contiguous(), w.keys, w.values, w.key_offsets,
+                              torch.as_tensor(qo, device="cuda"), w.p_lm[:3].contiguous(), w.r, w.mu, w.lam,
+                              key_offsets_host=w.key_offsets_host, query_offsets_host=qo)
+    p3, ids3, d3 = prob.run()
+    torch.cuda.synchronize()
+    assert torch.equal(ids3, ids20[:3]) and torch.equal(d3, d20[:3])
+    torch.testing.assert_close(p3, p20[:3], rtol=0, atol=1e-7)
+
+
+def _sampled_positions(path, n):
+    """Key positions whose distances the sampled threshold of each select path reads."""
+    if path == "split":  # 4096 keys, one every n / 4096
+        return (np.arange(4096) * n) >> 12
     t = np.arange(1024)
-    sampled = ((t & 15) * 4096 + 4 * t + ((t >> 4) & 3))
+    return (t & 15) * 4096 + 4 * t + ((t >> 4) & 3)  # one-workgroup path: a key per thread's registers
+
+
+# One query (the row is split over 16 workgroups) and 20 queries on one set
+# (too many parts for one pass of the chip, so one workgroup per query).
+@pytest.mark.parametrize("path,B", [("split", 1), ("one-workgroup", 20)])
+def test_adversarial_row_takes_the_streamed_path(path, B):
+    """Keys at the positions the select samples are far away and every other
+    key sits on the query: the sampled threshold then keeps more than the
+    candidate capacity, the streamed path over the whole row takes over, and
+    the answer (ties broken by index) is still exact."""
+    _say(f"adversarial sample ({path})")
+    n, d, r = 65536, 16, 1000
+    sampled = _sampled_positions(path, n)
     k = np.zeros((n, d), np.float32)
     k[sampled] = 3.0
-    q = np.zeros((1, d), np.float32)
+    q = np.zeros((B, d), np.float32)
     vals = (np.arange(n) % 50).astype(np.int32)
-    p_lm = np.full((1, 50), 0.02, np.float32)
-    tq, tk, tv, tko, tqo, tp = _tensor_inputs(q, k, vals, p_lm, [0, n], [0, 1], torch.bfloat16)
+    p_lm = np.full((B, 50), 0.02, np.float32)
+    tq, tk, tv, tko, tqo, tp = _tensor_inputs(q, k, vals, p_lm, [0, n], [0, B], torch.bfloat16)
     p_m, ids, dists = knn.mixture(tq, tk, tv, tko, tqo, tp, r, 0.1, 0.5)
     torch.cuda.synchronize()
     expect = np.setdiff1d(np.arange(n), sampled)[:r]
-    assert ids[0].cpu().numpy().tolist() == expect.tolist()
+    for b in range(B):
+        assert ids[b].cpu().numpy().tolist() == expect.tolist()
     assert torch.all(dists == 0.0)
+    # every neighbour is at distance 0: equal weights 1/r on tokens i % 50
+    counts = np.bincount(vals[expect], minlength=50).astype(np.float64)
+    want = 0.5 * 0.02 + 0.5 * counts / r
+    np.testing.assert_allclose(p_m.cpu().numpy(), np.broadcast_to(want, (B, 50)), rtol=0, atol=1e-6)
 
 
 # ------------------------------------------------- matrix-core (query batch) path
