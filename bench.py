@@ -26,7 +26,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0  # MI355X HBM3E, published
-PMC_FILE = os.path.join(ROOT, "profiles", "dist_kernel_decode_7b_pmc.json")
+PMC_FILE = os.path.join(ROOT, "profiles", "dist_kernel_{workload}_pmc.json")
 
 
 def _args():
@@ -44,15 +44,16 @@ def _args():
 
 def dist_kernel_source_hash() -> str:
     h = hashlib.sha256()
-    for f in ("dist_kernels.hip", "knnlm_device.h", "knnlm_internal.h"):
+    for f in ("dist_kernels.hip", "mfma_kernels.hip", "knnlm_device.h", "knnlm_internal.h"):
         h.update(open(os.path.join(ROOT, "paper_2405_19325_amd", "csrc", f), "rb").read())
     return h.hexdigest()[:16]
 
 
-def measured_traffic():
-    """HBM bytes per distance launch from committed rocprofv3 counters, if they match this kernel source."""
+def measured_traffic(workload):
+    """HBM bytes per distance launch from committed rocprofv3 counters for this
+    workload, if they were taken on this kernel source."""
     try:
-        rec = json.load(open(PMC_FILE))
+        rec = json.load(open(PMC_FILE.format(workload=workload)))
     except (OSError, ValueError):
         return None
     if rec.get("kernel_source_hash") != dist_kernel_source_hash():
@@ -133,11 +134,32 @@ def main():
     ms_per_step = elapsed_ms / a.steps
     qps = B * a.steps / (elapsed_ms / 1e3)
 
+    # The distance and top-r stages alone (no mixture), the same way: the
+    # path whose HBM efficiency the distance + select design is judged on.
+    n_topr = min(a.steps, 200)
+    t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for i in range(4):
+        probs[i % 2].run_part("distances")
+        probs[i % 2].run_part("select")
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for i in range(n_topr):
+        probs[i % 2].run_part("distances")
+        probs[i % 2].run_part("select")
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    topr_ms = t_start.elapsed_time(t_end) / n_topr
+    topr = {"ms_per_step": round(topr_ms, 5), "alg_bytes": dist_alg_bytes + B * w.r * 8, "steps": n_topr,
+            "hbm_frac": round((dist_alg_bytes + B * w.r * 8) / (topr_ms / 1e3) / 1e9 / PEAK_HBM_GBS, 4)}
+
+    max_q = int(np.diff(w.query_offsets_host).max())
+    matrix_core = spec.dtype in ("bf16", "f16") and spec.d % 8 == 0 and max_q >= 16
     achieved = dist_alg_bytes / (avg_dist_ms / 1e3) / 1e9
-    traffic = measured_traffic()
+    traffic = measured_traffic(a.workload)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
-                "kernel": "distance stage (k_dist_vec)", "alg_bytes_per_launch": dist_alg_bytes,
+                "kernel": "distance stage (" + ("k_dist_mfma" if matrix_core else "k_dist_vec") + ")",
+                "alg_bytes_per_launch": dist_alg_bytes,
                 "avg_launch_ms": round(avg_dist_ms, 5), "timed_launches": len(dist_ms)}
 
     if a.copy_calibration:
@@ -178,6 +200,7 @@ def main():
         "select_mix_ms": round(avg_tail_ms, 5),
         "step_alg_bytes": step_alg_bytes,
         "step_hbm_frac": round(step_alg_bytes / (ms_per_step / 1e3) / 1e9 / PEAK_HBM_GBS, 4),
+        "distance_topr": topr,
         "host_wall_s": round(wall, 3),
         "roofline": roofline,
         "cpu_baseline": cpu,
@@ -197,7 +220,7 @@ def cpu_baseline(w, spec, seed, budget_s):
     keys_h, dt = oracle.host_elements(w.keys[:n0])
     vals = w.values[:n0].cpu().numpy()
     ko, qo1 = np.array([0, n0], dtype=np.int64), np.array([0, 1], dtype=np.int64)
-    extra = gen.extra_queries(spec, seed, 64, device="cpu")
+    extra = gen.extra_queries(spec, seed, 4096, device="cpu")
     q_all, _ = oracle.host_elements(extra)
     p_lm = w.p_lm[:1].cpu().numpy()
     done = 0

@@ -38,7 +38,7 @@ Layout layout(int64_t B, int64_t d, int64_t S, int64_t max_keys, int64_t max_que
     L.split_parts = select_split_parts(B, L.ld, r);
     const size_t np = static_cast<size_t>(L.split_parts) * static_cast<size_t>(B);  // 0 unless split
     L.off_count = align_up(L.off_cand + sizeof(uint64_t) * kSplitKeys * np);
-    L.off_thr = align_up(L.off_count + sizeof(uint32_t) * np);
+    L.off_thr = align_up(L.off_count + 2 * sizeof(uint32_t) * np);  // counts, then minima
     L.total = align_up(L.off_thr + (L.split_parts > 0 ? sizeof(uint32_t) * static_cast<size_t>(B) : 0));
     return L;
 }
@@ -174,6 +174,7 @@ knn_status run_part(const Call &c, int part, hipStream_t stream) {
         a.dists = c.nbr_dists;
         a.cand = cand;
         a.part_count = part_count;
+        a.part_min = part_count ? part_count + L.split_parts * c.B : nullptr;
         a.part_thr = part_thr;
         if (part == KNN_PART_SELECT) return status_of(launch_select(a, c.B, stream));
         return status_of(launch_select_mix(a, mix_args(c), c.B, stream));

@@ -61,6 +61,7 @@ struct SelectArgs {
     float *dists;                // [B, r]
     uint64_t *cand;              // split select: [B, parts, kSplitKeys] candidate keys, or null
     uint32_t *part_count;        // split select: [B, parts] candidates per part
+    uint32_t *part_min;          // split select: [B, parts] smallest candidate distance bits per part
     uint32_t *part_thr;          // split select: [B] threshold on the distance bits
 };
 

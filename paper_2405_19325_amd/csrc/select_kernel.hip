@@ -59,6 +59,7 @@ struct Shared {
     uint32_t wave_tot[kNumWaves];
     float red_f[kNumWaves];
     uint32_t lo, hi, below, cnt, found, total;
+    uint32_t ccount, cmin;  // split path: a part's candidates so far, and their smallest distance bits
     float dmin;
 };
 
@@ -181,9 +182,39 @@ __device__ __forceinline__ void pick_bin(const uint32_t *hist, uint32_t need, in
     __syncthreads();
 }
 
+template <int BLOG = kSelectBinsLog2>
 __device__ __forceinline__ int range_shift(uint32_t w) {
     const int nbits = 32 - __clz(static_cast<int>(w - 1u));
-    return nbits > kSelectBinsLog2 ? nbits - kSelectBinsLog2 : 0;
+    return nbits > BLOG ? nbits - BLOG : 0;
+}
+
+// One wave (lane = its lane index): the bin of hist[0, 2048) holding the
+// need-th (1-based) of the counted keys, or ~0u if there are fewer.  Each lane
+// sums 32 consecutive bins, a wave scan finds the lane where the running count
+// reaches need, and that lane walks its 32 bins.
+__device__ __forceinline__ uint32_t wave_pick_bin(const uint32_t *hist, uint32_t need, int lane) {
+    static_assert(kSelectBins == 32 * kWave, "32 bins per lane");
+    uint32_t c[32];
+    uint32_t sum = 0;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const uint4 q = reinterpret_cast<const uint4 *>(hist + 32 * lane)[i];
+        c[4 * i] = q.x; c[4 * i + 1] = q.y; c[4 * i + 2] = q.z; c[4 * i + 3] = q.w;
+        sum += q.x + q.y + q.z + q.w;
+    }
+    const uint32_t incl = wave_incl_scan_u32(sum, lane);
+    const uint32_t excl = incl - sum;
+    const bool mine = excl < need && incl >= need;
+    const uint64_t who = __ballot(mine);
+    if (who == 0) return ~0u;
+    uint32_t j = 0, run = excl;
+    bool done = false;
+#pragma unroll
+    for (int i = 0; i < 32; ++i) {
+        run += c[i];
+        if (!done && run >= need) { j = static_cast<uint32_t>(32 * lane + i); done = true; }
+    }
+    return readlane_u32(j, __ffsll(static_cast<unsigned long long>(who)) - 1);
 }
 
 // Is key (bits, i) before the end of the range?  In the distance regime the
@@ -223,21 +254,27 @@ struct NoHook {
 };
 
 // Ascending sort of the n <= PER * 1024 keys in cand[0, n), in place, by
-// buckets of their distance bits over [lo, lo + w): each key takes a slot in
-// its bucket with an LDS atomic, a block scan turns bucket sizes into bucket
-// starts, the keys are scattered to tmp, and each key's final place is its
-// bucket start plus its rank among the (few) keys of its bucket.  A bucket
+// 2^BLOG buckets of their distance bits over [lo, lo + w): each key takes a
+// slot in its bucket with an LDS atomic, a block scan turns bucket sizes into
+// bucket starts, the keys are scattered to tmp, and each key's final place is
+// its bucket start plus its rank among the (few) keys of its bucket (the first
+// eight compared at once; reads past the bucket are discarded).  A bucket
 // holding many equal distances only costs time, never order.  With ZEROED the
 // caller has cleared count[] and ordered that with a barrier.  `mid` runs
 // between the scan and the scatter (callers issue loads there that the rest
-// of the sort hides).
-template <int PER, bool ZEROED = false, typename Hook = NoHook>
+// of the sort hides).  Only cand[0, keep) is guaranteed on return: keys whose
+// bucket starts at or after `keep` are not placed.
+template <int PER, int BLOG = kSelectBinsLog2, bool ZEROED = false, typename Hook = NoHook>
 __device__ __forceinline__ void bucket_sort(uint64_t *cand, uint32_t n, uint32_t lo, uint32_t w, uint32_t *count,
-                                            uint32_t *start, uint64_t *tmp, Shared &sh, Hook mid = Hook()) {
+                                            uint32_t *start, uint64_t *tmp, Shared &sh, Hook mid = Hook(),
+                                            uint32_t keep = ~0u) {
+    constexpr int BINS = 1 << BLOG;
+    constexpr int BPT = BINS / kT;  // bins per thread in the scan
+    static_assert(BPT >= 1 && BINS % kT == 0, "whole bins per thread");
     const int tid = threadIdx.x;
-    const int shift = range_shift(w > 1u ? w : 2u);
+    const int shift = range_shift<BLOG>(w > 1u ? w : 2u);
     if (!ZEROED) {
-        for (int i = tid; i < kSelectBins; i += kT) count[i] = 0u;
+        for (int i = tid; i < BINS; i += kT) count[i] = 0u;
         __syncthreads();
     }
     uint64_t key[PER];
@@ -247,41 +284,47 @@ __device__ __forceinline__ void bucket_sort(uint64_t *cand, uint32_t n, uint32_t
         const uint32_t j = static_cast<uint32_t>(q * kT + tid);
         key[q] = j < n ? cand[j] : ~0ull;
         bin[q] = j < n ? ((static_cast<uint32_t>(key[q] >> 32) - lo) >> shift) : 0u;
-        if (bin[q] >= static_cast<uint32_t>(kSelectBins)) bin[q] = kSelectBins - 1;  // never for consistent input
+        if (bin[q] >= static_cast<uint32_t>(BINS)) bin[q] = BINS - 1;  // never for consistent input
         slot[q] = j < n ? atomicAdd(&count[bin[q]], 1u) : 0u;
     }
     __syncthreads();
-    const uint32_t c0 = count[2 * tid], c1 = count[2 * tid + 1];
-    const uint32_t excl = block_excl_scan(c0 + c1, sh.wave_tot);
-    start[2 * tid] = excl;
-    start[2 * tid + 1] = excl + c0;
+    uint32_t cb[BPT], tsum = 0;
+#pragma unroll
+    for (int i = 0; i < BPT; ++i) {
+        cb[i] = count[BPT * tid + i];
+        tsum += cb[i];
+    }
+    uint32_t run = block_excl_scan(tsum, sh.wave_tot);
+#pragma unroll
+    for (int i = 0; i < BPT; ++i) {
+        start[BPT * tid + i] = run;
+        run += cb[i];
+    }
     mid();
     __syncthreads();
 #pragma unroll
     for (int q = 0; q < PER; ++q)
         if (q * kT + tid < static_cast<int>(n)) tmp[start[bin[q]] + slot[q]] = key[q];
     __syncthreads();
-    // Rank within the bucket: its first four entries are compared at once
-    // (reads past the bucket are discarded), a longer bucket goes on in a loop.
     uint32_t b0[PER], nb[PER], rank[PER];
 #pragma unroll
     for (int q = 0; q < PER; ++q) {
         b0[q] = start[bin[q]];
-        nb[q] = count[bin[q]];
+        nb[q] = b0[q] < keep ? count[bin[q]] : 0u;  // a bucket past `keep` holds no key of the first `keep`
         rank[q] = 0u;
     }
 #pragma unroll
     for (int q = 0; q < PER; ++q) {
 #pragma unroll
-        for (uint32_t i = 0; i < 4; ++i) {
+        for (uint32_t i = 0; i < 8; ++i) {
             const uint32_t at = b0[q] + i < static_cast<uint32_t>(PER * kT) ? b0[q] + i : PER * kT - 1;
             rank[q] += (i < nb[q] && tmp[at] < key[q]) ? 1u : 0u;
         }
     }
 #pragma unroll
     for (int q = 0; q < PER; ++q) {
-        for (uint32_t i = 4; i < nb[q]; ++i) rank[q] += tmp[b0[q] + i] < key[q] ? 1u : 0u;
-        if (q * kT + tid < static_cast<int>(n)) cand[b0[q] + rank[q]] = key[q];
+        for (uint32_t i = 8; i < nb[q]; ++i) rank[q] += tmp[b0[q] + i] < key[q] ? 1u : 0u;
+        if (q * kT + tid < static_cast<int>(n) && b0[q] < keep) cand[b0[q] + rank[q]] = key[q];
     }
     __syncthreads();
 }
@@ -676,13 +719,18 @@ constexpr int kSplitSamples = 4 * kT;
 
 template <bool MIX>
 __global__ __launch_bounds__(kT) void k_select_parts(SelectArgs a, MixArgs m, int parts) {
-    __shared__ uint32_t hist[kSelectBins];
+    __shared__ __align__(16) uint32_t hist[kSelectBins];
     __shared__ Shared sh;
     const int tid = threadIdx.x;
+    const int lane = tid & (kWave - 1);
     const int64_t b = blockIdx.x / parts;
     const int part = static_cast<int>(blockIdx.x - b * parts);
     const float *drow = a.dist + b * a.ld;
     const int64_t ld = a.ld < kSplitMaxN ? a.ld : kSplitMaxN;  // the host launches this kernel only when ld <= kSplitMaxN
+    if (tid == 0) {
+        sh.ccount = 0u;
+        sh.cmin = ~0u;
+    }
 
     // Requests first: the part's keys (4 per thread), 4 samples per thread for
     // a full row, and the first float4 of the part's p_LM slice.
@@ -732,23 +780,36 @@ __global__ __launch_bounds__(kT) void k_select_parts(SelectArgs a, MixArgs m, in
         for (int u = 0; u < 4; ++u) atomicAdd(&hist[(sb[u] - smin) >> shift], 1u);
         const float k0f = ceilf(static_cast<float>(r_eff) * static_cast<float>(kSplitSamples) / static_cast<float>(N));
         const uint32_t ks = static_cast<uint32_t>(k0f + ceilf(4.0f * sqrtf(k0f)) + 4.0f);
-        if (tid == 0) { sh.lo = smin; sh.hi = smax + 1u; sh.below = 0u; sh.cnt = kSplitSamples; }
         __syncthreads();
-        if (ks < static_cast<uint32_t>(kSplitSamples)) {
-            pick_bin(hist, ks, shift, sh);
-            thr = sh.hi;  // at least ks samples lie below it
+        if (tid < kWave) {
+            // the end of the bin holding the ks-th sample: at least ks samples lie below it
+            const uint32_t j = ks < static_cast<uint32_t>(kSplitSamples) ? wave_pick_bin(hist, ks, lane) : ~0u;
+            const uint64_t end = static_cast<uint64_t>(smin) + ((static_cast<uint64_t>(j) + 1u) << shift);
+            if (lane == 0) sh.hi = j == ~0u ? ~0u : static_cast<uint32_t>(end < smax + 1ull ? end : smax + 1ull);
         }
     }
+    __syncthreads();
+    if (sampled) thr = sh.hi;
 
-    uint32_t c = 0;
-    c += v.x < thr ? 1u : 0u;
-    c += v.y < thr ? 1u : 0u;
-    c += v.z < thr ? 1u : 0u;
-    c += v.w < thr ? 1u : 0u;
-    uint32_t pos = block_excl_scan(c, sh.wave_tot);
+    // Keys below the threshold go to the part's list: each wave reserves its
+    // range with one LDS atomic (the list's order is free: the finish sorts).
+    uint32_t c = 0, cmin = ~0u;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const uint32_t bits = lane_word(v, e);
+        c += bits < thr ? 1u : 0u;
+        cmin = bits < thr ? min(cmin, bits) : cmin;
+    }
+    const uint32_t incl = wave_incl_scan_u32(c, lane);
+    const uint32_t wtot = readlane_u32(incl, kWave - 1);
+    const uint32_t wmin = wave_allmin_u32(cmin);
+    uint32_t base = 0;
+    if (lane == 0 && wtot > 0) {
+        base = atomicAdd(&sh.ccount, wtot);
+        atomicMin(&sh.cmin, wmin);
+    }
+    uint32_t pos = readlane_u32(base, 0) + incl - c;
     const int64_t bp = b * parts + part;
-    if (tid == kT - 1) a.part_count[bp] = pos + c;
-    if (part == 0 && tid == 0) a.part_thr[b] = thr;
     uint64_t *list = a.cand + bp * kSplitKeys;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -770,6 +831,12 @@ __global__ __launch_bounds__(kT) void k_select_parts(SelectArgs a, MixArgs m, in
             for (int64_t i = tid; i < nv; i += kT) pm[i] = fmaf(lam, plm[i], 0.0f);
         }
     }
+    __syncthreads();
+    if (tid == 0) {
+        a.part_count[bp] = sh.ccount;
+        a.part_min[bp] = sh.cmin;
+        if (part == 0) a.part_thr[b] = thr;
+    }
 }
 
 // Finish kernel (one workgroup per query).  It loads the part counts together
@@ -777,21 +844,18 @@ __global__ __launch_bounds__(kT) void k_select_parts(SelectArgs a, MixArgs m, in
 // candidates into LDS (the rest of a longer list afterwards), and bucket-sorts
 // them on their distance bits; the neighbours' tokens and p_LM values load
 // meanwhile.  Then it writes pi; with mixing, each neighbour adds its
-// unnormalised weight to its token's entry of an LDS hash table (as many slots
-// as twice the largest r, so probes stay short) while the block sums the
-// weights, and the tokens' p_M entries are written.  If the sample misjudged
+// unnormalised weight at its token in an LDS vocabulary tile that takes over
+// the sort buffers, and the tokens' p_M entries are written.  If the sample misjudged
 // the count (fewer than r candidates, or more than kSplitCap) it selects over
 // the whole row instead.  In LDS a candidate carries its slot (< 4096) in the
 // low 12 bits, below the key index, which it cannot reorder since indices are
 // distinct; the slot names where its token and p_LM value were staged.
-constexpr int kHashBits = 11;
-constexpr int kHashSlots = 1 << kHashBits;
-static_assert(kHashSlots >= 2 * kSplitMaxR, "the mixture hash needs twice as many slots as tokens");
+constexpr int kFinishBinsLog2 = 12;  // 4096 buckets: about one candidate each where they crowd
 
 template <int PER, bool MIX>
 __device__ __forceinline__ void finish_sort(uint64_t *cand, uint32_t total, uint32_t lo, uint32_t thr, uint32_t *hist,
                                             uint64_t *tmp, Shared &sh, const bool (&valid)[4], const int32_t (&tv)[4],
-                                            float (&pv)[4], const float *plm_row, int64_t V) {
+                                            float (&pv)[4], const float *plm_row, int64_t V, uint32_t keep) {
     auto prefetch_plm = [&] {
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
@@ -799,19 +863,23 @@ __device__ __forceinline__ void finish_sort(uint64_t *cand, uint32_t total, uint
             pv[q] = MIX ? plm_row[in ? tv[q] : 0] : 0.0f;
         }
     };
-    bucket_sort<PER, true>(cand, total, lo, thr - lo, hist, hist + kSelectBins, tmp, sh, prefetch_plm);
+    bucket_sort<PER, kFinishBinsLog2, true>(cand, total, lo, thr - lo, hist, hist + (1 << kFinishBinsLog2), tmp, sh,
+                                             prefetch_plm, keep);
 }
 
 template <bool MIX>
 __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, int parts) {
     constexpr int PER = kSplitCap / kT;
-    __shared__ uint64_t cand[kSplitCap];
-    __shared__ uint64_t tmp[kSplitCap];
-    __shared__ uint32_t hist[2 * kSelectBins];
-    __shared__ int32_t tok_of[MIX ? kSplitCap : 1];
-    __shared__ float plm_of[MIX ? kSplitCap : 1];
-    __shared__ int32_t hkey[MIX ? kHashSlots : 1];
-    __shared__ float hval[MIX ? kHashSlots : 1];
+    constexpr int kSortBytes = 2 * kSplitCap * 8 + (8 << kFinishBinsLog2);
+    constexpr int kSmem = MIX ? kSortBytes + 2 * kSplitCap * 4 : kSortBytes;
+    static_assert(!MIX || kVocabTileFast * 4 <= kSmem, "the vocabulary tile fits over the sort buffers");
+    __shared__ __align__(16) unsigned char smem[kSmem];
+    uint64_t *cand = reinterpret_cast<uint64_t *>(smem);                          // [kSplitCap]
+    uint64_t *tmp = cand + kSplitCap;                                              // [kSplitCap]
+    uint32_t *hist = reinterpret_cast<uint32_t *>(tmp + kSplitCap);                // [2 << kFinishBinsLog2]: counts, starts
+    int32_t *tok_of = reinterpret_cast<int32_t *>(smem + kSortBytes);              // [kSplitCap]
+    float *plm_of = reinterpret_cast<float *>(tok_of + kSplitCap);                 // [kSplitCap]
+    float *acc = reinterpret_cast<float *>(smem);  // mixture: a vocabulary tile, over everything above
     __shared__ Shared sh;
     __shared__ uint32_t part_off[kWave + 1];
 
@@ -823,6 +891,7 @@ __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, i
     // Counts, threshold and the first `win` entries of every list, all in flight together.
     const uint32_t win = static_cast<uint32_t>(kSplitCap / parts);
     const uint32_t cnt = (tid < kWave && lane < parts) ? a.part_count[b * parts + lane] : 0u;
+    const uint32_t pmin = (tid < kWave && lane < parts) ? a.part_min[b * parts + lane] : ~0u;
     const uint32_t thr = a.part_thr[b];
     uint64_t key[PER];
 #pragma unroll
@@ -837,20 +906,18 @@ __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, i
     if (N > a.ld) N = a.ld;
     if (N > kSplitMaxN) N = kSplitMaxN;
     const uint32_t r_eff = static_cast<uint32_t>(N < a.r ? N : a.r);
-    // LDS to clear while the loads are in flight: bucket counts, hash table.
-    for (int i = tid; i < kSelectBins; i += kT) hist[i] = 0u;
-    if constexpr (MIX) {
-        for (int i = tid; i < kHashSlots; i += kT) {
-            hkey[i] = -1;
-            hval[i] = 0.0f;
-        }
-    }
+    // Bucket counts to clear while the loads are in flight.
+    for (int i = tid; i < (1 << kFinishBinsLog2); i += kT) hist[i] = 0u;
     if (tid < kWave) {  // list starts, and whether any list is longer than its window
         const uint32_t incl = wave_incl_scan_u32(cnt, lane);
         if (lane < parts) part_off[lane] = incl - cnt;
         if (lane == parts - 1) part_off[parts] = incl;
         const uint32_t longest = wave_allmax_u32(cnt);
-        if (lane == 0) sh.found = longest > win ? 1u : 0u;
+        const uint32_t cmin = wave_allmin_u32(pmin);
+        if (lane == 0) {
+            sh.found = longest > win ? 1u : 0u;
+            sh.cmin = cmin;  // the smallest candidate distance bits
+        }
     }
     __syncthreads();
     const uint32_t total = part_off[parts];
@@ -865,7 +932,7 @@ __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, i
     if (fast) {
         uint32_t slot[PER];
         bool valid[PER];
-        uint32_t lo = ~0u;
+        const uint32_t lo = sh.cmin;
 #pragma unroll
         for (int q = 0; q < PER; ++q) {
             const uint32_t e = static_cast<uint32_t>(q * kT + tid);
@@ -876,7 +943,6 @@ __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, i
             valid[q] = p < static_cast<uint32_t>(parts) && i < end - start;
             slot[q] = start + i;
             if (valid[q]) cand[slot[q]] = key[q] | slot[q];
-            lo = valid[q] ? min(lo, static_cast<uint32_t>(key[q] >> 32)) : lo;
         }
         // Tokens: unconditional loads (an invalid entry reads key 0's), so
         // that nothing waits for them before the sort needs them.
@@ -896,17 +962,15 @@ __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, i
                         tok_of[sl] = t;
                         plm_of[sl] = (t >= 0 && t < m.V) ? plm_row[t] : 0.0f;
                     }
-                    lo = min(lo, static_cast<uint32_t>(k >> 32));
                 }
             }
         }
-        uint32_t hi_unused = 0u;
-        block_minmax_u32(lo, hi_unused, sh);  // also orders the LDS writes before the sort
+        __syncthreads();  // the candidates are in LDS
         float pv[PER];
         if (total <= static_cast<uint32_t>(kSplitCap / 2))
-            finish_sort<PER / 2, MIX>(cand, total, lo, thr, hist, tmp, sh, valid, tv, pv, plm_row, m.V);
+            finish_sort<PER / 2, MIX>(cand, total, lo, thr, hist, tmp, sh, valid, tv, pv, plm_row, m.V, r_eff);
         else
-            finish_sort<PER, MIX>(cand, total, lo, thr, hist, tmp, sh, valid, tv, pv, plm_row, m.V);
+            finish_sort<PER, MIX>(cand, total, lo, thr, hist, tmp, sh, valid, tv, pv, plm_row, m.V, r_eff);
         if constexpr (MIX) {
 #pragma unroll
             for (int q = 0; q < PER; ++q)
@@ -944,23 +1008,28 @@ __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, i
     if constexpr (MIX) {
         const float dj = __uint_as_float(static_cast<uint32_t>(x >> 32));
         const float wj = ok ? expf(-m.mu * (dj - d0)) : 0.0f;
-        // Token -> slot by linear probing from a multiplicative hash; at most
-        // r <= kHashSlots / 2 distinct tokens, so a free slot always exists.
-        uint32_t h = 0;
-        if (tok >= 0) {
-            h = (static_cast<uint32_t>(tok) * 2654435761u) >> (32 - kHashBits);
-            for (;;) {
-                const int32_t old = atomicCAS(&hkey[h], -1, tok);
-                if (old == -1 || old == tok) break;
-                h = (h + 1u) & (kHashSlots - 1);
-            }
-            atomicAdd(&hval[h], wj);
-        }
-        const float z = block_sum(wj, sh.red_f);  // its barriers also complete the additions
+        // Z; the barrier also ends every use of the sort buffers, which the
+        // vocabulary tile then takes over.
+        const float wsum = wave_allsum(wj);
+        if (lane == 0) sh.red_f[tid / kWave] = wsum;
+        __syncthreads();
+        float z = 0.0f;
+#pragma unroll
+        for (int w = 0; w < kNumWaves; ++w) z += sh.red_f[w];
         const float lam = m.lambda;
         const float scale = (1.0f - lam) / z;
-        // Duplicate tokens write the same value.
-        if (tok >= 0) m.p_m[b * m.V + tok] = fmaf(lam, plm_t, hval[h] * scale);
+        // Each neighbour adds its weight at its token in a vocabulary tile
+        // (only the touched entries are cleared); the tokens' p_M entries are
+        // then written, duplicates writing the same value.
+        for (int64_t t0 = 0; t0 < m.V; t0 += kVocabTileFast) {
+            const bool in = tok >= t0 && tok < t0 + kVocabTileFast;
+            if (t0 > 0) __syncthreads();  // the previous tile's reads are done
+            if (in) acc[tok - t0] = 0.0f;
+            __syncthreads();
+            if (in) atomicAdd(&acc[tok - t0], wj);
+            __syncthreads();
+            if (in) m.p_m[b * m.V + tok] = fmaf(lam, plm_t, acc[tok - t0] * scale);
+        }
     }
 }
 
