@@ -842,43 +842,34 @@ __global__ __launch_bounds__(kT) void k_select_parts(SelectArgs a, MixArgs m, in
 // Finish kernel (one workgroup per query).  It loads the part counts together
 // with the first kSplitCap / parts entries of every list, gathers the
 // candidates into LDS (the rest of a longer list afterwards), and bucket-sorts
-// them on their distance bits; the neighbours' tokens and p_LM values load
-// meanwhile.  Then it writes pi; with mixing, each neighbour adds its
-// unnormalised weight at its token in an LDS vocabulary tile that takes over
-// the sort buffers, and the tokens' p_M entries are written.  If the sample misjudged
-// the count (fewer than r candidates, or more than kSplitCap) it selects over
-// the whole row instead.  In LDS a candidate carries its slot (< 4096) in the
-// low 12 bits, below the key index, which it cannot reorder since indices are
-// distinct; the slot names where its token and p_LM value were staged.
+// them on their distance bits while their tokens load.  Then it writes pi;
+// with mixing, each neighbour adds its unnormalised weight at its token in an
+// LDS vocabulary tile that takes over the sort buffers, and the tokens' p_M
+// entries are written.  If the sample misjudged the count (fewer than r
+// candidates, or more than kSplitCap) it selects over the whole row instead.
+// In LDS a candidate carries its slot (< 4096) in the low 12 bits, below the
+// key index, which it cannot reorder since indices are distinct; the slot
+// names where its token was staged.
 constexpr int kFinishBinsLog2 = 12;  // 4096 buckets: about one candidate each where they crowd
 
-template <int PER, bool MIX>
+template <int PER>
 __device__ __forceinline__ void finish_sort(uint64_t *cand, uint32_t total, uint32_t lo, uint32_t thr, uint32_t *hist,
-                                            uint64_t *tmp, Shared &sh, const bool (&valid)[4], const int32_t (&tv)[4],
-                                            float (&pv)[4], const float *plm_row, int64_t V, uint32_t keep) {
-    auto prefetch_plm = [&] {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const bool in = MIX && valid[q] && tv[q] >= 0 && tv[q] < V;
-            pv[q] = MIX ? plm_row[in ? tv[q] : 0] : 0.0f;
-        }
-    };
+                                            uint64_t *tmp, Shared &sh, uint32_t keep) {
     bucket_sort<PER, kFinishBinsLog2, true>(cand, total, lo, thr - lo, hist, hist + (1 << kFinishBinsLog2), tmp, sh,
-                                             prefetch_plm, keep);
+                                             NoHook(), keep);
 }
 
 template <bool MIX>
 __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, int parts) {
     constexpr int PER = kSplitCap / kT;
     constexpr int kSortBytes = 2 * kSplitCap * 8 + (8 << kFinishBinsLog2);
-    constexpr int kSmem = MIX ? kSortBytes + 2 * kSplitCap * 4 : kSortBytes;
+    constexpr int kSmem = MIX ? kSortBytes + kSplitCap * 4 + 16384 : kSortBytes;  // + tokens, + room for the tile
     static_assert(!MIX || kVocabTileFast * 4 <= kSmem, "the vocabulary tile fits over the sort buffers");
     __shared__ __align__(16) unsigned char smem[kSmem];
     uint64_t *cand = reinterpret_cast<uint64_t *>(smem);                          // [kSplitCap]
     uint64_t *tmp = cand + kSplitCap;                                              // [kSplitCap]
     uint32_t *hist = reinterpret_cast<uint32_t *>(tmp + kSplitCap);                // [2 << kFinishBinsLog2]: counts, starts
     int32_t *tok_of = reinterpret_cast<int32_t *>(smem + kSortBytes);              // [kSplitCap]
-    float *plm_of = reinterpret_cast<float *>(tok_of + kSplitCap);                 // [kSplitCap]
     float *acc = reinterpret_cast<float *>(smem);  // mixture: a vocabulary tile, over everything above
     __shared__ Shared sh;
     __shared__ uint32_t part_off[kWave + 1];
@@ -957,36 +948,24 @@ __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, i
                     const uint64_t k = lists[p * kSplitKeys + i];
                     const uint32_t sl = part_off[p] + i;
                     cand[sl] = k | sl;
-                    if constexpr (MIX) {
-                        const int32_t t = m.values[k0 + (static_cast<uint32_t>(k) >> 12)];
-                        tok_of[sl] = t;
-                        plm_of[sl] = (t >= 0 && t < m.V) ? plm_row[t] : 0.0f;
-                    }
+                    if constexpr (MIX) tok_of[sl] = m.values[k0 + (static_cast<uint32_t>(k) >> 12)];
                 }
             }
         }
         __syncthreads();  // the candidates are in LDS
-        float pv[PER];
         if (total <= static_cast<uint32_t>(kSplitCap / 2))
-            finish_sort<PER / 2, MIX>(cand, total, lo, thr, hist, tmp, sh, valid, tv, pv, plm_row, m.V, r_eff);
+            finish_sort<PER / 2>(cand, total, lo, thr, hist, tmp, sh, r_eff);
         else
-            finish_sort<PER, MIX>(cand, total, lo, thr, hist, tmp, sh, valid, tv, pv, plm_row, m.V, r_eff);
+            finish_sort<PER>(cand, total, lo, thr, hist, tmp, sh, r_eff);
         if constexpr (MIX) {
 #pragma unroll
             for (int q = 0; q < PER; ++q)
-                if (valid[q]) {
-                    tok_of[slot[q]] = tv[q];
-                    plm_of[slot[q]] = pv[q];
-                }
+                if (valid[q]) tok_of[slot[q]] = tv[q];
             __syncthreads();
         }
         x = ok ? cand[tid] : ~0ull;
         id = static_cast<uint32_t>(x) >> 12;
-        if (MIX && ok) {
-            const uint32_t sl = static_cast<uint32_t>(x) & (kSplitCap - 1);
-            tok = tok_of[sl];
-            plm_t = plm_of[sl];
-        }
+        if (MIX && ok) tok = tok_of[static_cast<uint32_t>(x) & (kSplitCap - 1)];
     } else {
         // The sample misjudged the count: select over the whole row.
         uint32_t bmin, bmax;
@@ -994,12 +973,10 @@ __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, i
         const uint32_t n = select_stream<kSplitCap>(a.dist + b * a.ld, N, r_eff, bmin, bmax, cand, hist, sh);
         x = (ok && static_cast<uint32_t>(tid) < n) ? cand[tid] : ~0ull;
         id = static_cast<uint32_t>(x);
-        if (MIX && ok) {
-            tok = m.values[k0 + id];
-            plm_t = (tok >= 0 && tok < m.V) ? plm_row[tok] : 0.0f;
-        }
+        if (MIX && ok) tok = m.values[k0 + id];
     }
     if (tok < 0 || tok >= m.V) tok = -1;  // tokens outside [0, V) carry no mass
+    if (MIX && tok >= 0) plm_t = plm_row[tok];  // needed only at the end
     const float d0 = __uint_as_float(static_cast<uint32_t>(cand[0] >> 32));  // the nearest distance
     if (tid < a.r) {
         a.ids[b * a.r + tid] = ok ? static_cast<int32_t>(id) : -1;
