@@ -377,7 +377,7 @@ bool vector_path_ok(int64_t d, knn_dtype dtype, const void *queries, const void 
 }  // namespace
 
 bool mfma_shape(int64_t d, knn_dtype dtype, int64_t max_queries) {
-    return (dtype == KNN_BF16 || dtype == KNN_F16) && d % 8 == 0 && max_queries >= kMfmaMinQueries;
+    return (dtype == KNN_BF16 || dtype == KNN_F16) && d % kMfmaSpan == 0 && max_queries >= kMfmaMinQueries;
 }
 
 // Key rows per distance workgroup.  Streaming path: about 1 MiB of keys, fewer

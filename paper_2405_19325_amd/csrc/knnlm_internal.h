@@ -83,9 +83,10 @@ struct MixArgs {
 DistPlan plan_distances(int64_t d, knn_dtype dtype, int64_t max_queries, const void *queries,
                         const void *keys);
 
-// The matrix-core path serves 16-bit keys with d % 8 == 0 when at least this
-// many queries share a key set.
+// The matrix-core path serves 16-bit keys with d % kMfmaSpan == 0 when at
+// least kMfmaMinQueries queries share a key set.
 constexpr int kMfmaMinQueries = 16;
+constexpr int kMfmaSpan = 128;
 bool mfma_shape(int64_t d, knn_dtype dtype, int64_t max_queries);
 int mfma_keys_per_pass();
 int dist_tile_rows(int64_t d, knn_dtype dtype, int64_t S, int64_t max_keys, int64_t max_queries);

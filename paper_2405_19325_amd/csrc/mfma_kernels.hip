@@ -7,23 +7,26 @@
 // products form a dense [queries x d] . [d x keys] contraction: every key
 // element is used by up to 128 queries, so streaming the keys from HBM once
 // needs up to 128 flop per byte -- beyond the vector ALUs, within the
-// matrix cores.  A workgroup owns 256 keys of one set (4 waves x 4 blocks of
-// 16 keys) and up to 128 of the set's queries (MQ blocks of 16).  d is walked
-// in spans of 128 elements: each lane streams 64 contiguous bytes (four
-// 16-byte non-temporal loads) of each of its 4 key rows, so the four lanes of
-// a row read its 256 contiguous bytes, while the workgroup stages the span of
-// its queries (read from cache: every workgroup of the set shares them) into
-// LDS with a padded, bank-conflict-free pitch; the next span's keys and
-// queries are loading while v_mfma_f32_16x16x32 (bf16 or f16, fp32
-// accumulate) runs over the current one for every (query block, key block)
-// pair.  In MFMA step c of a span, lane l holds key (or query) row l % 16 and
-// elements 32 * (l / 16) + 8c .. +8 -- the same elements for both operands, so
-// the contraction is exact up to fp32 rounding.
+// matrix cores.  A workgroup of 4 waves takes passes of 4 * KB blocks of 16
+// keys of one set (KB per wave) against up to 128 of the set's queries (MQ
+// blocks of 16).  d is walked in spans of 128 elements.  In MFMA step c of a
+// span, lane l holds key (or query) row l % 16 and elements 32c + 8 (l / 16)
+// .. +8 -- the same elements for both operands, so the contraction is exact
+// up to fp32 rounding -- and one 16-byte non-temporal load per (key block, c)
+// reads 64 contiguous bytes of each of 16 rows.  The workgroup stages each
+// span of its queries (read from cache: every workgroup of the set shares
+// them) in LDS in exactly the A-operand lane order, so staging and reading
+// are contiguous 1 KB accesses.  The next span's keys and queries load while
+// v_mfma_f32_16x16x32 (bf16 or f16, fp32 accumulate) runs over the current
+// one for every (query block, key block) pair; every load is unconditional,
+// since a branch around loads makes the compiler wait for all loads in flight.
 //
 // ||k||^2 (unless precomputed) and ||q||^2 are dot2 chains over the same
 // elements.  The summation order differs from the matrix cores', so unlike the
 // streaming kernel a query equal to a key gives a distance of a few ulps of
 // ||q||^2 + ||k||^2 rather than exactly 0 (clamped at 0 from below).
+#include <type_traits>
+
 #include "knnlm_device.h"
 #include "knnlm_internal.h"
 
@@ -36,8 +39,9 @@ typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kMfmaWaves = 4;
-constexpr int kKeyBlocks = 4;  // 16-key blocks per wave
-constexpr int kMfmaKeys = kMfmaWaves * kKeyBlocks * 16;  // 256 keys per workgroup pass
+// Key rows per distance tile: a multiple of every variant's keys per pass
+// (kMfmaWaves * KB * 16 for KB = 2 or 4).
+constexpr int kMfmaTileRows = 256;
 
 template <knn_dtype DT>
 __device__ __forceinline__ f32x4_t mfma16(const uint4 a, const uint4 b, f32x4_t c) {
@@ -72,12 +76,14 @@ __device__ __forceinline__ float group4_sum(float v) {
     return v;
 }
 
-constexpr int kSpan = 128;                // elements of d per pipeline step (256 bytes of a row)
+constexpr int kSpan = kMfmaSpan;          // elements of d per pipeline step (256 bytes of a row)
 constexpr int kFragBytes = kWave * 16;    // one MFMA operand fragment: 64 lanes x 16 bytes
 
-// MQ: 16-query blocks per workgroup; KB: 16-key blocks per wave and pass.
-template <knn_dtype DT, int MQ, int KB>
-__global__ __launch_bounds__(kMfmaWaves * kWave) void k_dist_mfma(DistArgs a, int64_t n_tiles, int64_t groups) {
+// MQ: 16-query blocks per workgroup; KB: 16-key blocks per wave and pass;
+// NORMS: ||k||^2 comes precomputed; OCC: waves per SIMD the registers must
+// allow (measured best: 4 for one query block, 2 otherwise).
+template <knn_dtype DT, int MQ, int KB, bool NORMS, int OCC>
+__global__ __launch_bounds__(kMfmaWaves * kWave, OCC) void k_dist_mfma(DistArgs a, int64_t n_tiles, int64_t groups) {
     constexpr int QB = MQ * 16;
     constexpr int KEYS = kMfmaWaves * KB * 16;  // keys per pass
     // Staged query span, double-buffered.  Fragment (j, c) -- rows j*16 .. +16,
@@ -112,35 +118,40 @@ __global__ __launch_bounds__(kMfmaWaves * kWave) void k_dist_mfma(DistArgs a, in
     const int lane = tid & (kWave - 1);
     const int wave = tid / kWave;
     const int g = lane >> 4, lr = lane & 15;
-    const int64_t d = a.d;
-    const int64_t row_bytes = d * 2;
-    const int64_t nspan = (d + kSpan - 1) / kSpan;
+    const int64_t row_bytes = a.d * 2;
+    const int64_t nspan = a.d / kSpan;
     const char *qbase = static_cast<const char *>(a.queries) + qb * row_bytes;
     const char *kset = static_cast<const char *>(a.keys) + k0 * row_bytes;
-    const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
-    const bool have_norms = a.key_sqnorms != nullptr;
 
     for (int q = tid; q < QB; q += kMfmaWaves * kWave) {
         smin[q] = 0xffffffffu;
         smax[q] = 0u;
     }
 
+    // Every load is unconditional (d is a multiple of kSpan; a query row or
+    // key row past the data reads row 0 of the block or tile instead, and the
+    // results of those lanes are never used), so that no branch makes the
+    // compiler wait for the loads already in flight.
+    //
+    // Query staging: wave `wave` stages fragments (m, wave) of a span -- query
+    // row m*16 + lr, elements 32*wave + 8g .. +8 -- and its lanes sum the
+    // squares of what they stage (||q||^2, completed over lanes and waves).
+    const char *qptr[MQ];
+#pragma unroll
+    for (int m = 0; m < MQ; ++m) {
+        const int qr = m * 16 + lr;
+        qptr[m] = qbase + (qr < nq ? qr : 0) * row_bytes + 64 * wave + 16 * g;
+    }
+
     for (int64_t c0 = r0; c0 < r1; c0 += KEYS) {
-        // Wave `wave` stages fragments (m, wave) of the next span: query row
-        // m*16 + lr, elements 32*wave + 8g .. +8.  Its lanes also sum the squares
-        // of what they stage (||q||^2, completed over lanes and waves below).
         float qqp[MQ];
 #pragma unroll
         for (int m = 0; m < MQ; ++m) qqp[m] = 0.0f;
         auto load_q = [&](int64_t sp, uint4 (&qn)[MQ]) {
-            const int64_t e = sp * kSpan + 32 * wave + 8 * g;
 #pragma unroll
-            for (int m = 0; m < MQ; ++m) {
-                const int qr = m * 16 + lr;
-                qn[m] = (qr < nq && e < d) ? *reinterpret_cast<const uint4 *>(qbase + qr * row_bytes + e * 2) : zero;
-            }
+            for (int m = 0; m < MQ; ++m) qn[m] = *reinterpret_cast<const uint4 *>(qptr[m] + sp * (2 * kSpan));
         };
-        auto store_q = [&](int buf, const uint4 (&qn)[MQ]) {
+        auto stage_q = [&](int buf, const uint4 (&qn)[MQ]) {
 #pragma unroll
             for (int m = 0; m < MQ; ++m) {
                 *reinterpret_cast<uint4 *>(&qlds[buf][((m * 4 + wave) * kWave + lane) * 16]) = qn[m];
@@ -151,11 +162,14 @@ __global__ __launch_bounds__(kMfmaWaves * kWave) void k_dist_mfma(DistArgs a, in
         // 32c + 8g .. +8, so one load instruction reads 64 contiguous bytes of
         // each of 16 rows.
         const int64_t wrow = c0 + wave * (KB * 16) + lr;
-        auto load_k = [&](int64_t sp, int kb, int c) {
+        const char *kptr[KB];  // this lane's byte 16g of its row in each key block
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) {
             const int64_t row = wrow + kb * 16;
-            const int64_t e = sp * kSpan + 32 * c + 8 * g;
-            return (row < r1 && e < d) ? load_stream(reinterpret_cast<const uint4 *>(kset + row * row_bytes + e * 2))
-                                       : zero;
+            kptr[kb] = kset + (row < r1 ? row : r0) * row_bytes + 16 * g;
+        }
+        auto load_k = [&](int64_t sp, int kb, int c) {
+            return load_stream(reinterpret_cast<const uint4 *>(kptr[kb] + sp * (2 * kSpan) + 64 * c));
         };
 
         f32x4_t acc[MQ][KB];
@@ -175,15 +189,18 @@ __global__ __launch_bounds__(kMfmaWaves * kWave) void k_dist_mfma(DistArgs a, in
         {
             uint4 qn[MQ];
             load_q(0, qn);
-            store_q(0, qn);
+            stage_q(0, qn);
         }
         __syncthreads();
 
-        for (int64_t sp = 0; sp < nspan; ++sp) {
+        // One span; with MORE the next one's keys and queries load meanwhile.
+        // The last span is peeled off so that the loop body has no branch (a
+        // branch around loads makes the compiler wait for every load in flight).
+        auto span = [&](int64_t sp, auto more_tag) {
+            constexpr bool MORE = decltype(more_tag)::value;
             const int cur = static_cast<int>(sp & 1);
-            const bool more = sp + 1 < nspan;
             uint4 qn[MQ];
-            if (more) load_q(sp + 1, qn);
+            if constexpr (MORE) load_q(sp + 1, qn);
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
                 uint4 af[MQ];
@@ -194,27 +211,41 @@ __global__ __launch_bounds__(kMfmaWaves * kWave) void k_dist_mfma(DistArgs a, in
                 for (int j = 0; j < MQ; ++j)
 #pragma unroll
                     for (int kb = 0; kb < KB; ++kb) acc[j][kb] = mfma16<DT>(af[j], bk[kb][c], acc[j][kb]);
-                if (!have_norms) {
+                if constexpr (!NORMS) {
 #pragma unroll
                     for (int kb = 0; kb < KB; ++kb) kkp[kb] = dot_chunk<DT>(bk[kb][c], bk[kb][c], kkp[kb]);
                 }
                 // chunk c of this span is consumed: start loading it for the next
-                if (more) {
+                if constexpr (MORE) {
 #pragma unroll
                     for (int kb = 0; kb < KB; ++kb) bk[kb][c] = load_k(sp + 1, kb, c);
                 }
             }
-            if (more) store_q(cur ^ 1, qn);
+            if constexpr (MORE) stage_q(cur ^ 1, qn);
             __syncthreads();
-        }
+        };
+        for (int64_t sp = 0; sp + 1 < nspan; ++sp) span(sp, std::true_type{});
+        span(nspan - 1, std::false_type{});
 
-        // ||q||^2: lanes g share a row, waves share the rest.
+        // ||q||^2 for the epilogue: lane (g, lr) needs query j*16 + 4g + i;
+        // lanes g share a row, waves share the rest.
 #pragma unroll
         for (int m = 0; m < MQ; ++m) {
             const float t = group4_sum(qqp[m]);
             if (g == 0) sqq[wave][m * 16 + lr] = t;
         }
         __syncthreads();
+        float qsel[MQ][4];
+#pragma unroll
+        for (int j = 0; j < MQ; ++j)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int q = j * 16 + g * 4 + i;
+                float t = sqq[0][q];
+#pragma unroll
+                for (int w = 1; w < kMfmaWaves; ++w) t += sqq[w][q];
+                qsel[j][i] = t;
+            }
 
         // Epilogue: lane (g, lr) holds dot(query j*16 + 4g + i, key wrow + 16 kb)
         // in acc[j][kb][i].
@@ -222,21 +253,18 @@ __global__ __launch_bounds__(kMfmaWaves * kWave) void k_dist_mfma(DistArgs a, in
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb) {
             const int64_t row = wrow + kb * 16;
-            kk[kb] = have_norms ? (row < r1 ? a.key_sqnorms[k0 + row] : 0.0f) : group4_sum(kkp[kb]);
+            kk[kb] = NORMS ? (row < r1 ? a.key_sqnorms[k0 + row] : 0.0f) : group4_sum(kkp[kb]);
         }
 #pragma unroll
         for (int j = 0; j < MQ; ++j) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int q = j * 16 + g * 4 + i;
-                float qsq = sqq[0][q];
-#pragma unroll
-                for (int w = 1; w < kMfmaWaves; ++w) qsq += sqq[w][q];
                 float mn = __builtin_huge_valf(), mx = 0.0f;
 #pragma unroll
                 for (int kb = 0; kb < KB; ++kb) {
                     const int64_t row = wrow + kb * 16;
-                    const float dist = clamp_nonneg(fmaf(-2.0f, acc[j][kb][i], qsq + kk[kb]));
+                    const float dist = clamp_nonneg(fmaf(-2.0f, acc[j][kb][i], qsel[j][i] + kk[kb]));
                     const bool ok = q < nq && row < r1;
                     if (ok) {
                         a.dist[(qb + q) * a.ld + row] = dist;
@@ -256,6 +284,7 @@ __global__ __launch_bounds__(kMfmaWaves * kWave) void k_dist_mfma(DistArgs a, in
     }
 
     if (a.tile_min != nullptr) {
+        __syncthreads();
         for (int q = tid; q < nq; q += kMfmaWaves * kWave) {
             a.tile_min[(qb + q) * tiles + tile] = __uint_as_float(smin[q]);
             a.tile_max[(qb + q) * tiles + tile] = __uint_as_float(smax[q]);
@@ -263,33 +292,39 @@ __global__ __launch_bounds__(kMfmaWaves * kWave) void k_dist_mfma(DistArgs a, in
     }
 }
 
-template <knn_dtype DT>
+template <knn_dtype DT, bool NORMS>
 hipError_t launch_mq(int mq, const DistArgs &a, int64_t n_tiles, int64_t groups, dim3 grid, hipStream_t st) {
     const dim3 block(kMfmaWaves * kWave);
     switch (mq) {
-    case 1: hipLaunchKernelGGL((k_dist_mfma<DT, 1, 4>), grid, block, 0, st, a, n_tiles, groups); break;
-    case 2: hipLaunchKernelGGL((k_dist_mfma<DT, 2, 4>), grid, block, 0, st, a, n_tiles, groups); break;
-    case 4: hipLaunchKernelGGL((k_dist_mfma<DT, 4, 4>), grid, block, 0, st, a, n_tiles, groups); break;
-    case 8: hipLaunchKernelGGL((k_dist_mfma<DT, 8, 2>), grid, block, 0, st, a, n_tiles, groups); break;
+    case 1: hipLaunchKernelGGL((k_dist_mfma<DT, 1, 2, NORMS, 4>), grid, block, 0, st, a, n_tiles, groups); break;
+    case 2: hipLaunchKernelGGL((k_dist_mfma<DT, 2, 4, NORMS, 2>), grid, block, 0, st, a, n_tiles, groups); break;
+    case 4: hipLaunchKernelGGL((k_dist_mfma<DT, 4, 2, NORMS, 2>), grid, block, 0, st, a, n_tiles, groups); break;
+    case 8: hipLaunchKernelGGL((k_dist_mfma<DT, 8, 2, NORMS, 2>), grid, block, 0, st, a, n_tiles, groups); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
 
+template <knn_dtype DT>
+hipError_t launch_dt(int mq, const DistArgs &a, int64_t n_tiles, int64_t groups, dim3 grid, hipStream_t st) {
+    return a.key_sqnorms != nullptr ? launch_mq<DT, true>(mq, a, n_tiles, groups, grid, st)
+                                    : launch_mq<DT, false>(mq, a, n_tiles, groups, grid, st);
+}
+
 }  // namespace
 
-int mfma_keys_per_pass() { return kMfmaKeys; }
+int mfma_keys_per_pass() { return kMfmaTileRows; }
 
 hipError_t launch_distances_mfma(int mq, knn_dtype dtype, const DistArgs &args, int64_t S, int64_t groups,
                                  hipStream_t stream) {
     const int64_t n_tiles = S * args.tiles_per_set;
-    if (groups < 1 || args.rows_per_tile % kMfmaKeys != 0) return hipErrorInvalidConfiguration;
+    if (groups < 1 || args.rows_per_tile % kMfmaTileRows != 0) return hipErrorInvalidConfiguration;
     const int64_t nblocks = (n_tiles + 7) / 8 * 8 * groups;
     if (nblocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
     const dim3 grid(static_cast<unsigned>(nblocks));
     switch (dtype) {
-    case KNN_BF16: return launch_mq<KNN_BF16>(mq, args, n_tiles, groups, grid, stream);
-    case KNN_F16: return launch_mq<KNN_F16>(mq, args, n_tiles, groups, grid, stream);
+    case KNN_BF16: return launch_dt<KNN_BF16>(mq, args, n_tiles, groups, grid, stream);
+    case KNN_F16: return launch_dt<KNN_F16>(mq, args, n_tiles, groups, grid, stream);
     default: return hipErrorInvalidValue;
     }
 }

@@ -139,6 +139,9 @@ SMALL = [
     ("r1", gen.scaled(gen.config("decode_7b"), n_keys=5000, r=1), 9, None),
     ("r4096", gen.scaled(gen.config("decode_7b"), n_keys=9000, r=4096, B=2), 10, None),
     ("planted-bf16", gen.scaled(gen.config("decode_7b"), n_keys=30000, B=3, query_mode="planted"), 12, None),
+    # 40 queries per set, but d is no multiple of 128: the streaming kernel, 8 queries per workgroup
+    ("batch-f16-d1000", gen.scaled(gen.config("specverify_static"), B=80, S=2, n_keys=(3000, 4500), d=1000,
+                                   query_mode="iid", mu=1 / math.sqrt(1000)), 14, None),
     ("empty-sets", gen.scaled(gen.config("decode_7b"), B=3, S=5, n_keys=(3000, 2000, 4000, 2500, 1500), d=512,
                               r=256, mu=1 / math.sqrt(512)), 13, [0, 2, 0, 1, 0]),
 ]
@@ -363,8 +366,10 @@ def test_adversarial_row_takes_the_streamed_path(path, B):
 MFMA = [
     ("mfma-16q-bf16", gen.scaled(gen.config("specverify_seq"), B=16, S=1, n_keys=5000, d=1024,
                                  mu=1 / 32), 31),
-    ("mfma-40q-2sets-f16-d1000", gen.scaled(gen.config("specverify_static"), B=80, S=2, n_keys=(3000, 4500), d=1000,
-                                            query_mode="iid", mu=1 / math.sqrt(1000)), 32),
+    ("mfma-40q-2sets-f16-d1152", gen.scaled(gen.config("specverify_static"), B=80, S=2, n_keys=(3000, 4500), d=1152,
+                                            query_mode="iid", mu=1 / math.sqrt(1152)), 32),
+    ("mfma-d128-one-span", gen.scaled(gen.config("specverify_static"), B=32, S=1, n_keys=2900, d=128,
+                                      query_mode="iid", mu=1 / math.sqrt(128), r=300), 36),
     ("mfma-130q-bf16-groups", gen.scaled(gen.config("specverify_seq"), B=130, S=1, n_keys=3001, d=256, mu=1 / 16,
                                          r=700), 33),
     ("mfma-ragged-sets", gen.scaled(gen.config("specverify_seq"), B=51, S=3, n_keys=(2048, 1300, 4100), d=512,
