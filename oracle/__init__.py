@@ -11,7 +11,9 @@ Pinned against the paper and the mathematics by `tests/test_oracle_pins.py`:
 hand-computed cases, closed forms (sum of p_M, lambda = 1 and 0, r = 1,
 duplicate tokens, mu -> 0), a textbook softmax when r = N, a stable argsort on
 tiny inputs, exact-integer inputs, metamorphic invariances, and the element
-decoding against numpy / torch conversions.
+decoding against numpy / torch conversions; relative retrieval confidence
+(Section 3.2, eq. rrc) by sigmoid values known in closed form, its symmetry,
+its scale invariance and a hand-worked case.
 """
 from __future__ import annotations
 
@@ -52,6 +54,8 @@ def _load():
     lib.knn_oracle_sqdist.argtypes = [P, P, I, I64, I64, I64, I, P]
     lib.knn_oracle_select.argtypes = [P, P, I, I64, I64, P, P, I64, I32, I, P, P]
     lib.knn_oracle_mix.argtypes = [P, P, P, P, P, I64, I64, I32, P, I64, D, D, P, P]
+    lib.knn_oracle_mix_lambdas.argtypes = [P, P, P, P, P, I64, I64, I32, P, I64, D, P, P, P]
+    lib.knn_oracle_rrc_lambda.argtypes = [P, I64, I32, D, D, P]
     for f in (lib.knn_oracle_widen, lib.knn_oracle_sqdist, lib.knn_oracle_select, lib.knn_oracle_mix):
         f.restype = ctypes.c_int
     _lib = lib
@@ -116,9 +120,12 @@ def select(queries: np.ndarray, keys: np.ndarray, dtype: str, key_offsets: np.nd
 
 
 def mix(ids: np.ndarray, dists: np.ndarray, values: np.ndarray, key_offsets: np.ndarray,
-        query_offsets: np.ndarray, p_lm: np.ndarray, mu: float, lam: float,
+        query_offsets: np.ndarray, p_lm: np.ndarray, mu: float, lam,
         want_pknn: bool = False):
-    """p_M (and optionally p_kNN) in fp64 from per-query neighbour ids and fp64 distances."""
+    """p_M (and optionally p_kNN) in fp64 from per-query neighbour ids and fp64 distances.
+
+    `lam` is one weight of p_LM for every query (eq. kNN-LM) or an array of
+    one weight per query (e.g. from rrc_lambda)."""
     ids = np.ascontiguousarray(ids, dtype=np.int32)
     dists = np.ascontiguousarray(dists, dtype=np.float64)
     values = np.ascontiguousarray(values, dtype=np.int32)
@@ -129,10 +136,27 @@ def mix(ids: np.ndarray, dists: np.ndarray, values: np.ndarray, key_offsets: np.
     V = p_lm.shape[1]
     pm = np.empty((B, V), dtype=np.float64)
     pk = np.empty((B, V), dtype=np.float64) if want_pknn else None
-    rc = _load().knn_oracle_mix(_ptr(ids), _ptr(dists), _ptr(values), _ptr(ko), _ptr(qo), len(ko) - 1, B, r,
-                                _ptr(p_lm), V, float(mu), float(lam), _ptr(pm), _ptr(pk))
+    if np.ndim(lam) == 0:
+        rc = _load().knn_oracle_mix(_ptr(ids), _ptr(dists), _ptr(values), _ptr(ko), _ptr(qo), len(ko) - 1, B, r,
+                                    _ptr(p_lm), V, float(mu), float(lam), _ptr(pm), _ptr(pk))
+    else:
+        lams = np.ascontiguousarray(lam, dtype=np.float64)
+        if lams.shape != (B,):
+            raise ValueError("one lambda per query")
+        rc = _load().knn_oracle_mix_lambdas(_ptr(ids), _ptr(dists), _ptr(values), _ptr(ko), _ptr(qo), len(ko) - 1,
+                                            B, r, _ptr(p_lm), V, float(mu), _ptr(lams), _ptr(pm), _ptr(pk))
     _check(rc, "mix")
     return (pm, pk) if want_pknn else pm
+
+
+def rrc_lambda(dists: np.ndarray, alpha: float, tau: float) -> np.ndarray:
+    """Per-query lambda_t of relative retrieval confidence (Section 3.2, eq. rrc) from each
+    query's r neighbour distances (any order), in fp64."""
+    dists = np.ascontiguousarray(dists, dtype=np.float64)
+    B, r = dists.shape
+    out = np.empty(B, dtype=np.float64)
+    _check(_load().knn_oracle_rrc_lambda(_ptr(dists), B, r, float(alpha), float(tau), _ptr(out)), "rrc_lambda")
+    return out
 
 
 def host_elements(t) -> Tuple[np.ndarray, str]:

@@ -22,6 +22,9 @@
  *      largest mu*s, which changes nothing mathematically.
  *   4. p_M = lambda * p_LM + (1 - lambda) * p_kNN (eq. kNN-LM), with p_LM the
  *      caller's fp32 row widened to fp64.
+ *   5. Optionally a per-query lambda_t from relative retrieval confidence
+ *      (Section 3.2, eq. rrc): sigmoid((min_i |s_i| / max_i |s_i| - alpha) / tau)
+ *      over the query's r neighbours.
  *
  * Every function returns 0 on success and a negative code on a rejected
  * argument; nothing is printed.
@@ -242,14 +245,17 @@ int knn_oracle_select(const void *queries, const void *keys, int dtype, int64_t 
  * p_M = lambda * p_LM + (1 - lambda) * p_kNN.  out_pknn may be NULL.
  * Returns ORC_ERR_RANGE for an id outside its set or a value outside [0, V).
  */
-int knn_oracle_mix(const int32_t *ids, const double *dists, const int32_t *values,
-                   const int64_t *key_offsets, const int64_t *query_offsets, int64_t S, int64_t B,
-                   int32_t r, const float *p_lm, int64_t V, double mu, double lambda, double *out_pm,
-                   double *out_pknn) {
+/* The mixture with a per-query weight of p_LM: lambdas[b] for query b. */
+int knn_oracle_mix_lambdas(const int32_t *ids, const double *dists, const int32_t *values,
+                           const int64_t *key_offsets, const int64_t *query_offsets, int64_t S, int64_t B,
+                           int32_t r, const float *p_lm, int64_t V, double mu, const double *lambdas,
+                           double *out_pm, double *out_pknn) {
     int64_t total_keys, total_q;
-    if (!ids || !dists || !values || !key_offsets || !query_offsets || !p_lm || !out_pm) return ORC_ERR_ARG;
-    if (S < 1 || B < 0 || r < 1 || V < 1 || !(mu >= 0.0) || !(lambda >= 0.0 && lambda <= 1.0))
+    if (!ids || !dists || !values || !key_offsets || !query_offsets || !p_lm || !lambdas || !out_pm)
         return ORC_ERR_ARG;
+    if (S < 1 || B < 0 || r < 1 || V < 1 || !(mu >= 0.0)) return ORC_ERR_ARG;
+    for (int64_t b = 0; b < B; ++b)
+        if (!(lambdas[b] >= 0.0 && lambdas[b] <= 1.0)) return ORC_ERR_ARG;
     if (!check_offsets(key_offsets, S, &total_keys) || !check_offsets(query_offsets, S, &total_q) ||
         total_q != B)
         return ORC_ERR_ARG;
@@ -265,6 +271,7 @@ int knn_oracle_mix(const int32_t *ids, const double *dists, const int32_t *value
         for (int64_t b = query_offsets[s]; b < query_offsets[s + 1] && rc == 0; ++b) {
             const int32_t *id = ids + b * r;
             const double *dd = dists + b * r;
+            const double lambda = lambdas[b];
             /* the largest mu*s over pi is -mu times the smallest distance */
             double dmin = dd[0];
             for (int32_t j = 1; j < r; ++j)
@@ -289,6 +296,46 @@ int knn_oracle_mix(const int32_t *ids, const double *dists, const int32_t *value
     }
     free(pknn); free(w);
     return rc;
+}
+
+/* The mixture with one weight of p_LM for every query (eq. kNN-LM). */
+int knn_oracle_mix(const int32_t *ids, const double *dists, const int32_t *values,
+                   const int64_t *key_offsets, const int64_t *query_offsets, int64_t S, int64_t B,
+                   int32_t r, const float *p_lm, int64_t V, double mu, double lambda, double *out_pm,
+                   double *out_pknn) {
+    if (!(lambda >= 0.0 && lambda <= 1.0) || B < 0) return ORC_ERR_ARG;
+    double *lams = (double *)malloc(sizeof(double) * (size_t)(B > 0 ? B : 1));
+    if (!lams) return ORC_ERR_NOMEM;
+    for (int64_t b = 0; b < B; ++b) lams[b] = lambda;
+    int rc = knn_oracle_mix_lambdas(ids, dists, values, key_offsets, query_offsets, S, B, r, p_lm, V, mu, lams,
+                                    out_pm, out_pknn);
+    free(lams);
+    return rc;
+}
+
+/*
+ * Relative retrieval confidence (Section 3.2, eq. rrc): for each query b, with
+ * s_i = -dists[b * r + i] <= 0 over its r neighbours (any order),
+ *   lambda_t = sigmoid((min_i |s_i| / max_i |s_i| - alpha) / tau).
+ * |s_i| is the distance, so the ratio is the smallest over the largest
+ * neighbour distance.  If every neighbour is at distance 0 the ratio is 0/0;
+ * it is taken as 1 (the neighbours are all equally close).  tau > 0.
+ */
+int knn_oracle_rrc_lambda(const double *dists, int64_t B, int32_t r, double alpha, double tau,
+                          double *out_lambda) {
+    if (!dists || !out_lambda || B < 0 || r < 1 || !(tau > 0.0) || !isfinite(alpha)) return ORC_ERR_ARG;
+    for (int64_t b = 0; b < B; ++b) {
+        double dmin = dists[b * r], dmax = dists[b * r];
+        for (int32_t j = 1; j < r; ++j) {
+            double x = dists[b * r + j];
+            if (x < dmin) dmin = x;
+            if (x > dmax) dmax = x;
+        }
+        if (dmin < 0.0) return ORC_ERR_RANGE;
+        double ratio = dmax > 0.0 ? dmin / dmax : 1.0;
+        out_lambda[b] = 1.0 / (1.0 + exp(-(ratio - alpha) / tau));
+    }
+    return 0;
 }
 
 int knn_oracle_version(void) { return 1; }

@@ -305,3 +305,98 @@ def test_f16_decoding_matches_numpy_for_every_pattern():
     nan = np.isnan(ref)
     np.testing.assert_array_equal(np.isnan(got), nan)
     np.testing.assert_array_equal(got[~nan], ref[~nan])
+
+
+# ------------------------------------------- relative retrieval confidence
+
+ALPHA, TAU = 0.3, 0.1
+
+
+def test_rrc_hand_cases(golden_dir):
+    doc = json.load(open(os.path.join(golden_dir, "rrc_cases.json")))
+    h = json.load(open(os.path.join(golden_dir, "hand_cases.json")))["H-A"]
+    q = np.array([h["query"]], dtype=np.float32)
+    k = np.array(h["keys"], dtype=np.float32)
+    vals = np.array(h["values"], dtype=np.int32)
+    p_lm = np.array([doc["p_lm"]], dtype=np.float32)
+    for case in doc["cases"]:
+        ko, qo = _one_set(1, k.shape[0])
+        ids, dists = oracle.select(q, k, "f32", ko, qo, case["r"])
+        lam = oracle.rrc_lambda(dists, doc["alpha"], doc["tau"])
+        want_lam = _eval_closed_form(case["lambda_expr"])
+        assert abs(lam[0] - want_lam) <= 1e-15, case["name"]
+        pm, pk = oracle.mix(ids, dists, vals, ko, qo, p_lm, case["mu"], lam, want_pknn=True)
+        pknn = np.array([_eval_closed_form(e) for e in case["pknn_expr"]])
+        np.testing.assert_allclose(pk[0], pknn, rtol=0, atol=1e-14, err_msg=case["name"])
+        want = want_lam * p_lm[0].astype(np.float64) + (1 - want_lam) * pknn
+        np.testing.assert_allclose(pm[0], want, rtol=0, atol=1e-14, err_msg=case["name"])
+
+
+def test_rrc_ratio_equal_to_alpha_gives_one_half():
+    # 3/10 rounds to the same double as the literal 0.3, so the logit is exactly 0
+    lam = oracle.rrc_lambda(np.array([[3.0, 7.0, 10.0], [10.0, 3.0, 5.0]]), ALPHA, TAU)
+    assert lam.tolist() == [0.5, 0.5]
+
+
+def test_rrc_known_sigmoid_values():
+    # sigmoid(ln 3) = 3/4 and sigmoid(-ln 3) = 1/4
+    for sign, want in ((1, 0.75), (-1, 0.25)):
+        ratio = ALPHA + sign * TAU * math.log(3.0)
+        lam = oracle.rrc_lambda(np.array([[ratio * 8.0, 8.0]]), ALPHA, TAU)
+        assert abs(lam[0] - want) < 1e-15
+
+
+def test_rrc_symmetry_about_alpha():
+    rng = np.random.default_rng(11)
+    d = rng.uniform(0.5, 4.0, (64, 16))
+    ratio = d.min(1) / d.max(1)
+    lam = oracle.rrc_lambda(d, ALPHA, TAU)
+    for b in range(0, 64, 7):
+        # alpha' = 2*ratio - alpha mirrors the logit: lambda' = 1 - lambda
+        mirrored = oracle.rrc_lambda(d[b:b + 1], 2 * ratio[b] - ALPHA, TAU)
+        assert abs(mirrored[0] + lam[b] - 1.0) < 1e-12
+
+
+def test_rrc_limits_and_degenerate_rows():
+    # one neighbour, or every neighbour at one distance (0 included): ratio 1
+    want = 1.0 / (1.0 + math.exp(-7.0))
+    lam = oracle.rrc_lambda(np.array([[2.5, 2.5, 2.5], [0.0, 0.0, 0.0]]), ALPHA, TAU)
+    np.testing.assert_allclose(lam, [want, want], rtol=0, atol=1e-15)
+    assert abs(oracle.rrc_lambda(np.array([[4.0]]), ALPHA, TAU)[0] - want) < 1e-15
+    # an exact match next to a far key: ratio 0
+    lam0 = oracle.rrc_lambda(np.array([[0.0, 5.0]]), ALPHA, TAU)
+    assert abs(lam0[0] - 1.0 / (1.0 + math.exp(3.0))) < 1e-15
+    with pytest.raises(RuntimeError):
+        oracle.rrc_lambda(np.array([[-1.0, 2.0]]), ALPHA, TAU)
+    with pytest.raises(RuntimeError):
+        oracle.rrc_lambda(np.array([[1.0, 2.0]]), ALPHA, 0.0)
+
+
+def test_rrc_scale_and_order_invariant_and_monotone():
+    rng = np.random.default_rng(12)
+    d = rng.uniform(0.1, 3.0, (32, 8))
+    lam = oracle.rrc_lambda(d, ALPHA, TAU)
+    np.testing.assert_allclose(oracle.rrc_lambda(d * 37.0, ALPHA, TAU), lam, rtol=1e-14, atol=0)
+    np.testing.assert_array_equal(oracle.rrc_lambda(d[:, ::-1], ALPHA, TAU), lam)
+    # moving the nearest neighbour closer lowers the ratio, hence lambda_t
+    closer = d.copy()
+    closer[np.arange(32), d.argmin(1)] *= 0.5
+    assert np.all(oracle.rrc_lambda(closer, ALPHA, TAU) < lam)
+    assert np.all((lam > 0) & (lam < 1))
+
+
+def test_mix_with_per_query_lambdas_matches_rows_of_scalar_mix():
+    rng = np.random.default_rng(13)
+    q, k, vals, p_lm = _rand_case(rng, B=4, N=120, d=8, V=30)
+    ko, qo = _one_set(4, 120)
+    ids, dists = oracle.select(q, k, "f32", ko, qo, 10)
+    lams = np.array([0.0, 0.25, 0.7, 1.0])
+    pm = oracle.mix(ids, dists, vals, ko, qo, p_lm, 0.5, lams)
+    for b, lam in enumerate(lams):
+        one = oracle.mix(ids, dists, vals, ko, qo, p_lm, 0.5, float(lam))
+        np.testing.assert_array_equal(pm[b], one[b])
+    np.testing.assert_array_equal(pm[3], p_lm[3].astype(np.float64))
+    with pytest.raises(ValueError):
+        oracle.mix(ids, dists, vals, ko, qo, p_lm, 0.5, lams[:3])
+    with pytest.raises(RuntimeError):
+        oracle.mix(ids, dists, vals, ko, qo, p_lm, 0.5, np.array([0.1, 0.2, 1.5, 0.3]))
