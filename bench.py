@@ -165,6 +165,22 @@ def main():
     topr = {"ms_per_step": round(topr_ms, 5), "alg_bytes": dist_alg_bytes + B * w.r * 8, "steps": n_topr,
             "hbm_frac": round((dist_alg_bytes + B * w.r * 8) / (topr_ms / 1e3) / 1e9 / PEAK_HBM_GBS, 4)}
 
+    # The whole step with lambda_t per query from relative retrieval confidence
+    # (alpha = 0.3, tau = 0.1) in place of the fixed lambda, the same way.
+    n_rrc = min(a.steps, 200)
+    r_start, r_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for i in range(4):
+        probs[i % 2].run_rrc(0.3, 0.1)
+    torch.cuda.synchronize()
+    r_start.record(stream)
+    for i in range(n_rrc):
+        probs[i % 2].run_rrc(0.3, 0.1)
+    r_end.record(stream)
+    torch.cuda.synchronize()
+    rrc_ms = r_start.elapsed_time(r_end) / n_rrc
+    rrc = {"ms_per_step": round(rrc_ms, 5), "queries_per_s": round(B / (rrc_ms / 1e3), 1), "steps": n_rrc,
+           "alpha": 0.3, "tau": 0.1}
+
     max_q = int(np.diff(w.query_offsets_host).max())
     matrix_core = spec.dtype in ("bf16", "f16") and spec.d % 8 == 0 and max_q >= 16
     achieved = dist_alg_bytes / (dist_launch_ms / 1e3) / 1e9
@@ -215,6 +231,7 @@ def main():
         "step_alg_bytes": step_alg_bytes,
         "step_hbm_frac": round(step_alg_bytes / (ms_per_step / 1e3) / 1e9 / PEAK_HBM_GBS, 4),
         "distance_topr": topr,
+        "rrc_step": rrc,
         "host_wall_s": round(wall, 3),
         "roofline": roofline,
         "cpu_baseline": cpu,

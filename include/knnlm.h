@@ -112,6 +112,31 @@ knn_status knn_lm_mixture(const void *queries, const void *keys, const float *ke
                           float *nbr_dists, void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * knn_lm_mixture_rrc -- the whole step with a weight of p_LM per query from
+ * relative retrieval confidence (paper Section 3.2, eq. rrc) in place of the
+ * fixed lambda: with s_i = -nbr_dists[b, i] over query b's r neighbours,
+ *
+ *   lambda_t(b) = sigmoid((min_i |s_i| / max_i |s_i| - alpha) / tau)
+ *               = sigmoid((d_(1) / d_(r) - alpha) / tau),
+ *
+ * computed in fp32 from the neighbours' fp32 distances (a query whose r
+ * distances are all 0 takes ratio 1), then p_M as in knn_lm_mixture with
+ * lambda_t(b) for query b.  Arguments as knn_lm_mixture, and:
+ *   alpha          threshold on the ratio, finite (the paper uses 0.3, or 0.2).
+ *   tau            temperature > 0 (the paper uses 0.1).
+ *   lambda_out     [B] fp32 out: lambda_t of each query, or NULL.
+ * A bad alpha or tau returns KNN_ERR_INVALID_ARG.
+ */
+knn_status knn_lm_mixture_rrc(const void *queries, const void *keys, const float *key_sqnorms,
+                              const int32_t *values, const int64_t *key_offsets,
+                              const int64_t *query_offsets, const float *p_lm, int64_t B, int64_t d,
+                              int64_t V, int64_t S, int64_t total_keys, int64_t min_keys_per_set,
+                              int64_t max_keys_per_set, int64_t max_queries_per_set, knn_dtype dtype,
+                              int32_t r, float mu, float alpha, float tau, float *lambda_out, float *p_m,
+                              int32_t *nbr_ids, float *nbr_dists, void *workspace, size_t workspace_bytes,
+                              void *stream);
+
+/*
  * knn_lm_mixture_part -- one stage of knn_lm_mixture with the same arguments.
  * KNN_PART_DISTANCES followed by either KNN_PART_SELECT_MIX or KNN_PART_SELECT
  * then KNN_PART_MIX, on one stream with one workspace, computes what
@@ -185,6 +210,18 @@ knn_status knn_mix(const int32_t *nbr_ids, const float *nbr_dists, const int32_t
                    const int64_t *key_offsets, const int64_t *query_offsets, const float *p_lm,
                    int64_t B, int64_t V, int64_t S, int32_t r, float mu, float lambda, float *p_m,
                    void *stream);
+
+/*
+ * knn_mix_rrc -- knn_mix with lambda_t per query from relative retrieval
+ * confidence (Section 3.2, eq. rrc) over the query's r caller-given distances
+ * (any order): sigmoid((min_j nbr_dists[b, j] / max_j nbr_dists[b, j] - alpha) / tau),
+ * ratio 1 if every distance is 0.  alpha finite, tau > 0; lambda_out [B] fp32
+ * out or NULL.
+ */
+knn_status knn_mix_rrc(const int32_t *nbr_ids, const float *nbr_dists, const int32_t *values,
+                       const int64_t *key_offsets, const int64_t *query_offsets, const float *p_lm,
+                       int64_t B, int64_t V, int64_t S, int32_t r, float mu, float alpha, float tau,
+                       float *lambda_out, float *p_m, void *stream);
 
 /* Static text for a status code. */
 const char *knn_status_string(knn_status status);

@@ -18,7 +18,7 @@ import torch
 from . import _lib
 from ._lib import DTYPES, PARTS, KnnError, load, status_string  # noqa: F401
 
-__all__ = ["MixtureProblem", "mixture", "distances", "key_sqnorms", "mix", "workspace_size", "KnnError",
+__all__ = ["MixtureProblem", "mixture", "distances", "key_sqnorms", "mix", "mix_rrc", "workspace_size", "KnnError",
            "load", "status_string", "abi_version"]
 
 _TORCH_DTYPES = {torch.float32: "f32", torch.bfloat16: "bf16", torch.float16: "f16"}
@@ -108,6 +108,7 @@ class MixtureProblem:
         self.p_m = torch.empty((self.B, self.V), dtype=torch.float32, device=dev)
         self.ids = torch.empty((self.B, self.r), dtype=torch.int32, device=dev)
         self.dists = torch.empty((self.B, self.r), dtype=torch.float32, device=dev)
+        self.lambdas = torch.empty(self.B, dtype=torch.float32, device=dev)  # lambda_t of run_rrc
 
     def _args(self, stream):
         return (_ptr(self.queries), _ptr(self.keys), _ptr(self.key_sqnorms), _ptr(self.values),
@@ -126,6 +127,18 @@ class MixtureProblem:
         """One knn_lm_mixture call; returns (p_m, nbr_ids, nbr_dists), valid after stream sync."""
         _lib.check("knn_lm_mixture", load().knn_lm_mixture(*self._args(stream)))
         return self.p_m, self.ids, self.dists
+
+    def run_rrc(self, alpha: float, tau: float, stream=None):
+        """One knn_lm_mixture_rrc call (lambda_t per query from relative retrieval
+        confidence); returns (p_m, nbr_ids, nbr_dists, lambda_t [B]), valid after stream sync."""
+        st = load().knn_lm_mixture_rrc(
+            _ptr(self.queries), _ptr(self.keys), _ptr(self.key_sqnorms), _ptr(self.values), _ptr(self.key_offsets),
+            _ptr(self.query_offsets), _ptr(self.p_lm), self.B, self.d, self.V, self.S, self.total_keys,
+            self.min_keys, self.max_keys, self.max_queries, self.dtype, self.r, self.mu, float(alpha), float(tau),
+            _ptr(self.lambdas), _ptr(self.p_m), _ptr(self.ids), _ptr(self.dists), _ptr(self.workspace),
+            self.workspace.numel(), _stream(stream))
+        _lib.check("knn_lm_mixture_rrc", st)
+        return self.p_m, self.ids, self.dists, self.lambdas
 
     def run_part(self, part: str, stream=None):
         """One stage ("distances", "select", "mix", "select_mix") of knn_lm_mixture on this problem's workspace."""
@@ -176,3 +189,18 @@ def mix(ids, dists, values, key_offsets, query_offsets, p_lm, mu, lam):
                         B, V, S, r, float(mu), float(lam), _ptr(out), _stream(None))
     _lib.check("knn_mix", st)
     return out
+
+
+def mix_rrc(ids, dists, values, key_offsets, query_offsets, p_lm, mu, alpha, tau):
+    """knn_mix_rrc: (p_M [B, V], lambda_t [B]) from caller-given neighbours with lambda_t
+    from relative retrieval confidence."""
+    B, r = ids.shape
+    V = p_lm.shape[1]
+    S = key_offsets.numel() - 1
+    out = torch.empty((B, V), dtype=torch.float32, device=p_lm.device)
+    lam = torch.empty(B, dtype=torch.float32, device=p_lm.device)
+    st = load().knn_mix_rrc(_ptr(ids), _ptr(dists), _ptr(values), _ptr(key_offsets), _ptr(query_offsets),
+                            _ptr(p_lm), B, V, S, r, float(mu), float(alpha), float(tau), _ptr(lam), _ptr(out),
+                            _stream(None))
+    _lib.check("knn_mix_rrc", st)
+    return out, lam

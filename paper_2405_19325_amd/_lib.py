@@ -27,9 +27,11 @@ DTYPES = {"f32": 0, "bf16": 1, "f16": 2}
 PARTS = {"distances": 1, "select": 2, "mix": 3, "select_mix": 4}
 
 _MIX_ARGS = [P, P, P, P, P, P, P, I64, I64, I64, I64, I64, I64, I64, I64, I, I32, F, F, P, P, P, P, SZ, P]
+_RRC_ARGS = [P, P, P, P, P, P, P, I64, I64, I64, I64, I64, I64, I64, I64, I, I32, F, F, F, P, P, P, P, P, SZ, P]
 
 SIGNATURES: Dict[str, tuple] = {
     "knn_lm_mixture": (I, _MIX_ARGS),
+    "knn_lm_mixture_rrc": (I, _RRC_ARGS),
     "knn_lm_mixture_part": (I, [I] + _MIX_ARGS),
     "knn_lm_mixture_workspace_size": (SZ, [I64, I64, I64, I64, I64, I64, I64, I64, I, I32]),
     "knn_lm_mixture_validate": (I, [P, P, P, P, P, P, I64, I64, I64, I64, I64, I64, I64, I64, I, I32, F, F,
@@ -37,6 +39,7 @@ SIGNATURES: Dict[str, tuple] = {
     "knn_distances": (I, [P, P, P, P, P, I64, I64, I64, I64, I64, I, P, I64, P]),
     "knn_key_sqnorms": (I, [P, I64, I64, I, P, P]),
     "knn_mix": (I, [P, P, P, P, P, P, I64, I64, I64, I32, F, F, P, P]),
+    "knn_mix_rrc": (I, [P, P, P, P, P, P, I64, I64, I64, I32, F, F, F, P, P, P]),
     "knn_status_string": (ctypes.c_char_p, [I]),
     "knn_abi_version": (I, []),
 }

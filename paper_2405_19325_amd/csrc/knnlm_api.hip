@@ -71,6 +71,13 @@ knn_status check_scalars(float mu, float lambda) {
     return KNN_OK;
 }
 
+// Relative retrieval confidence: alpha finite, tau > 0 and finite.
+knn_status check_rrc(float alpha, float tau) {
+    if (!isfinite(alpha)) return KNN_ERR_INVALID_ARG;
+    if (!finite_pos(tau)) return KNN_ERR_INVALID_ARG;
+    return KNN_OK;
+}
+
 knn_status status_of(hipError_t e) { return e == hipSuccess ? KNN_OK : KNN_ERR_HIP; }
 
 struct Call {
@@ -85,6 +92,9 @@ struct Call {
     knn_dtype dtype;
     int32_t r;
     float mu, lambda;
+    int rrc;             // 1: lambda_t per query (eq. rrc) instead of lambda
+    float alpha, tau;
+    float *lambda_out;   // [B] lambda_t, or null
     float *p_m;
     int32_t *nbr_ids;
     float *nbr_dists;
@@ -104,6 +114,7 @@ knn_status validate_part(const Call &c, int part) {
     if ((sel || mix) && (!c.nbr_ids || !c.nbr_dists)) return KNN_ERR_INVALID_ARG;
     if (mix && (!c.values || !c.p_lm || !c.p_m)) return KNN_ERR_INVALID_ARG;
     if (mix && (st = check_scalars(c.mu, c.lambda)) != KNN_OK) return st;
+    if (mix && c.rrc && (st = check_rrc(c.alpha, c.tau)) != KNN_OK) return st;
     if (dist || sel) {
         if (!c.workspace) return KNN_ERR_WORKSPACE;
         if (reinterpret_cast<uintptr_t>(c.workspace) % kAlign) return KNN_ERR_WORKSPACE;
@@ -127,6 +138,10 @@ MixArgs mix_args(const Call &c) {
     a.r = c.r;
     a.mu = c.mu;
     a.lambda = c.lambda;
+    a.rrc = c.rrc;
+    a.alpha = c.alpha;
+    a.tau = c.tau;
+    a.lambda_out = c.lambda_out;
     return a;
 }
 
@@ -208,6 +223,10 @@ Call make_call(const void *queries, const void *keys, const float *key_sqnorms, 
     c.r = r;
     c.mu = mu;
     c.lambda = lambda;
+    c.rrc = 0;
+    c.alpha = 0.0f;
+    c.tau = 1.0f;
+    c.lambda_out = nullptr;
     c.p_m = p_m;
     c.nbr_ids = nbr_ids;
     c.nbr_dists = nbr_dists;
@@ -230,6 +249,29 @@ knn_status knn_lm_mixture(const void *queries, const void *keys, const float *ke
     const Call c = make_call(queries, keys, key_sqnorms, values, key_offsets, query_offsets, p_lm, B, d, V, S,
                              total_keys, min_keys_per_set, max_keys_per_set, max_queries_per_set, dtype, r, mu,
                              lambda, p_m, nbr_ids, nbr_dists, workspace, workspace_bytes);
+    knn_status st = validate_part(c, 0);
+    if (st != KNN_OK) return st;
+    hipStream_t hs = static_cast<hipStream_t>(stream);
+    st = run_part(c, KNN_PART_DISTANCES, hs);
+    if (st != KNN_OK) return st;
+    return run_part(c, KNN_PART_SELECT_MIX, hs);
+}
+
+knn_status knn_lm_mixture_rrc(const void *queries, const void *keys, const float *key_sqnorms,
+                              const int32_t *values, const int64_t *key_offsets,
+                              const int64_t *query_offsets, const float *p_lm, int64_t B, int64_t d,
+                              int64_t V, int64_t S, int64_t total_keys, int64_t min_keys_per_set,
+                              int64_t max_keys_per_set, int64_t max_queries_per_set, knn_dtype dtype,
+                              int32_t r, float mu, float alpha, float tau, float *lambda_out, float *p_m,
+                              int32_t *nbr_ids, float *nbr_dists, void *workspace, size_t workspace_bytes,
+                              void *stream) {
+    Call c = make_call(queries, keys, key_sqnorms, values, key_offsets, query_offsets, p_lm, B, d, V, S, total_keys,
+                       min_keys_per_set, max_keys_per_set, max_queries_per_set, dtype, r, mu, 0.5f, p_m, nbr_ids,
+                       nbr_dists, workspace, workspace_bytes);
+    c.rrc = 1;
+    c.alpha = alpha;
+    c.tau = tau;
+    c.lambda_out = lambda_out;
     knn_status st = validate_part(c, 0);
     if (st != KNN_OK) return st;
     hipStream_t hs = static_cast<hipStream_t>(stream);
@@ -317,16 +359,21 @@ knn_status knn_key_sqnorms(const void *keys, int64_t n, int64_t d, knn_dtype dty
     return status_of(launch_key_sqnorms(keys, n, d, dtype, out, static_cast<hipStream_t>(stream)));
 }
 
-knn_status knn_mix(const int32_t *nbr_ids, const float *nbr_dists, const int32_t *values,
-                   const int64_t *key_offsets, const int64_t *query_offsets, const float *p_lm,
-                   int64_t B, int64_t V, int64_t S, int32_t r, float mu, float lambda, float *p_m,
-                   void *stream) {
+}  // extern "C"
+
+namespace {
+
+knn_status mix_call(const int32_t *nbr_ids, const float *nbr_dists, const int32_t *values, const int64_t *key_offsets,
+                    const int64_t *query_offsets, const float *p_lm, int64_t B, int64_t V, int64_t S, int32_t r,
+                    float mu, float lambda, int rrc, float alpha, float tau, float *lambda_out, float *p_m,
+                    void *stream) {
     if (!nbr_ids || !nbr_dists || !values || !key_offsets || !query_offsets || !p_lm || !p_m)
         return KNN_ERR_INVALID_ARG;
     if (B < 1 || V < 1 || S < 1 || r < 1) return KNN_ERR_INVALID_ARG;
     if (r > KNNLM_MAX_R || B > 0x7fffffffLL || V > 0x7fffffffLL) return KNN_ERR_UNSUPPORTED;
-    const knn_status st = check_scalars(mu, lambda);
+    knn_status st = check_scalars(mu, lambda);
     if (st != KNN_OK) return st;
+    if (rrc && (st = check_rrc(alpha, tau)) != KNN_OK) return st;
     MixArgs a{};
     a.ids = nbr_ids;
     a.dists = nbr_dists;
@@ -340,7 +387,31 @@ knn_status knn_mix(const int32_t *nbr_ids, const float *nbr_dists, const int32_t
     a.r = r;
     a.mu = mu;
     a.lambda = lambda;
+    a.rrc = rrc;
+    a.alpha = alpha;
+    a.tau = tau;
+    a.lambda_out = lambda_out;
     return status_of(launch_mix(a, B, static_cast<hipStream_t>(stream)));
+}
+
+}  // namespace
+
+extern "C" {
+
+knn_status knn_mix(const int32_t *nbr_ids, const float *nbr_dists, const int32_t *values,
+                   const int64_t *key_offsets, const int64_t *query_offsets, const float *p_lm,
+                   int64_t B, int64_t V, int64_t S, int32_t r, float mu, float lambda, float *p_m,
+                   void *stream) {
+    return mix_call(nbr_ids, nbr_dists, values, key_offsets, query_offsets, p_lm, B, V, S, r, mu, lambda, 0, 0.0f,
+                    1.0f, nullptr, p_m, stream);
+}
+
+knn_status knn_mix_rrc(const int32_t *nbr_ids, const float *nbr_dists, const int32_t *values,
+                       const int64_t *key_offsets, const int64_t *query_offsets, const float *p_lm,
+                       int64_t B, int64_t V, int64_t S, int32_t r, float mu, float alpha, float tau,
+                       float *lambda_out, float *p_m, void *stream) {
+    return mix_call(nbr_ids, nbr_dists, values, key_offsets, query_offsets, p_lm, B, V, S, r, mu, 0.5f, 1, alpha,
+                    tau, lambda_out, p_m, stream);
 }
 
 const char *knn_status_string(knn_status status) {

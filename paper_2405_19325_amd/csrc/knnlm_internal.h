@@ -77,7 +77,10 @@ struct MixArgs {
     int64_t V;
     int r;
     float mu;
-    float lambda;
+    float lambda;                // weight of p_LM (rrc == 0)
+    int rrc;                     // 1: a weight per query from relative retrieval confidence
+    float alpha, tau;            // its parameters (rrc == 1; tau > 0)
+    float *lambda_out;           // [B] the weight each query used, or null (rrc == 1)
 };
 
 DistPlan plan_distances(int64_t d, knn_dtype dtype, int64_t max_queries, const void *queries,

@@ -34,6 +34,11 @@
 // get 0; duplicates accumulate), then p_M = fmaf(lambda, p_LM, acc * ((1 -
 // lambda) / Z)), so lambda = 1 returns p_LM bit for bit.  The order of the LDS
 // atomics is not fixed, so p_kNN may differ between runs in the last bits.
+// With relative retrieval confidence (Section 3.2, eq. rrc) lambda is each
+// query's own lambda_t = sigmoid((d_(1) / d_(r) - alpha) / tau), from the
+// nearest and the r-th nearest distance (|s| is the distance); the split path
+// then writes the whole p_M row in the finish kernel, since the parts kernel
+// cannot know lambda_t.
 #include <math.h>
 
 #include "knnlm_device.h"
@@ -54,14 +59,34 @@ constexpr int kFastCap = 4096;                              // candidates the fa
 constexpr int kVocabTile = 8192;                            // mixture tile, general path
 constexpr int kVocabTileFast = 32768;                       // mixture tile, fast path (128 KiB)
 
+// What a select launch does after pi: nothing, the mixture with one lambda,
+// or the mixture with lambda_t from relative retrieval confidence.
+enum MixMode { kNoMix = 0, kMixFixed = 1, kMixRrc = 2 };
+
 struct Shared {
     uint32_t red_u[2][kNumWaves];
     uint32_t wave_tot[kNumWaves];
     float red_f[kNumWaves];
     uint32_t lo, hi, below, cnt, found, total;
     uint32_t ccount, cmin;  // split path: a part's candidates so far, and their smallest distance bits
-    float dmin;
+    float dmin, dlast;
 };
+
+// The weight of p_LM for one query from its nearest (d_first) and r-th nearest
+// (d_last) distance: m.lambda, or with RRC (eq. rrc, |s| = the distance)
+// sigmoid((d_first / d_last - alpha) / tau), a row of zero distances having
+// ratio 1.  Thread 0 records it in m.lambda_out.
+template <int MODE>
+__device__ __forceinline__ float query_lambda(const MixArgs &m, int64_t b, float d_first, float d_last) {
+    if constexpr (MODE != kMixRrc) {
+        return m.lambda;
+    } else {
+        const float ratio = d_last > 0.0f ? d_first / d_last : 1.0f;
+        const float lam = 1.0f / (1.0f + expf(-(ratio - m.alpha) / m.tau));
+        if (threadIdx.x == 0 && m.lambda_out != nullptr) m.lambda_out[b] = lam;
+        return lam;
+    }
+}
 
 __device__ __forceinline__ uint64_t sort_key(uint32_t dbits, uint32_t i) {
     return (static_cast<uint64_t>(dbits) << 32) | i;
@@ -468,17 +493,17 @@ __device__ __forceinline__ void mix_prefetch(const MixArgs &m, int64_t b, int64_
     }
 }
 
-// p_M row b: weights wj (unnormalised softmax terms, sum z) are scatter-added
+// p_M row b with weight lam of p_LM: weights wj (unnormalised softmax terms, sum z) are scatter-added
 // onto their tokens tok (-1: none) one vocabulary tile of TILE entries at a
 // time in LDS; each tile's p_LM slice sits in registers (prefetched by the
 // caller for the first tile when `first` is given) and is mixed with 16-byte
 // accesses.
 template <int PER, int TILE>
-__device__ __forceinline__ void mix_row(const float (&wj)[PER], const int32_t (&tok)[PER], float z, const MixArgs &m,
-                                        int64_t b, float *acc, const float4 (*first)[TILE / 4 / kT] = nullptr) {
+__device__ __forceinline__ void mix_row(const float (&wj)[PER], const int32_t (&tok)[PER], float z, float lam,
+                                        const MixArgs &m, int64_t b, float *acc,
+                                        const float4 (*first)[TILE / 4 / kT] = nullptr) {
     constexpr int kV4 = TILE / 4 / kT;  // float4 per thread per tile
     const int tid = threadIdx.x;
-    const float lam = m.lambda;
     const float scale = (1.0f - lam) / z;
     const float *plm = m.p_lm + b * m.V;
     float *pm = m.p_m + b * m.V;
@@ -523,8 +548,9 @@ __device__ __forceinline__ void mix_row(const float (&wj)[PER], const int32_t (&
 // ------------------------------------------------------------------ kernels
 
 // General path: any row length, r <= KNNLM_MAX_R.
-template <int CAP, bool MIX>
+template <int CAP, int MODE>
 __global__ __launch_bounds__(kT) void k_select(SelectArgs a, MixArgs m) {
+    constexpr bool MIX = MODE != kNoMix;
     __shared__ uint32_t hist[kSelectBins];
     __shared__ uint64_t cand[CAP];
     __shared__ __align__(16) float acc[MIX ? kVocabTile : 4];
@@ -556,6 +582,8 @@ __global__ __launch_bounds__(kT) void k_select(SelectArgs a, MixArgs m) {
     if constexpr (MIX) {
         const uint32_t rn = r_eff < n ? r_eff : n;
         const float dmin = rn > 0 ? __uint_as_float(static_cast<uint32_t>(cand[0] >> 32)) : 0.0f;
+        const float dlast = rn > 0 ? __uint_as_float(static_cast<uint32_t>(cand[rn - 1] >> 32)) : 0.0f;
+        const float lam = query_lambda<MODE>(m, b, dmin, dlast);
         float wj[kPer];
         int32_t tok[kPer];
         float zpart = 0.0f;
@@ -572,13 +600,14 @@ __global__ __launch_bounds__(kT) void k_select(SelectArgs a, MixArgs m) {
             }
         }
         const float z = block_sum(zpart, sh.red_f);
-        mix_row<kPer, kVocabTile>(wj, tok, z, m, b, acc);
+        mix_row<kPer, kVocabTile>(wj, tok, z, lam, m, b, acc);
     }
 }
 
 // Fast path: rows of at most kFastMaxN keys (ld <= kFastMaxN), r <= 1024.
-template <bool MIX>
+template <int MODE>
 __global__ __launch_bounds__(kT) void k_select_fast(SelectArgs a, MixArgs m) {
+    constexpr bool MIX = MODE != kNoMix;
     constexpr int kSelBytes = 2 * kFastCap * 8 + 2 * kSelectBins * 4;
     constexpr int kSmem = (MIX && kVocabTileFast * 4 > kSelBytes) ? kVocabTileFast * 4 : kSelBytes;
     constexpr int kPre = MIX ? kVocabTileFast / 4 / kT : 1;
@@ -692,10 +721,12 @@ __global__ __launch_bounds__(kT) void k_select_fast(SelectArgs a, MixArgs m) {
         int32_t tok[1] = {ok ? m.values[k0 + static_cast<int32_t>(x & 0xffffffffu)] : -1};
         const float dj = __uint_as_float(static_cast<uint32_t>(x >> 32));
         if (tid == 0) sh.dmin = ok ? dj : 0.0f;
+        if (static_cast<uint32_t>(tid) == (r_eff > 0 ? r_eff - 1 : 0u)) sh.dlast = ok ? dj : 0.0f;
         __syncthreads();
+        const float lam = query_lambda<MODE>(m, b, sh.dmin, sh.dlast);
         float wj[1] = {ok ? expf(-m.mu * (dj - sh.dmin)) : 0.0f};
         const float z = block_sum(wj[0], sh.red_f);
-        mix_row<1, kVocabTileFast>(wj, tok, z, m, b, acc, &pre);
+        mix_row<1, kVocabTileFast>(wj, tok, z, lam, m, b, acc, &pre);
     }
 }
 
@@ -717,8 +748,9 @@ __global__ __launch_bounds__(kT) void k_select_fast(SelectArgs a, MixArgs m) {
 // known (as if the row filled the stride) and corrected after.
 constexpr int kSplitSamples = 4 * kT;
 
-template <bool MIX>
+template <int MODE>
 __global__ __launch_bounds__(kT) void k_select_parts(SelectArgs a, MixArgs m, int parts) {
+    constexpr bool DENSE = MODE == kMixFixed;  // the dense term lambda * p_LM is known here
     __shared__ __align__(16) uint32_t hist[kSelectBins];
     __shared__ Shared sh;
     const int tid = threadIdx.x;
@@ -743,7 +775,7 @@ __global__ __launch_bounds__(kT) void k_select_parts(SelectArgs a, MixArgs m, in
     int64_t v0 = 0, nv = 0;
     bool vec4 = false;
     float4 pl4 = make_float4(0.f, 0.f, 0.f, 0.f);
-    if constexpr (MIX) {
+    if constexpr (DENSE) {
         const int64_t slice = ((m.V + parts - 1) / parts + 3) / 4 * 4;
         v0 = static_cast<int64_t>(part) * slice;
         nv = m.V - v0 < slice ? m.V - v0 : slice;
@@ -817,7 +849,7 @@ __global__ __launch_bounds__(kT) void k_select_parts(SelectArgs a, MixArgs m, in
         if (bits < thr)
             list[pos++] = (static_cast<uint64_t>(bits) << 32) | (static_cast<uint64_t>(static_cast<uint32_t>(i0) + e) << 12);
     }
-    if constexpr (MIX) {
+    if constexpr (DENSE) {
         const float lam = m.lambda;
         float *pm = m.p_m + b * m.V + v0;
         const float *plm = m.p_lm + b * m.V + v0;
@@ -859,8 +891,9 @@ __device__ __forceinline__ void finish_sort(uint64_t *cand, uint32_t total, uint
                                              NoHook(), keep);
 }
 
-template <bool MIX>
+template <int MODE>
 __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, int parts) {
+    constexpr bool MIX = MODE != kNoMix;
     constexpr int PER = kSplitCap / kT;
     constexpr int kSortBytes = 2 * kSplitCap * 8 + (8 << kFinishBinsLog2);
     constexpr int kSmem = MIX ? kSortBytes + kSplitCap * 4 + 16384 : kSortBytes;  // + tokens, + room for the tile
@@ -976,8 +1009,12 @@ __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, i
         if (MIX && ok) tok = m.values[k0 + id];
     }
     if (tok < 0 || tok >= m.V) tok = -1;  // tokens outside [0, V) carry no mass
-    if (MIX && tok >= 0) plm_t = plm_row[tok];  // needed only at the end
+    if (MODE == kMixFixed && tok >= 0) plm_t = plm_row[tok];  // needed only at the end
     const float d0 = __uint_as_float(static_cast<uint32_t>(cand[0] >> 32));  // the nearest distance
+    // the r-th nearest (RRC): the last of pi, in LDS in both branches above
+    const float dlast = __uint_as_float(static_cast<uint32_t>(cand[r_eff > 0 ? r_eff - 1 : 0] >> 32));
+    float4 pre[kVocabTileFast / 4 / kT];
+    if constexpr (MODE == kMixRrc) mix_prefetch(m, b, 0, pre);  // the first p_LM tile, during the write-out
     if (tid < a.r) {
         a.ids[b * a.r + tid] = ok ? static_cast<int32_t>(id) : -1;
         a.dists[b * a.r + tid] = ok ? __uint_as_float(static_cast<uint32_t>(x >> 32)) : __builtin_huge_valf();
@@ -993,11 +1030,19 @@ __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, i
         float z = 0.0f;
 #pragma unroll
         for (int w = 0; w < kNumWaves; ++w) z += sh.red_f[w];
-        const float lam = m.lambda;
+        const float lam = query_lambda<MODE>(m, b, d0, dlast);
+        if constexpr (MODE == kMixRrc) {
+            // lambda_t is known only now: the whole row, tile by tile
+            const float w1[1] = {wj};
+            const int32_t t1[1] = {tok};
+            mix_row<1, kVocabTileFast>(w1, t1, z, lam, m, b, acc, &pre);
+            return;
+        }
         const float scale = (1.0f - lam) / z;
         // Each neighbour adds its weight at its token in a vocabulary tile
         // (only the touched entries are cleared); the tokens' p_M entries are
-        // then written, duplicates writing the same value.
+        // then written, duplicates writing the same value; the parts kernel
+        // wrote lambda * p_LM everywhere else.
         for (int64_t t0 = 0; t0 < m.V; t0 += kVocabTileFast) {
             const bool in = tok >= t0 && tok < t0 + kVocabTileFast;
             if (t0 > 0) __syncthreads();  // the previous tile's reads are done
@@ -1011,6 +1056,7 @@ __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, i
 }
 
 // Standalone mixture on caller-given neighbours (any order): one workgroup per query.
+template <int MODE>
 __global__ __launch_bounds__(kT) void k_mix(MixArgs m) {
     __shared__ __align__(16) float acc[kVocabTile];
     __shared__ float red_f[kNumWaves];
@@ -1021,15 +1067,19 @@ __global__ __launch_bounds__(kT) void k_mix(MixArgs m) {
     const int64_t N = m.key_offsets[s + 1] - k0;
     float dj[kPer];
     int32_t id[kPer];
-    float dmin = __builtin_huge_valf();
+    float dmin = __builtin_huge_valf(), neg_dmax = __builtin_huge_valf();
 #pragma unroll
     for (int q = 0; q < kPer; ++q) {
         const int j = q * kT + tid;
         dj[q] = j < m.r ? m.dists[b * m.r + j] : __builtin_huge_valf();
         id[q] = j < m.r ? m.ids[b * m.r + j] : -1;
         dmin = fminf(dmin, dj[q]);
+        if (j < m.r) neg_dmax = fminf(neg_dmax, -dj[q]);
     }
     dmin = block_min(dmin, red_f);
+    float dmax = 0.0f;
+    if constexpr (MODE == kMixRrc) dmax = -block_min(neg_dmax, red_f);
+    const float lam = query_lambda<MODE>(m, b, dmin, dmax);
     float wj[kPer];
     int32_t tok[kPer];
     float zpart = 0.0f;
@@ -1041,10 +1091,10 @@ __global__ __launch_bounds__(kT) void k_mix(MixArgs m) {
         tok[q] = (j < m.r && id[q] >= 0 && id[q] < N) ? m.values[k0 + id[q]] : -1;
     }
     const float z = block_sum(zpart, red_f);
-    mix_row<kPer, kVocabTile>(wj, tok, z, m, b, acc);
+    mix_row<kPer, kVocabTile>(wj, tok, z, lam, m, b, acc);
 }
 
-template <bool MIX>
+template <int MODE>
 hipError_t launch_sel(const SelectArgs &a, const MixArgs &m, int64_t B, hipStream_t st) {
     if (B == 0) return hipSuccess;
     if (B > 0x7fffffffLL) return hipErrorInvalidConfiguration;
@@ -1053,20 +1103,20 @@ hipError_t launch_sel(const SelectArgs &a, const MixArgs &m, int64_t B, hipStrea
     const int parts = select_split_parts(B, a.ld, a.r);
     if (parts > 0) {
         if (a.cand == nullptr || a.part_count == nullptr || a.part_thr == nullptr) return hipErrorInvalidValue;
-        hipLaunchKernelGGL((k_select_parts<MIX>), dim3(static_cast<unsigned>(B * parts)), block, 0, st, a, m, parts);
+        hipLaunchKernelGGL((k_select_parts<MODE>), dim3(static_cast<unsigned>(B * parts)), block, 0, st, a, m, parts);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
-        hipLaunchKernelGGL((k_select_finish<MIX>), grid, block, 0, st, a, m, parts);
+        hipLaunchKernelGGL((k_select_finish<MODE>), grid, block, 0, st, a, m, parts);
         return hipGetLastError();
     }
     if (a.ld <= kFastMaxN && a.r <= kT) {
-        hipLaunchKernelGGL((k_select_fast<MIX>), grid, block, 0, st, a, m);
+        hipLaunchKernelGGL((k_select_fast<MODE>), grid, block, 0, st, a, m);
         return hipGetLastError();
     }
     switch (select_capacity(a.r)) {
-    case 2048: hipLaunchKernelGGL((k_select<2048, MIX>), grid, block, 0, st, a, m); break;
-    case 4096: hipLaunchKernelGGL((k_select<4096, MIX>), grid, block, 0, st, a, m); break;
-    case 8192: hipLaunchKernelGGL((k_select<8192, MIX>), grid, block, 0, st, a, m); break;
+    case 2048: hipLaunchKernelGGL((k_select<2048, MODE>), grid, block, 0, st, a, m); break;
+    case 4096: hipLaunchKernelGGL((k_select<4096, MODE>), grid, block, 0, st, a, m); break;
+    case 8192: hipLaunchKernelGGL((k_select<8192, MODE>), grid, block, 0, st, a, m); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -1090,17 +1140,20 @@ int select_capacity(int r) {
 
 hipError_t launch_select(const SelectArgs &args, int64_t B, hipStream_t stream) {
     MixArgs none{};
-    return launch_sel<false>(args, none, B, stream);
+    return launch_sel<kNoMix>(args, none, B, stream);
 }
 
 hipError_t launch_select_mix(const SelectArgs &args, const MixArgs &mix, int64_t B, hipStream_t stream) {
-    return launch_sel<true>(args, mix, B, stream);
+    return mix.rrc ? launch_sel<kMixRrc>(args, mix, B, stream) : launch_sel<kMixFixed>(args, mix, B, stream);
 }
 
 hipError_t launch_mix(const MixArgs &args, int64_t B, hipStream_t stream) {
     if (B == 0) return hipSuccess;
     if (B > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL(k_mix, dim3(static_cast<unsigned>(B)), dim3(kT), 0, stream, args);
+    if (args.rrc)
+        hipLaunchKernelGGL(k_mix<kMixRrc>, dim3(static_cast<unsigned>(B)), dim3(kT), 0, stream, args);
+    else
+        hipLaunchKernelGGL(k_mix<kMixFixed>, dim3(static_cast<unsigned>(B)), dim3(kT), 0, stream, args);
     return hipGetLastError();
 }
 

@@ -12,6 +12,13 @@ P4  distances: |d^gpu - d^oracle| <= max(1e-5 * max(1, d^oracle), bound), with
     (words per lane + 8) * 2^-23 * (||q||^2 + ||k||^2).  The GPU's order is
     ascending by its own (distance, id).
 P5  sum: |sum_w p_M^gpu - (lambda * sum p_LM + (1 - lambda))| <= 1e-5 (fp64 host sum).
+P6  (relative retrieval confidence, Section 3.2 eq. rrc) lambda_t: |lambda_t^gpu -
+    lambda_t^ref| <= (1 / (4 tau)) * dratio + 1e-6, where lambda_t^ref is the
+    oracle's sigmoid((d_(1) / d_(r) - alpha) / tau) over the oracle's fp64
+    distances of the GPU's ids, 1 / (4 tau) bounds the sigmoid's slope, and
+    dratio = (e_1 + ratio * e_r) / d_(r) is what the P4 tolerances e_1, e_r of
+    the first and r-th distance can move the ratio; 1e-6 covers the fp32
+    division and sigmoid.  P3 and P5 then take the GPU's lambda_t as lambda.
 """
 from __future__ import annotations
 
@@ -36,6 +43,7 @@ class Report:
     max_pm_err: float = 0.0
     max_dist_err_ratio: float = 0.0
     max_sum_err: float = 0.0
+    max_lambda_err_ratio: float = 0.0
     failures: List[str] = field(default_factory=list)
 
     def ok(self) -> bool:
@@ -44,7 +52,7 @@ class Report:
     def summary(self) -> str:
         return (f"{self.queries} queries, {self.exact_id_sets} identical id sets, {self.boundary_swaps} boundary "
                 f"swaps, max|dp_M|={self.max_pm_err:.3g}, max dist err/tol={self.max_dist_err_ratio:.3g}, "
-                f"max|dsum|={self.max_sum_err:.3g}")
+                f"max|dsum|={self.max_sum_err:.3g}, max lambda_t err/tol={self.max_lambda_err_ratio:.3g}")
 
 
 def dist_bound(d: int, dtype: str, qq: float, kk: float) -> float:
@@ -55,8 +63,10 @@ def dist_bound(d: int, dtype: str, qq: float, kk: float) -> float:
 
 def check_query(rep: Report, b: int, q_host: np.ndarray, keys_host: np.ndarray, dtype: str, values_set: np.ndarray,
                 p_lm_row: np.ndarray, r: int, mu: float, lam: float, gpu_ids: np.ndarray, gpu_dists: np.ndarray,
-                gpu_pm: np.ndarray, oracle_ids: Optional[np.ndarray] = None, oracle_dists: Optional[np.ndarray] = None):
-    """Apply P2-P5 to one query b with its own key set (host element arrays)."""
+                gpu_pm: np.ndarray, oracle_ids: Optional[np.ndarray] = None, oracle_dists: Optional[np.ndarray] = None,
+                rrc: Optional[tuple] = None, gpu_lambda: Optional[float] = None):
+    """Apply P2-P5 to one query b with its own key set (host element arrays); with
+    rrc = (alpha, tau) and the GPU's lambda_t also P6, and P3 / P5 use that lambda_t."""
     n = keys_host.shape[0]
     d = q_host.shape[-1]
     q1 = q_host.reshape(1, d)
@@ -99,6 +109,20 @@ def check_query(rep: Report, b: int, q_host: np.ndarray, keys_host: np.ndarray, 
         if err > tol:
             rep.failures.append(f"{tag}: neighbour {j} id {gi[j]} distance {gpu_dists[j]!r} vs oracle {d_or[j]!r}")
             break
+    # P6
+    if rrc is not None:
+        alpha, tau = rrc
+        lam_ref = float(oracle.rrc_lambda(d_or.reshape(1, r), alpha, tau)[0])
+        e1 = max(DIST_REL * max(1.0, d_or[0]), dist_bound(d, dtype, qq, float(kk[0])))
+        er = max(DIST_REL * max(1.0, d_or[r - 1]), dist_bound(d, dtype, qq, float(kk[r - 1])))
+        d1, dr = float(np.min(d_or)), float(np.max(d_or))
+        dratio = (e1 + (d1 / dr) * er) / dr if dr > 0 else 0.0
+        tol = dratio / (4.0 * tau) + 1e-6
+        err = abs(float(gpu_lambda) - lam_ref)
+        rep.max_lambda_err_ratio = max(rep.max_lambda_err_ratio, err / tol)
+        if err > tol:
+            rep.failures.append(f"{tag}: lambda_t {gpu_lambda!r} vs oracle {lam_ref!r} (tol {tol:.3g})")
+        lam = float(gpu_lambda)
     gd = gpu_dists.astype(np.float64)
     order_ok = np.all((gd[1:] > gd[:-1]) | ((gd[1:] == gd[:-1]) & (gi[1:] > gi[:-1])))
     if not order_ok:
@@ -119,14 +143,17 @@ def check_query(rep: Report, b: int, q_host: np.ndarray, keys_host: np.ndarray, 
         rep.failures.append(f"{tag}: sum p_M off by {serr:.3g}")
 
 
-def check_workload(w, p_m, ids, dists, sample: Optional[List[int]] = None) -> Report:
-    """P2-P5 on the queries `sample` (all by default) of a workload run on the GPU."""
+def check_workload(w, p_m, ids, dists, sample: Optional[List[int]] = None, rrc: Optional[tuple] = None,
+                   lambdas=None) -> Report:
+    """P2-P5 on the queries `sample` (all by default) of a workload run on the GPU; with
+    rrc = (alpha, tau) and the GPU's per-query lambdas, P6 too."""
     rep = Report()
     ko, qo = w.key_offsets_host, w.query_offsets_host
     set_of = w.set_of_query()
     B = int(qo[-1])
     sample = list(range(B)) if sample is None else list(sample)
     ids_h, dists_h = ids.cpu().numpy(), dists.cpu().numpy()
+    lam_h = None if lambdas is None else lambdas.cpu().numpy()
     by_set = {}
     for b in sample:
         by_set.setdefault(int(set_of[b]), []).append(b)
@@ -136,6 +163,7 @@ def check_workload(w, p_m, ids, dists, sample: Optional[List[int]] = None) -> Re
         for b in bs:
             q_h, _ = oracle.host_elements(w.queries[b:b + 1])
             check_query(rep, b, q_h, keys_h, dt, vals, w.p_lm[b].cpu().numpy(), w.r, w.mu, w.lam, ids_h[b],
-                        dists_h[b], p_m[b].cpu().numpy())
+                        dists_h[b], p_m[b].cpu().numpy(), rrc=rrc,
+                        gpu_lambda=None if lam_h is None else float(lam_h[b]))
         del keys_h
     return rep
