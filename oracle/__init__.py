@@ -53,6 +53,7 @@ def _load():
     lib.knn_oracle_widen.argtypes = [P, I, I64, P]
     lib.knn_oracle_sqdist.argtypes = [P, P, I, I64, I64, I64, I, P]
     lib.knn_oracle_select.argtypes = [P, P, I, I64, I64, P, P, I64, I32, I, P, P]
+    lib.knn_oracle_select_masked.argtypes = [P, P, I, I64, I64, P, P, I64, I32, P, I, P, P]
     lib.knn_oracle_mix.argtypes = [P, P, P, P, P, I64, I64, I32, P, I64, D, D, P, P]
     lib.knn_oracle_mix_lambdas.argtypes = [P, P, P, P, P, I64, I64, I32, P, I64, D, P, P, P]
     lib.knn_oracle_rrc_lambda.argtypes = [P, I64, I32, D, D, P]
@@ -105,16 +106,25 @@ def sqdist(queries: np.ndarray, keys: np.ndarray, dtype: str, nthreads: Optional
 
 
 def select(queries: np.ndarray, keys: np.ndarray, dtype: str, key_offsets: np.ndarray,
-           query_offsets: np.ndarray, r: int, nthreads: Optional[int] = None) -> Tuple[np.ndarray, np.ndarray]:
-    """Per query: the r nearest local key ids of its own set, ascending by (dist, id), and their dists."""
+           query_offsets: np.ndarray, r: int, nthreads: Optional[int] = None,
+           key_mask: Optional[np.ndarray] = None) -> Tuple[np.ndarray, np.ndarray]:
+    """Per query: the r nearest local key ids of its own set, ascending by (dist, id), and their dists.
+
+    key_mask: uint32 words, bit (i & 31) of word i >> 5 set for a masked global key row i
+    (Section 3.4); masked keys are never neighbours, and slots the unmasked keys cannot
+    fill hold id -1 and distance +inf."""
     queries, keys = _raw(queries), _raw(keys)
     ko = np.ascontiguousarray(key_offsets, dtype=np.int64)
     qo = np.ascontiguousarray(query_offsets, dtype=np.int64)
     B, d = queries.shape
     ids = np.empty((B, r), dtype=np.int32)
     dists = np.empty((B, r), dtype=np.float64)
-    rc = _load().knn_oracle_select(_ptr(queries), _ptr(keys), DTYPE_CODES[dtype], B, d, _ptr(ko), _ptr(qo),
-                                   len(ko) - 1, r, nthreads or default_threads(), _ptr(ids), _ptr(dists))
+    mask = None if key_mask is None else np.ascontiguousarray(key_mask, dtype=np.uint32)
+    if mask is not None and mask.size * 32 < int(ko[-1]):
+        raise ValueError("key_mask needs one bit per key row")
+    rc = _load().knn_oracle_select_masked(_ptr(queries), _ptr(keys), DTYPE_CODES[dtype], B, d, _ptr(ko), _ptr(qo),
+                                          len(ko) - 1, r, _ptr(mask), nthreads or default_threads(), _ptr(ids),
+                                          _ptr(dists))
     _check(rc, "select")
     return ids, dists
 

@@ -25,6 +25,12 @@
  *   5. Optionally a per-query lambda_t from relative retrieval confidence
  *      (Section 3.2, eq. rrc): sigmoid((min_i |s_i| / max_i |s_i| - alpha) / tau)
  *      over the query's r neighbours.
+ *   6. Optionally a key mask (Section 3.4, last paragraph: the keys of an
+ *      accepted span are never used again in that generation): a masked key
+ *      is never a neighbour.  If fewer than r keys of a set are unmasked, the
+ *      remaining slots of pi are absent (id -1, distance +infinity); an absent
+ *      neighbour carries no weight and takes no part in the softmax or in
+ *      lambda_t.
  *
  * Every function returns 0 on success and a negative code on a rejected
  * argument; nothing is printed.
@@ -191,10 +197,14 @@ static int check_offsets(const int64_t *off, int64_t S, int64_t *total) {
  * the r local key indices with the smallest distance, ascending by
  * (distance, index), and their fp64 squared distances.  All arrays are host
  * memory.  Returns ORC_ERR_RANGE when a set with queries has fewer than r keys.
+ *
+ * key_mask (NULL: none) holds one bit per global key row, bit (i & 31) of
+ * word i >> 5, 1 = masked: masked keys are left out, and slots pi cannot fill
+ * from the unmasked keys get id -1 and distance +infinity.
  */
-int knn_oracle_select(const void *queries, const void *keys, int dtype, int64_t B, int64_t d,
-                      const int64_t *key_offsets, const int64_t *query_offsets, int64_t S, int32_t r,
-                      int nthreads, int32_t *out_ids, double *out_dists) {
+int knn_oracle_select_masked(const void *queries, const void *keys, int dtype, int64_t B, int64_t d,
+                             const int64_t *key_offsets, const int64_t *query_offsets, int64_t S, int32_t r,
+                             const uint32_t *key_mask, int nthreads, int32_t *out_ids, double *out_dists) {
     int64_t total_keys, total_q;
     if (!queries || !keys || !key_offsets || !query_offsets || !out_ids || !out_dists) return ORC_ERR_ARG;
     if (B < 0 || d < 1 || S < 1 || r < 1 || elem_size(dtype) == 0) return ORC_ERR_ARG;
@@ -225,15 +235,30 @@ int knn_oracle_select(const void *queries, const void *keys, int dtype, int64_t 
                 order[i].d = dist[i];
                 order[i].i = i;
             }
-            qsort(order, (size_t)n, sizeof(dist_idx), by_dist_then_index);
+            int64_t kept = 0;  /* the unmasked keys, in index order */
+            for (int64_t i = 0; i < n; ++i) {
+                const int64_t g = key_offsets[s] + i;
+                if (key_mask && ((key_mask[g >> 5] >> (g & 31)) & 1u)) continue;
+                order[kept].d = dist[i];
+                order[kept].i = i;
+                ++kept;
+            }
+            qsort(order, (size_t)kept, sizeof(dist_idx), by_dist_then_index);
             for (int32_t j = 0; j < r; ++j) {
-                out_ids[b * r + j] = (int32_t)order[j].i;
-                out_dists[b * r + j] = order[j].d;
+                out_ids[b * r + j] = j < kept ? (int32_t)order[j].i : -1;
+                out_dists[b * r + j] = j < kept ? order[j].d : INFINITY;
             }
         }
     }
     free(q); free(dist); free(order);
     return 0;
+}
+
+int knn_oracle_select(const void *queries, const void *keys, int dtype, int64_t B, int64_t d,
+                      const int64_t *key_offsets, const int64_t *query_offsets, int64_t S, int32_t r,
+                      int nthreads, int32_t *out_ids, double *out_dists) {
+    return knn_oracle_select_masked(queries, keys, dtype, B, d, key_offsets, query_offsets, S, r, NULL, nthreads,
+                                    out_ids, out_dists);
 }
 
 /* ---- steps 3-4: p_kNN over pi and the lambda mixture -------------------- */
@@ -243,7 +268,10 @@ int knn_oracle_select(const void *queries, const void *keys, int dtype, int64_t 
  * order), form p_kNN by a softmax over mu * s = -mu * dist scattered onto the
  * neighbours' value tokens (duplicates accumulate), then
  * p_M = lambda * p_LM + (1 - lambda) * p_kNN.  out_pknn may be NULL.
- * Returns ORC_ERR_RANGE for an id outside its set or a value outside [0, V).
+ * An id of -1 is an absent neighbour (a slot a masked select could not fill):
+ * it carries no weight and takes no part in the softmax; with no neighbour
+ * present p_kNN is 0.  Returns ORC_ERR_RANGE for any other id outside its set
+ * or a value outside [0, V).
  */
 /* The mixture with a per-query weight of p_LM: lambdas[b] for query b. */
 int knn_oracle_mix_lambdas(const int32_t *ids, const double *dists, const int32_t *values,
@@ -273,16 +301,17 @@ int knn_oracle_mix_lambdas(const int32_t *ids, const double *dists, const int32_
             const double *dd = dists + b * r;
             const double lambda = lambdas[b];
             /* the largest mu*s over pi is -mu times the smallest distance */
-            double dmin = dd[0];
-            for (int32_t j = 1; j < r; ++j)
-                if (dd[j] < dmin) dmin = dd[j];
+            double dmin = INFINITY;
+            for (int32_t j = 0; j < r; ++j)
+                if (id[j] != -1 && dd[j] < dmin) dmin = dd[j];
             double z = 0.0;
             for (int32_t j = 0; j < r; ++j) {
-                w[j] = exp(-mu * (dd[j] - dmin));
+                w[j] = id[j] == -1 ? 0.0 : exp(-mu * (dd[j] - dmin));
                 z += w[j];
             }
             for (int64_t v = 0; v < V; ++v) pknn[v] = 0.0;
             for (int32_t j = 0; j < r; ++j) {
+                if (id[j] == -1) continue;
                 if (id[j] < 0 || id[j] >= n) { rc = ORC_ERR_RANGE; break; }
                 int32_t tok = values[key_offsets[s] + id[j]];
                 if (tok < 0 || tok >= V) { rc = ORC_ERR_RANGE; break; }
@@ -319,19 +348,22 @@ int knn_oracle_mix(const int32_t *ids, const double *dists, const int32_t *value
  *   lambda_t = sigmoid((min_i |s_i| / max_i |s_i| - alpha) / tau).
  * |s_i| is the distance, so the ratio is the smallest over the largest
  * neighbour distance.  If every neighbour is at distance 0 the ratio is 0/0;
- * it is taken as 1 (the neighbours are all equally close).  tau > 0.
+ * it is taken as 1 (the neighbours are all equally close).  tau > 0.  An
+ * absent neighbour (distance +infinity, from a masked select) is left out;
+ * with none present the ratio is taken as 1 as well.
  */
 int knn_oracle_rrc_lambda(const double *dists, int64_t B, int32_t r, double alpha, double tau,
                           double *out_lambda) {
     if (!dists || !out_lambda || B < 0 || r < 1 || !(tau > 0.0) || !isfinite(alpha)) return ORC_ERR_ARG;
     for (int64_t b = 0; b < B; ++b) {
-        double dmin = dists[b * r], dmax = dists[b * r];
-        for (int32_t j = 1; j < r; ++j) {
+        double dmin = INFINITY, dmax = 0.0;
+        for (int32_t j = 0; j < r; ++j) {
             double x = dists[b * r + j];
+            if (isinf(x) && x > 0.0) continue;
             if (x < dmin) dmin = x;
             if (x > dmax) dmax = x;
         }
-        if (dmin < 0.0) return ORC_ERR_RANGE;
+        if (dmin < 0.0 || isnan(dmin) || isnan(dmax)) return ORC_ERR_RANGE;
         double ratio = dmax > 0.0 ? dmin / dmax : 1.0;
         out_lambda[b] = 1.0 / (1.0 + exp(-(ratio - alpha) / tau));
     }
