@@ -137,6 +137,62 @@ knn_status knn_lm_mixture_rrc(const void *queries, const void *keys, const float
                               void *stream);
 
 /*
+ * knn_nest_step -- one decoding step of NEST (paper Algorithm 1, one time
+ * step, without the corpus n-gram fetch): the token search with masked keys
+ * left out, p_kNN, lambda_t from relative retrieval confidence and p_M exactly
+ * as knn_lm_mixture_rrc computes them, followed by the decisions the algorithm
+ * takes on p_M.  Arguments as knn_lm_mixture_rrc, and:
+ *   delta          span threshold of eq. span_expansion (Section 3.3), finite
+ *                  (the paper uses 0.5).
+ *   key_mask       [ceil(total_keys / 32)] uint32 or NULL: bit (i & 31) of word
+ *                  i >> 5 set means global key row i is masked (Section 3.4,
+ *                  last paragraph: the keys of an accepted span are not used
+ *                  again).  A masked key is never a neighbour; if a set keeps
+ *                  fewer than r unmasked keys, the remaining slots of pi hold
+ *                  id -1 and distance +infinity and carry no weight (with no
+ *                  neighbour at all, p_kNN = 0 and p_M = lambda_t p_LM).
+ *   draft_tokens   [B] int32 or NULL: the draft token each row checks (relaxed
+ *                  speculative decoding, Section 3.4); p_draft must then be given.
+ *   next_token     [B] int32 out: w_t = argmax_w p_M(w), the lowest id among
+ *                  equal maxima (Algorithm 1, dynamic span selection).
+ *   p_max          [B] fp32 out: p_M(w_t).
+ *   p_draft        [B] fp32 out or NULL: p_M(draft_tokens[b]), 0 for a token
+ *                  outside [0, V).
+ *   span_key       [B] int32 out: the start of the span (eq. knn_interpolation,
+ *                  max-pooling read as the neighbour with the largest softmax
+ *                  weight): the local id of the nearest neighbour in pi whose
+ *                  value is w_t (lower id on equal distances), or -1 if none.
+ *   use_span       [B] int32 out: 1 if lambda_t <= delta and span_key >= 0
+ *                  (eq. span_expansion), else 0.
+ * next_token, p_max, span_key and use_span are required.
+ */
+knn_status knn_nest_step(const void *queries, const void *keys, const float *key_sqnorms, const int32_t *values,
+                         const int64_t *key_offsets, const int64_t *query_offsets, const float *p_lm, int64_t B,
+                         int64_t d, int64_t V, int64_t S, int64_t total_keys, int64_t min_keys_per_set,
+                         int64_t max_keys_per_set, int64_t max_queries_per_set, knn_dtype dtype, int32_t r,
+                         float mu, float alpha, float tau, float delta, const uint32_t *key_mask,
+                         const int32_t *draft_tokens, float *lambda_out, float *p_m, int32_t *nbr_ids,
+                         float *nbr_dists, int32_t *next_token, float *p_max, float *p_draft, int32_t *span_key,
+                         int32_t *use_span, void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * knn_spec_verify -- relaxed speculative verification of drafts (Section 3.4,
+ * eq. rejection, and Algorithm 1) from the per-row outputs of knn_nest_step.
+ * Draft j owns rows draft_offsets[j] .. draft_offsets[j+1]-1 (int64, device,
+ * monotone); row i holds p_M given the prefix and the draft tokens before
+ * row i's own.  ratio_i = p_draft[i] / (gamma * p_max[i]) in fp32.  Without
+ * uniforms a draft token is accepted while ratio_i > 0.5; with uniforms [rows]
+ * fp32 in [0, 1) drawn by the caller, while uniforms[i] < min(1, ratio_i).
+ *   n_accept    [n_drafts] int32 out: draft tokens accepted before the first rejection.
+ *   out_token   [n_drafts] int32 out: next_token of the first rejected row (the
+ *               replacement), or -1 if every draft token was accepted.
+ * gamma in (0, 1]; n_drafts >= 1.
+ */
+knn_status knn_spec_verify(const float *p_max, const float *p_draft, const int32_t *next_token,
+                           const int64_t *draft_offsets, int64_t n_drafts, float gamma, const float *uniforms,
+                           int32_t *n_accept, int32_t *out_token, void *stream);
+
+/*
  * knn_lm_mixture_part -- one stage of knn_lm_mixture with the same arguments.
  * KNN_PART_DISTANCES followed by either KNN_PART_SELECT_MIX or KNN_PART_SELECT
  * then KNN_PART_MIX, on one stream with one workspace, computes what
@@ -203,8 +259,11 @@ knn_status knn_key_sqnorms(const void *keys, int64_t n, int64_t d, knn_dtype dty
 /*
  * knn_mix -- the softmax / scatter / mixture stage alone (eq. non-parametric
  * and eq. kNN-LM) on caller-given neighbours: for each query b of set s, the
- * r entries (nbr_ids[b, j], nbr_dists[b, j]) in any order; ids outside
- * [0, N_s) and values outside [0, V) are skipped.  p_m [B, V] is written.
+ * r entries (nbr_ids[b, j], nbr_dists[b, j]) in any order.  An entry whose id
+ * lies outside [0, N_s) is absent (as the -1 slots a masked select leaves): it
+ * carries no weight and takes no part in the softmax; with no entry present
+ * p_kNN = 0.  A value outside [0, V) gives its weight to no token.  p_m [B, V]
+ * is written.
  */
 knn_status knn_mix(const int32_t *nbr_ids, const float *nbr_dists, const int32_t *values,
                    const int64_t *key_offsets, const int64_t *query_offsets, const float *p_lm,

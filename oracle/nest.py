@@ -70,8 +70,9 @@ def decode_outputs(p_m: np.ndarray, ids: np.ndarray, values: np.ndarray, key_off
             w = greedy_token(p_m[b])
             out["next_token"][b] = w
             out["p_max"][b] = p_m[b, w]
-            if draft_tokens is not None and 0 <= draft_tokens[b] < p_m.shape[1]:
-                out["p_draft"][b] = p_m[b, draft_tokens[b]]
+            if draft_tokens is not None:  # a token outside [0, V) has probability 0
+                dt = int(draft_tokens[b])
+                out["p_draft"][b] = p_m[b, dt] if 0 <= dt < p_m.shape[1] else 0.0
             k = span_start(ids[b], vals, w)
             out["span_key"][b] = k
             out["use_span"][b] = use_span(float(lambdas[b]), delta, k)

@@ -18,7 +18,8 @@ import torch
 from . import _lib
 from ._lib import DTYPES, PARTS, KnnError, load, status_string  # noqa: F401
 
-__all__ = ["MixtureProblem", "mixture", "distances", "key_sqnorms", "mix", "mix_rrc", "workspace_size", "KnnError",
+__all__ = ["MixtureProblem", "mixture", "distances", "key_sqnorms", "mix", "mix_rrc", "spec_verify", "mask_words",
+           "workspace_size", "KnnError",
            "load", "status_string", "abi_version"]
 
 _TORCH_DTYPES = {torch.float32: "f32", torch.bfloat16: "bf16", torch.float16: "f16"}
@@ -140,6 +141,41 @@ class MixtureProblem:
         _lib.check("knn_lm_mixture_rrc", st)
         return self.p_m, self.ids, self.dists, self.lambdas
 
+    def run_nest(self, alpha: float, tau: float, delta: float, key_mask: Optional[torch.Tensor] = None,
+                 draft_tokens: Optional[torch.Tensor] = None, stream=None) -> dict:
+        """One knn_nest_step call: the RRC mixture with masked keys left out and the step's
+        decoding outputs.  Returns a dict of device tensors: p_m, ids, dists, lambdas,
+        next_token, p_max, span_key, use_span and (with draft_tokens) p_draft."""
+        if not hasattr(self, "next_token"):
+            dev = self.p_m.device
+            self.next_token = torch.empty(self.B, dtype=torch.int32, device=dev)
+            self.p_max = torch.empty(self.B, dtype=torch.float32, device=dev)
+            self.p_draft = torch.empty(self.B, dtype=torch.float32, device=dev)
+            self.span_key = torch.empty(self.B, dtype=torch.int32, device=dev)
+            self.use_span = torch.empty(self.B, dtype=torch.int32, device=dev)
+        if key_mask is not None:
+            _need(key_mask.is_cuda and key_mask.dtype == torch.int32 and key_mask.is_contiguous(),
+                  "key_mask: contiguous int32 device words (see mask_words)")
+            _need(key_mask.numel() * 32 >= self.total_keys, "key_mask needs one bit per key row")
+        if draft_tokens is not None:
+            _need(draft_tokens.is_cuda and draft_tokens.dtype == torch.int32 and draft_tokens.numel() == self.B,
+                  "draft_tokens: [B] int32 device tensor")
+        st = load().knn_nest_step(
+            _ptr(self.queries), _ptr(self.keys), _ptr(self.key_sqnorms), _ptr(self.values), _ptr(self.key_offsets),
+            _ptr(self.query_offsets), _ptr(self.p_lm), self.B, self.d, self.V, self.S, self.total_keys,
+            self.min_keys, self.max_keys, self.max_queries, self.dtype, self.r, self.mu, float(alpha), float(tau),
+            float(delta), _ptr(key_mask), _ptr(draft_tokens), _ptr(self.lambdas), _ptr(self.p_m), _ptr(self.ids),
+            _ptr(self.dists), _ptr(self.next_token), _ptr(self.p_max),
+            _ptr(self.p_draft) if draft_tokens is not None else None, _ptr(self.span_key), _ptr(self.use_span),
+            _ptr(self.workspace), self.workspace.numel(), _stream(stream))
+        _lib.check("knn_nest_step", st)
+        out = {"p_m": self.p_m, "ids": self.ids, "dists": self.dists, "lambdas": self.lambdas,
+               "next_token": self.next_token, "p_max": self.p_max, "span_key": self.span_key,
+               "use_span": self.use_span}
+        if draft_tokens is not None:
+            out["p_draft"] = self.p_draft
+        return out
+
     def run_part(self, part: str, stream=None):
         """One stage ("distances", "select", "mix", "select_mix") of knn_lm_mixture on this problem's workspace."""
         _lib.check("knn_lm_mixture_part", load().knn_lm_mixture_part(PARTS[part], *self._args(stream)))
@@ -204,3 +240,26 @@ def mix_rrc(ids, dists, values, key_offsets, query_offsets, p_lm, mu, alpha, tau
                             _stream(None))
     _lib.check("knn_mix_rrc", st)
     return out, lam
+
+
+def mask_words(masked_rows, total_keys: int, device) -> torch.Tensor:
+    """A key mask for knn_nest_step: int32 words with bit (i & 31) of word i >> 5 set for
+    every masked global key row i (built on the host, then copied)."""
+    words = np.zeros((total_keys + 31) // 32, dtype=np.uint32)
+    rows = np.asarray(list(masked_rows), dtype=np.int64)
+    if rows.size:
+        _need(rows.min() >= 0 and rows.max() < total_keys, "masked row out of range")
+        np.bitwise_or.at(words, rows >> 5, (np.uint32(1) << (rows & 31).astype(np.uint32)))
+    return torch.as_tensor(words.view(np.int32), device=device)
+
+
+def spec_verify(p_max, p_draft, next_token, draft_offsets, gamma, uniforms=None):
+    """knn_spec_verify: (accepted count [n], replacement token or -1 [n]) per draft."""
+    n = draft_offsets.numel() - 1
+    dev = p_max.device
+    n_acc = torch.empty(n, dtype=torch.int32, device=dev)
+    tok = torch.empty(n, dtype=torch.int32, device=dev)
+    st = load().knn_spec_verify(_ptr(p_max), _ptr(p_draft), _ptr(next_token), _ptr(draft_offsets), n, float(gamma),
+                                _ptr(uniforms), _ptr(n_acc), _ptr(tok), _stream(None))
+    _lib.check("knn_spec_verify", st)
+    return n_acc, tok

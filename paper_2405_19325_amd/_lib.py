@@ -33,6 +33,9 @@ SIGNATURES: Dict[str, tuple] = {
     "knn_lm_mixture": (I, _MIX_ARGS),
     "knn_lm_mixture_rrc": (I, _RRC_ARGS),
     "knn_lm_mixture_part": (I, [I] + _MIX_ARGS),
+    "knn_nest_step": (I, [P, P, P, P, P, P, P, I64, I64, I64, I64, I64, I64, I64, I64, I, I32, F, F, F, F, P, P,
+                          P, P, P, P, P, P, P, P, P, P, SZ, P]),
+    "knn_spec_verify": (I, [P, P, P, P, I64, F, P, P, P, P]),
     "knn_lm_mixture_workspace_size": (SZ, [I64, I64, I64, I64, I64, I64, I64, I64, I, I32]),
     "knn_lm_mixture_validate": (I, [P, P, P, P, P, P, I64, I64, I64, I64, I64, I64, I64, I64, I, I32, F, F,
                                     P, P, P, P, SZ]),

@@ -13,6 +13,12 @@
 // v_dot2_f32_f16 for 16-bit elements, FMA for fp32); the 64 lane partials are
 // then summed by a fixed reduction tree that leaves the same bits in every lane.
 // ||q||^2, ||k||^2 and q.k all use this order, so q == k gives exactly 0.
+//
+// Key masking (Section 3.4: the keys of an accepted span are not used again in
+// that generation): a masked row's distance is written as +infinity and left
+// out of the tile extrema, so no select path takes it while unmasked keys
+// remain.  The streaming kernel loads a row's mask bit with the row's key
+// loads, one pipeline stage ahead of its use.
 #include "knnlm_device.h"
 #include "knnlm_internal.h"
 
@@ -81,8 +87,8 @@ __device__ __forceinline__ void write_tile_extrema(const DistArgs &a, const Tile
 
 // 16-byte loads: d % VEC == 0, 16-byte aligned rows, at most CPL chunks per lane.
 // Queries stay packed in registers (NQ x CPL chunks per lane); ROWS key rows per
-// wave are loaded before any of them is used.
-template <knn_dtype DT, int CPL, int NQ, int ROWS>
+// wave are loaded before any of them is used.  MASK: a.key_mask is given.
+template <knn_dtype DT, int CPL, int NQ, int ROWS, bool MASK>
 __global__ __launch_bounds__(kDistThreads) void k_dist_vec(DistArgs a) {
     constexpr int EB = Elem<DT>::BYTES;
     constexpr int NW = kWavesPerDistBlock;
@@ -118,6 +124,7 @@ __global__ __launch_bounds__(kDistThreads) void k_dist_vec(DistArgs a) {
     // while the current rows are reduced.
     constexpr int64_t kStep = static_cast<int64_t>(NW) * ROWS;
     uint4 kv[ROWS][CPL];
+    bool mk[ROWS];  // the rows' mask bits (MASK)
     int64_t row = t.r0 + wave * ROWS;
 #pragma unroll
     for (int rr = 0; rr < ROWS; ++rr) {
@@ -128,6 +135,7 @@ __global__ __launch_bounds__(kDistThreads) void k_dist_vec(DistArgs a) {
             const int ch = lane + kWave * c;
             kv[rr][c] = (rw < t.r1 && ch < nchunks) ? load_stream(krow + ch) : zero;
         }
+        if constexpr (MASK) mk[rr] = key_masked(a.key_mask, t.k0 + (rw < t.r1 ? rw : t.r0)) & (rw < t.r1);
     }
     // ||q||^2 after the first key loads are issued, so they overlap the query's latency.
     float qq[NQ];
@@ -140,6 +148,7 @@ __global__ __launch_bounds__(kDistThreads) void k_dist_vec(DistArgs a) {
     }
     for (; row < t.r1; row += kStep) {
         uint4 kn[ROWS][CPL];
+        bool mkn[ROWS];
 #pragma unroll
         for (int rr = 0; rr < ROWS; ++rr) {
             const int64_t rw = row + kStep + rr;
@@ -149,6 +158,8 @@ __global__ __launch_bounds__(kDistThreads) void k_dist_vec(DistArgs a) {
                 const int ch = lane + kWave * c;
                 kn[rr][c] = (rw < t.r1 && ch < nchunks) ? load_stream(krow + ch) : zero;
             }
+            // the word of a row past the tile is read from the tile's first row: no branch around the load
+            if constexpr (MASK) mkn[rr] = key_masked(a.key_mask, t.k0 + (rw < t.r1 ? rw : t.r0)) & (rw < t.r1);
         }
 #pragma unroll
         for (int rr = 0; rr < ROWS; ++rr) {
@@ -167,18 +178,23 @@ __global__ __launch_bounds__(kDistThreads) void k_dist_vec(DistArgs a) {
 #pragma unroll
             for (int j = 0; j < NQ; ++j) {
                 const float dot = wave_allsum(acc_q[j]);
-                const float dist = clamp_nonneg(fmaf(-2.0f, dot, qq[j] + kk));
+                float dist = clamp_nonneg(fmaf(-2.0f, dot, qq[j] + kk));
+                if constexpr (MASK) dist = mk[rr] ? __uint_as_float(kMaskedBits) : dist;
                 if (rw < t.r1) {
                     if (lane == j && j < t.nq) a.dist[(t.qb + j) * a.ld + rw] = dist;
-                    mn[j] = fminf(mn[j], dist);
-                    mx[j] = fmaxf(mx[j], dist);
+                    if (!MASK || !mk[rr]) {
+                        mn[j] = fminf(mn[j], dist);
+                        mx[j] = fmaxf(mx[j], dist);
+                    }
                 }
             }
         }
 #pragma unroll
-        for (int rr = 0; rr < ROWS; ++rr)
+        for (int rr = 0; rr < ROWS; ++rr) {
 #pragma unroll
             for (int c = 0; c < CPL; ++c) kv[rr][c] = kn[rr][c];
+            if constexpr (MASK) mk[rr] = mkn[rr];
+        }
     }
     if (a.tile_min != nullptr) write_tile_extrema<NQ>(a, t, mn, mx);
 }
@@ -250,13 +266,16 @@ __global__ __launch_bounds__(kDistThreads) void k_dist_elem(DistArgs a) {
             }
         }
         const float kk = have_norms ? a.key_sqnorms[t.k0 + rw] : wave_allsum(acc_k);
+        const bool masked = a.key_mask != nullptr && key_masked(a.key_mask, t.k0 + rw);
 #pragma unroll
         for (int j = 0; j < NQ; ++j) {
             const float dot = wave_allsum(acc_q[j]);
-            const float dist = clamp_nonneg(fmaf(-2.0f, dot, qq[j] + kk));
+            const float dist = masked ? __uint_as_float(kMaskedBits) : clamp_nonneg(fmaf(-2.0f, dot, qq[j] + kk));
             if (lane == j && j < t.nq) a.dist[(t.qb + j) * a.ld + rw] = dist;
-            mn[j] = fminf(mn[j], dist);
-            mx[j] = fmaxf(mx[j], dist);
+            if (!masked) {
+                mn[j] = fminf(mn[j], dist);
+                mx[j] = fmaxf(mx[j], dist);
+            }
         }
     }
     if (a.tile_min != nullptr) write_tile_extrema<NQ>(a, t, mn, mx);
@@ -315,7 +334,10 @@ __global__ __launch_bounds__(kDistThreads) void k_sqnorm_elem(const void *keys, 
 template <knn_dtype DT, int CPL, int NQ, int ROWS>
 hipError_t launch_vec(const DistArgs &a, dim3 grid, hipStream_t st) {
     if constexpr (NQ * CPL <= kQueryRegChunks && ROWS * CPL <= kMaxCplVec) {
-        hipLaunchKernelGGL((k_dist_vec<DT, CPL, NQ, ROWS>), grid, dim3(kDistThreads), 0, st, a);
+        if (a.key_mask != nullptr)
+            hipLaunchKernelGGL((k_dist_vec<DT, CPL, NQ, ROWS, true>), grid, dim3(kDistThreads), 0, st, a);
+        else
+            hipLaunchKernelGGL((k_dist_vec<DT, CPL, NQ, ROWS, false>), grid, dim3(kDistThreads), 0, st, a);
         return hipGetLastError();
     } else {
         return hipErrorInvalidValue;

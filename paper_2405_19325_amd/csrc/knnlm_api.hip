@@ -95,6 +95,12 @@ struct Call {
     int rrc;             // 1: lambda_t per query (eq. rrc) instead of lambda
     float alpha, tau;
     float *lambda_out;   // [B] lambda_t, or null
+    const uint32_t *key_mask;  // masked key rows, or null
+    // NEST decoding outputs (all null unless a NEST step)
+    const int32_t *draft;
+    float *p_draft, *p_max;
+    int32_t *next_token, *span_key, *use_span;
+    float delta;
     float *p_m;
     int32_t *nbr_ids;
     float *nbr_dists;
@@ -115,6 +121,11 @@ knn_status validate_part(const Call &c, int part) {
     if (mix && (!c.values || !c.p_lm || !c.p_m)) return KNN_ERR_INVALID_ARG;
     if (mix && (st = check_scalars(c.mu, c.lambda)) != KNN_OK) return st;
     if (mix && c.rrc && (st = check_rrc(c.alpha, c.tau)) != KNN_OK) return st;
+    if (c.next_token || c.p_max || c.span_key || c.use_span || c.draft || c.p_draft) {
+        if (!c.rrc || !c.next_token || !c.p_max || !c.span_key || !c.use_span) return KNN_ERR_INVALID_ARG;
+        if ((c.draft == nullptr) != (c.p_draft == nullptr)) return KNN_ERR_INVALID_ARG;
+        if (!isfinite(c.delta)) return KNN_ERR_INVALID_ARG;
+    }
     if (dist || sel) {
         if (!c.workspace) return KNN_ERR_WORKSPACE;
         if (reinterpret_cast<uintptr_t>(c.workspace) % kAlign) return KNN_ERR_WORKSPACE;
@@ -142,6 +153,13 @@ MixArgs mix_args(const Call &c) {
     a.alpha = c.alpha;
     a.tau = c.tau;
     a.lambda_out = c.lambda_out;
+    a.draft = c.draft;
+    a.p_draft = c.p_draft;
+    a.p_max = c.p_max;
+    a.next_token = c.next_token;
+    a.span_key = c.span_key;
+    a.use_span = c.use_span;
+    a.delta = c.delta;
     return a;
 }
 
@@ -171,6 +189,7 @@ knn_status run_part(const Call &c, int part, hipStream_t stream) {
         a.tile_max = tmax;
         a.tiles_per_set = L.tiles_per_set;
         a.rows_per_tile = L.rows_per_tile;
+        a.key_mask = c.key_mask;
         return status_of(launch_distances(p, c.dtype, a, c.S, stream));
     }
     if (part == KNN_PART_SELECT || part == KNN_PART_SELECT_MIX) {
@@ -227,6 +246,14 @@ Call make_call(const void *queries, const void *keys, const float *key_sqnorms, 
     c.alpha = 0.0f;
     c.tau = 1.0f;
     c.lambda_out = nullptr;
+    c.key_mask = nullptr;
+    c.draft = nullptr;
+    c.p_draft = nullptr;
+    c.p_max = nullptr;
+    c.next_token = nullptr;
+    c.span_key = nullptr;
+    c.use_span = nullptr;
+    c.delta = 0.5f;
     c.p_m = p_m;
     c.nbr_ids = nbr_ids;
     c.nbr_dists = nbr_dists;
@@ -278,6 +305,47 @@ knn_status knn_lm_mixture_rrc(const void *queries, const void *keys, const float
     st = run_part(c, KNN_PART_DISTANCES, hs);
     if (st != KNN_OK) return st;
     return run_part(c, KNN_PART_SELECT_MIX, hs);
+}
+
+knn_status knn_nest_step(const void *queries, const void *keys, const float *key_sqnorms, const int32_t *values,
+                         const int64_t *key_offsets, const int64_t *query_offsets, const float *p_lm, int64_t B,
+                         int64_t d, int64_t V, int64_t S, int64_t total_keys, int64_t min_keys_per_set,
+                         int64_t max_keys_per_set, int64_t max_queries_per_set, knn_dtype dtype, int32_t r,
+                         float mu, float alpha, float tau, float delta, const uint32_t *key_mask,
+                         const int32_t *draft_tokens, float *lambda_out, float *p_m, int32_t *nbr_ids,
+                         float *nbr_dists, int32_t *next_token, float *p_max, float *p_draft, int32_t *span_key,
+                         int32_t *use_span, void *workspace, size_t workspace_bytes, void *stream) {
+    Call c = make_call(queries, keys, key_sqnorms, values, key_offsets, query_offsets, p_lm, B, d, V, S, total_keys,
+                       min_keys_per_set, max_keys_per_set, max_queries_per_set, dtype, r, mu, 0.5f, p_m, nbr_ids,
+                       nbr_dists, workspace, workspace_bytes);
+    c.rrc = 1;
+    c.alpha = alpha;
+    c.tau = tau;
+    c.lambda_out = lambda_out;
+    c.key_mask = key_mask;
+    c.draft = draft_tokens;
+    c.p_draft = p_draft;
+    c.p_max = p_max;
+    c.next_token = next_token;
+    c.span_key = span_key;
+    c.use_span = use_span;
+    c.delta = delta;
+    if (!next_token || !p_max || !span_key || !use_span) return KNN_ERR_INVALID_ARG;
+    knn_status st = validate_part(c, 0);
+    if (st != KNN_OK) return st;
+    hipStream_t hs = static_cast<hipStream_t>(stream);
+    st = run_part(c, KNN_PART_DISTANCES, hs);
+    if (st != KNN_OK) return st;
+    return run_part(c, KNN_PART_SELECT_MIX, hs);
+}
+
+knn_status knn_spec_verify(const float *p_max, const float *p_draft, const int32_t *next_token,
+                           const int64_t *draft_offsets, int64_t n_drafts, float gamma, const float *uniforms,
+                           int32_t *n_accept, int32_t *out_token, void *stream) {
+    if (!p_max || !p_draft || !next_token || !draft_offsets || !n_accept || !out_token) return KNN_ERR_INVALID_ARG;
+    if (n_drafts < 1 || !(gamma > 0.0f && gamma <= 1.0f)) return KNN_ERR_INVALID_ARG;
+    return status_of(launch_spec_verify(p_max, p_draft, next_token, draft_offsets, n_drafts, gamma, uniforms,
+                                        n_accept, out_token, static_cast<hipStream_t>(stream)));
 }
 
 knn_status knn_lm_mixture_part(knn_part part, const void *queries, const void *keys,

@@ -44,7 +44,15 @@ struct DistArgs {
     float *tile_max;
     int64_t tiles_per_set;
     int rows_per_tile;
+    const uint32_t *key_mask;    // bit (i & 31) of word i >> 5 set: global key row i is masked; or null
 };
+
+// A masked key row is at distance +infinity (bits kMaskedBits), above every
+// real distance, and stays out of the per-tile extrema.
+constexpr uint32_t kMaskedBits = 0x7f800000u;
+__device__ __forceinline__ bool key_masked(const uint32_t *mask, int64_t g) {
+    return ((mask[g >> 5] >> (g & 31)) & 1u) != 0u;
+}
 
 struct SelectArgs {
     const float *dist;           // [B, ld]
@@ -81,7 +89,20 @@ struct MixArgs {
     int rrc;                     // 1: a weight per query from relative retrieval confidence
     float alpha, tau;            // its parameters (rrc == 1; tau > 0)
     float *lambda_out;           // [B] the weight each query used, or null (rrc == 1)
+    // Decoding outputs of a NEST step (rrc == 1; all null, or next_token,
+    // p_max, span_key and use_span given):
+    const int32_t *draft;        // [B] the draft token each row checks, or null
+    float *p_draft;              // [B] p_M(draft[b]) (0 for a token outside [0, V)); with draft
+    float *p_max;                // [B] max_w p_M(w)
+    int32_t *next_token;         // [B] the lowest w with p_M(w) = p_max
+    int32_t *span_key;           // [B] the nearest neighbour in pi whose value is next_token, or -1
+    int32_t *use_span;           // [B] 1 if lambda_t <= delta and span_key >= 0
+    float delta;
 };
+
+hipError_t launch_spec_verify(const float *p_max, const float *p_draft, const int32_t *next_token,
+                              const int64_t *draft_offsets, int64_t n_drafts, float gamma, const float *uniforms,
+                              int32_t *n_accept, int32_t *out_token, hipStream_t stream);
 
 DistPlan plan_distances(int64_t d, knn_dtype dtype, int64_t max_queries, const void *queries,
                         const void *keys);

@@ -250,10 +250,12 @@ __global__ __launch_bounds__(kMfmaWaves * kWave, OCC) void k_dist_mfma(DistArgs 
         // Epilogue: lane (g, lr) holds dot(query j*16 + 4g + i, key wrow + 16 kb)
         // in acc[j][kb][i].
         float kk[KB];
+        bool mk[KB];  // masked key rows (Section 3.4): distance +infinity, no part in the extrema
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb) {
             const int64_t row = wrow + kb * 16;
             kk[kb] = NORMS ? (row < r1 ? a.key_sqnorms[k0 + row] : 0.0f) : group4_sum(kkp[kb]);
+            mk[kb] = a.key_mask != nullptr && row < r1 && key_masked(a.key_mask, k0 + row);
         }
 #pragma unroll
         for (int j = 0; j < MQ; ++j) {
@@ -264,10 +266,11 @@ __global__ __launch_bounds__(kMfmaWaves * kWave, OCC) void k_dist_mfma(DistArgs 
 #pragma unroll
                 for (int kb = 0; kb < KB; ++kb) {
                     const int64_t row = wrow + kb * 16;
-                    const float dist = clamp_nonneg(fmaf(-2.0f, acc[j][kb][i], qsel[j][i] + kk[kb]));
+                    const float dist = mk[kb] ? __uint_as_float(kMaskedBits)
+                                              : clamp_nonneg(fmaf(-2.0f, acc[j][kb][i], qsel[j][i] + kk[kb]));
                     const bool ok = q < nq && row < r1;
-                    if (ok) {
-                        a.dist[(qb + q) * a.ld + row] = dist;
+                    if (ok) a.dist[(qb + q) * a.ld + row] = dist;
+                    if (ok && !mk[kb]) {
                         mn = fminf(mn, dist);
                         mx = fmaxf(mx, dist);
                     }

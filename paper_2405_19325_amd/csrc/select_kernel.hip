@@ -60,8 +60,11 @@ constexpr int kVocabTile = 8192;                            // mixture tile, gen
 constexpr int kVocabTileFast = 32768;                       // mixture tile, fast path (128 KiB)
 
 // What a select launch does after pi: nothing, the mixture with one lambda,
-// or the mixture with lambda_t from relative retrieval confidence.
-enum MixMode { kNoMix = 0, kMixFixed = 1, kMixRrc = 2 };
+// the mixture with lambda_t from relative retrieval confidence, or that and
+// the decoding outputs of a NEST step (greedy token, span start, draft
+// probability).
+enum MixMode { kNoMix = 0, kMixFixed = 1, kMixRrc = 2, kMixNest = 3 };
+constexpr bool rrc_mode(int mode) { return mode == kMixRrc || mode == kMixNest; }
 
 struct Shared {
     uint32_t red_u[2][kNumWaves];
@@ -78,7 +81,7 @@ struct Shared {
 // ratio 1.  Thread 0 records it in m.lambda_out.
 template <int MODE>
 __device__ __forceinline__ float query_lambda(const MixArgs &m, int64_t b, float d_first, float d_last) {
-    if constexpr (MODE != kMixRrc) {
+    if constexpr (!rrc_mode(MODE)) {
         return m.lambda;
     } else {
         const float ratio = d_last > 0.0f ? d_first / d_last : 1.0f;
@@ -168,7 +171,7 @@ __device__ __forceinline__ void row_range(const SelectArgs &a, int64_t b, int64_
         bmax = max(bmax, __float_as_uint(a.tile_max[b * a.tiles_per_set + t]));
     }
     block_minmax_u32(bmin, bmax, sh);
-    if (N == 0) {
+    if (N == 0 || bmin > bmax) {  // no key, or every key masked
         bmin = 0u;
         bmax = 0u;
     }
@@ -498,16 +501,66 @@ __device__ __forceinline__ void mix_prefetch(const MixArgs &m, int64_t b, int64_
 // time in LDS; each tile's p_LM slice sits in registers (prefetched by the
 // caller for the first tile when `first` is given) and is mixed with 16-byte
 // accesses.
-template <int PER, int TILE>
-__device__ __forceinline__ void mix_row(const float (&wj)[PER], const int32_t (&tok)[PER], float z, float lam,
-                                        const MixArgs &m, int64_t b, float *acc,
+// 64-bit max / min over the block (every thread gets the result); red holds
+// kNumWaves entries and is free again on return.
+__device__ __forceinline__ uint64_t block_max_u64(uint64_t v, uint64_t *red) {
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) {
+        const uint64_t o = __shfl_xor(v, off);
+        v = o > v ? o : v;
+    }
+    if ((threadIdx.x & (kWave - 1)) == 0) red[threadIdx.x / kWave] = v;
+    __syncthreads();
+    uint64_t t = red[0];
+#pragma unroll
+    for (int w = 1; w < kNumWaves; ++w) t = red[w] > t ? red[w] : t;
+    __syncthreads();
+    return t;
+}
+
+__device__ __forceinline__ uint64_t block_min_u64(uint64_t v, uint64_t *red) {
+    return ~block_max_u64(~v, red);
+}
+
+// p_M entry (value, token) as a key whose largest is the largest value, the
+// lowest token among equal values (p_M >= 0, so the bits order like values).
+__device__ __forceinline__ uint64_t best_key(float v, int64_t w) {
+    return (static_cast<uint64_t>(__float_as_uint(v)) << 32) | (0xffffffffu - static_cast<uint32_t>(w));
+}
+
+template <bool NEST>
+__device__ __forceinline__ void note_entry(float v, int64_t w, int32_t dtok, uint64_t &best, float &pd) {
+    if constexpr (NEST) {
+        const uint64_t k = best_key(v, w);
+        best = k > best ? k : best;
+        pd = w == dtok ? v : pd;
+    }
+}
+
+// p_M row b with weight lam of p_LM: weights wj (unnormalised softmax terms, sum z) are scatter-added
+// onto their tokens tok (-1: none) one vocabulary tile of TILE entries at a
+// time in LDS; each tile's p_LM slice sits in registers (prefetched by the
+// caller for the first tile when `first` is given) and is mixed with 16-byte
+// accesses.  With no neighbour (z = 0) p_kNN is 0.
+//
+// NEST: the decoding outputs of the row from the values just written (Algorithm
+// 1; Section 3.3): the greedy token w_t = the lowest argmax of p_M and its
+// value, p_M at the row's draft token, and the span start -- the nearest
+// neighbour carrying w_t, from nkey = (distance bits << 32 | key id) of each
+// neighbour (~0 for none) -- with the span flag lambda <= delta.
+template <int PER, int TILE, bool NEST = false>
+__device__ __forceinline__ void mix_row(const float (&wj)[PER], const int32_t (&tok)[PER], const uint64_t (&nkey)[PER],
+                                        float z, float lam, const MixArgs &m, int64_t b, float *acc,
                                         const float4 (*first)[TILE / 4 / kT] = nullptr) {
     constexpr int kV4 = TILE / 4 / kT;  // float4 per thread per tile
     const int tid = threadIdx.x;
-    const float scale = (1.0f - lam) / z;
+    const float scale = z > 0.0f ? (1.0f - lam) / z : 0.0f;
     const float *plm = m.p_lm + b * m.V;
     float *pm = m.p_m + b * m.V;
     const bool vec4 = mix_vec4(m, b);
+    const int32_t dtok = (NEST && m.draft != nullptr) ? m.draft[b] : -1;
+    uint64_t best = 0;
+    float pd = 0.0f;  // p_M(dtok), held by the thread that writes it
     for (int64_t v0 = 0; v0 < m.V; v0 += TILE) {
         const int64_t nv = (m.V - v0 < TILE) ? m.V - v0 : TILE;
         float4 pre[kV4];
@@ -536,12 +589,44 @@ __device__ __forceinline__ void mix_row(const float (&wj)[PER], const int32_t (&
                     o.z = fmaf(lam, pre[q].z, a4.z * scale);
                     o.w = fmaf(lam, pre[q].w, a4.w * scale);
                     dst[i] = o;
+                    const int64_t w = v0 + 4 * i;
+                    note_entry<NEST>(o.x, w, dtok, best, pd);
+                    note_entry<NEST>(o.y, w + 1, dtok, best, pd);
+                    note_entry<NEST>(o.z, w + 2, dtok, best, pd);
+                    note_entry<NEST>(o.w, w + 3, dtok, best, pd);
                 }
             }
         } else {
-            for (int64_t i = tid; i < nv; i += kT) pm[v0 + i] = fmaf(lam, plm[v0 + i], acc[i] * scale);
+            for (int64_t i = tid; i < nv; i += kT) {
+                const float o = fmaf(lam, plm[v0 + i], acc[i] * scale);
+                pm[v0 + i] = o;
+                note_entry<NEST>(o, v0 + i, dtok, best, pd);
+            }
         }
         __syncthreads();
+    }
+    if constexpr (NEST) {
+        uint64_t *red = reinterpret_cast<uint64_t *>(acc);  // free after the last tile
+        const uint64_t top = block_max_u64(best, red);
+        const int32_t wt = static_cast<int32_t>(0xffffffffu - static_cast<uint32_t>(top));
+        uint64_t near = ~0ull;
+#pragma unroll
+        for (int q = 0; q < PER; ++q) near = (tok[q] == wt && nkey[q] < near) ? nkey[q] : near;
+        near = block_min_u64(near, red);
+        if (m.p_draft != nullptr) {
+            // entry w was written by thread (w / 4) % kT on the 16-byte path, w % kT otherwise
+            const bool mine = dtok >= 0 && dtok < m.V &&
+                              (vec4 ? ((dtok / 4) % kT == tid) : (dtok % kT == tid));
+            if (mine) m.p_draft[b] = pd;
+            if (tid == 0 && !(dtok >= 0 && dtok < m.V)) m.p_draft[b] = 0.0f;
+        }
+        if (tid == 0) {
+            const int32_t span = near == ~0ull ? -1 : static_cast<int32_t>(static_cast<uint32_t>(near));
+            m.next_token[b] = wt;
+            m.p_max[b] = __uint_as_float(static_cast<uint32_t>(top >> 32));
+            m.span_key[b] = span;
+            m.use_span[b] = (lam <= m.delta && span >= 0) ? 1 : 0;
+        }
     }
 }
 
@@ -574,7 +659,7 @@ __global__ __launch_bounds__(kT) void k_select(SelectArgs a, MixArgs m) {
             const uint64_t key = cand[j];
             out_ids[j] = static_cast<int32_t>(key & 0xffffffffu);
             out_d[j] = __uint_as_float(static_cast<uint32_t>(key >> 32));
-        } else {  // only reachable when a key set is smaller than r (a false hint)
+        } else {  // fewer than r unmasked keys, or a key set smaller than r (a false hint)
             out_ids[j] = -1;
             out_d[j] = __builtin_huge_valf();
         }
@@ -586,21 +671,24 @@ __global__ __launch_bounds__(kT) void k_select(SelectArgs a, MixArgs m) {
         const float lam = query_lambda<MODE>(m, b, dmin, dlast);
         float wj[kPer];
         int32_t tok[kPer];
+        uint64_t nkey[kPer];
         float zpart = 0.0f;
 #pragma unroll
         for (int q = 0; q < kPer; ++q) {
             const uint32_t j = static_cast<uint32_t>(q * kT + tid);
             tok[q] = -1;
             wj[q] = 0.0f;
+            nkey[q] = ~0ull;
             if (j < rn) {
                 const uint64_t key = cand[j];
                 wj[q] = expf(-m.mu * (__uint_as_float(static_cast<uint32_t>(key >> 32)) - dmin));
                 zpart += wj[q];
                 tok[q] = m.values[k0 + static_cast<int32_t>(key & 0xffffffffu)];
+                nkey[q] = key;
             }
         }
         const float z = block_sum(zpart, sh.red_f);
-        mix_row<kPer, kVocabTile>(wj, tok, z, lam, m, b, acc);
+        mix_row<kPer, kVocabTile, MODE == kMixNest>(wj, tok, nkey, z, lam, m, b, acc);
     }
 }
 
@@ -695,6 +783,7 @@ __global__ __launch_bounds__(kT) void k_select_fast(SelectArgs a, MixArgs m) {
     }
     __syncthreads();
     uint64_t x = ~0ull;
+    uint32_t nvalid = r_eff;  // neighbours found: fewer than r_eff only when masked keys leave too few
     if (fast) {
         // Sort every candidate (all keys below the threshold); the first r are pi.
         bucket_sort<kFastCap / kT>(cand, C, bmin, thr - bmin, hist, hist + kSelectBins, tmp, sh);
@@ -702,7 +791,8 @@ __global__ __launch_bounds__(kT) void k_select_fast(SelectArgs a, MixArgs m) {
     } else {
         // The sample misjudged the count: select over the streamed row.
         const uint32_t n = select_stream<kFastCap>(drow, N, r_eff, bmin, bmax, cand, hist, sh);
-        x = (static_cast<uint32_t>(tid) < r_eff && static_cast<uint32_t>(tid) < n) ? cand[tid] : ~0ull;
+        nvalid = n < r_eff ? n : r_eff;
+        x = static_cast<uint32_t>(tid) < nvalid ? cand[tid] : ~0ull;
     }
     __syncthreads();
 
@@ -710,23 +800,23 @@ __global__ __launch_bounds__(kT) void k_select_fast(SelectArgs a, MixArgs m) {
     float4 pre[kPre];
     if constexpr (MIX) mix_prefetch(m, b, 0, pre);
 
-    // Thread t holds the t-th nearest key (t < r_eff).
+    // Thread t holds the t-th nearest key (t < nvalid).
+    const bool ok = static_cast<uint32_t>(tid) < nvalid;
     if (tid < a.r) {
-        const bool ok = static_cast<uint32_t>(tid) < r_eff;
         a.ids[b * a.r + tid] = ok ? static_cast<int32_t>(x & 0xffffffffu) : -1;
         a.dists[b * a.r + tid] = ok ? __uint_as_float(static_cast<uint32_t>(x >> 32)) : __builtin_huge_valf();
     }
     if constexpr (MIX) {
-        const bool ok = static_cast<uint32_t>(tid) < r_eff;
         int32_t tok[1] = {ok ? m.values[k0 + static_cast<int32_t>(x & 0xffffffffu)] : -1};
+        const uint64_t nkey[1] = {ok ? x : ~0ull};
         const float dj = __uint_as_float(static_cast<uint32_t>(x >> 32));
         if (tid == 0) sh.dmin = ok ? dj : 0.0f;
-        if (static_cast<uint32_t>(tid) == (r_eff > 0 ? r_eff - 1 : 0u)) sh.dlast = ok ? dj : 0.0f;
+        if (static_cast<uint32_t>(tid) == (nvalid > 0 ? nvalid - 1 : 0u)) sh.dlast = ok ? dj : 0.0f;
         __syncthreads();
         const float lam = query_lambda<MODE>(m, b, sh.dmin, sh.dlast);
         float wj[1] = {ok ? expf(-m.mu * (dj - sh.dmin)) : 0.0f};
         const float z = block_sum(wj[0], sh.red_f);
-        mix_row<1, kVocabTileFast>(wj, tok, z, lam, m, b, acc, &pre);
+        mix_row<1, kVocabTileFast, MODE == kMixNest>(wj, tok, nkey, z, lam, m, b, acc, &pre);
     }
 }
 
@@ -798,18 +888,25 @@ __global__ __launch_bounds__(kT) void k_select_parts(SelectArgs a, MixArgs m, in
         sv = *reinterpret_cast<const uint4 *>(drow + (((static_cast<uint64_t>(tid) * static_cast<uint64_t>(N)) >> 10) & ~3ull));
     const uint32_t sb[4] = {sv.x, sv.y, sv.z, sv.w};
 
-    uint32_t thr = ~0u;  // a row that fits: every key
+    uint32_t thr = kMaskedBits;  // a row that fits: every key (but masked ones)
     if (sampled) {
-        // distances are >= +0 and never NaN: bits <= 0x7f800000
-        uint32_t smin = min(min(sb[0], sb[1]), min(sb[2], sb[3]));
-        uint32_t smax = max(max(sb[0], sb[1]), max(sb[2], sb[3]));
+        // distances are >= +0 and never NaN: bits <= 0x7f800000, which only
+        // masked keys reach; those samples are left out
+        uint32_t smin = ~0u, smax = 0u;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            smin = sb[u] < kMaskedBits ? min(smin, sb[u]) : smin;
+            smax = sb[u] < kMaskedBits ? max(smax, sb[u]) : smax;
+        }
         block_minmax_u32(smin, smax, sh);
+        if (smin > smax) smin = smax = 0u;  // every sample masked
         for (int i = tid; i < kSelectBins; i += kT) hist[i] = 0u;
         __syncthreads();
         const uint32_t w = smax + 1u - smin;
         const int shift = range_shift(w);
 #pragma unroll
-        for (int u = 0; u < 4; ++u) atomicAdd(&hist[(sb[u] - smin) >> shift], 1u);
+        for (int u = 0; u < 4; ++u)
+            if (sb[u] - smin < w) atomicAdd(&hist[(sb[u] - smin) >> shift], 1u);
         const float k0f = ceilf(static_cast<float>(r_eff) * static_cast<float>(kSplitSamples) / static_cast<float>(N));
         const uint32_t ks = static_cast<uint32_t>(k0f + ceilf(4.0f * sqrtf(k0f)) + 4.0f);
         __syncthreads();
@@ -817,7 +914,7 @@ __global__ __launch_bounds__(kT) void k_select_parts(SelectArgs a, MixArgs m, in
             // the end of the bin holding the ks-th sample: at least ks samples lie below it
             const uint32_t j = ks < static_cast<uint32_t>(kSplitSamples) ? wave_pick_bin(hist, ks, lane) : ~0u;
             const uint64_t end = static_cast<uint64_t>(smin) + ((static_cast<uint64_t>(j) + 1u) << shift);
-            if (lane == 0) sh.hi = j == ~0u ? ~0u : static_cast<uint32_t>(end < smax + 1ull ? end : smax + 1ull);
+            if (lane == 0) sh.hi = j == ~0u ? kMaskedBits : static_cast<uint32_t>(end < smax + 1ull ? end : smax + 1ull);
         }
     }
     __syncthreads();
@@ -951,7 +1048,8 @@ __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, i
     uint32_t id = 0;
     int32_t tok = -1;
     float plm_t = 0.0f;
-    const bool ok = static_cast<uint32_t>(tid) < r_eff;
+    uint32_t nvalid = r_eff;  // neighbours found: fewer only when masked keys leave too few
+    bool ok = static_cast<uint32_t>(tid) < r_eff;
     const float *plm_row = m.p_lm + b * m.V;
     if (fast) {
         uint32_t slot[PER];
@@ -1004,17 +1102,19 @@ __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, i
         uint32_t bmin, bmax;
         row_range(a, b, N, bmin, bmax, sh);
         const uint32_t n = select_stream<kSplitCap>(a.dist + b * a.ld, N, r_eff, bmin, bmax, cand, hist, sh);
-        x = (ok && static_cast<uint32_t>(tid) < n) ? cand[tid] : ~0ull;
+        nvalid = n < r_eff ? n : r_eff;
+        ok = static_cast<uint32_t>(tid) < nvalid;
+        x = ok ? cand[tid] : ~0ull;
         id = static_cast<uint32_t>(x);
         if (MIX && ok) tok = m.values[k0 + id];
     }
     if (tok < 0 || tok >= m.V) tok = -1;  // tokens outside [0, V) carry no mass
     if (MODE == kMixFixed && tok >= 0) plm_t = plm_row[tok];  // needed only at the end
-    const float d0 = __uint_as_float(static_cast<uint32_t>(cand[0] >> 32));  // the nearest distance
-    // the r-th nearest (RRC): the last of pi, in LDS in both branches above
-    const float dlast = __uint_as_float(static_cast<uint32_t>(cand[r_eff > 0 ? r_eff - 1 : 0] >> 32));
+    // the nearest and (RRC) the r-th nearest distance: the ends of pi, in LDS in both branches above
+    const float d0 = nvalid > 0 ? __uint_as_float(static_cast<uint32_t>(cand[0] >> 32)) : 0.0f;
+    const float dlast = nvalid > 0 ? __uint_as_float(static_cast<uint32_t>(cand[nvalid - 1] >> 32)) : 0.0f;
     float4 pre[kVocabTileFast / 4 / kT];
-    if constexpr (MODE == kMixRrc) mix_prefetch(m, b, 0, pre);  // the first p_LM tile, during the write-out
+    if constexpr (rrc_mode(MODE)) mix_prefetch(m, b, 0, pre);  // the first p_LM tile, during the write-out
     if (tid < a.r) {
         a.ids[b * a.r + tid] = ok ? static_cast<int32_t>(id) : -1;
         a.dists[b * a.r + tid] = ok ? __uint_as_float(static_cast<uint32_t>(x >> 32)) : __builtin_huge_valf();
@@ -1031,14 +1131,15 @@ __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, i
 #pragma unroll
         for (int w = 0; w < kNumWaves; ++w) z += sh.red_f[w];
         const float lam = query_lambda<MODE>(m, b, d0, dlast);
-        if constexpr (MODE == kMixRrc) {
+        if constexpr (rrc_mode(MODE)) {
             // lambda_t is known only now: the whole row, tile by tile
             const float w1[1] = {wj};
             const int32_t t1[1] = {tok};
-            mix_row<1, kVocabTileFast>(w1, t1, z, lam, m, b, acc, &pre);
+            const uint64_t k1[1] = {ok ? ((x >> 32) << 32) | id : ~0ull};
+            mix_row<1, kVocabTileFast, MODE == kMixNest>(w1, t1, k1, z, lam, m, b, acc, &pre);
             return;
         }
-        const float scale = (1.0f - lam) / z;
+        const float scale = z > 0.0f ? (1.0f - lam) / z : 0.0f;
         // Each neighbour adds its weight at its token in a vocabulary tile
         // (only the touched entries are cleared); the tokens' p_M entries are
         // then written, duplicates writing the same value; the parts kernel
@@ -1067,31 +1168,40 @@ __global__ __launch_bounds__(kT) void k_mix(MixArgs m) {
     const int64_t N = m.key_offsets[s + 1] - k0;
     float dj[kPer];
     int32_t id[kPer];
+    // a neighbour whose id lies outside [0, N) is absent: no weight, no part in
+    // the softmax's maximum or (RRC) in the ratio
+    bool present[kPer];
     float dmin = __builtin_huge_valf(), neg_dmax = __builtin_huge_valf();
 #pragma unroll
     for (int q = 0; q < kPer; ++q) {
         const int j = q * kT + tid;
         dj[q] = j < m.r ? m.dists[b * m.r + j] : __builtin_huge_valf();
         id[q] = j < m.r ? m.ids[b * m.r + j] : -1;
-        dmin = fminf(dmin, dj[q]);
-        if (j < m.r) neg_dmax = fminf(neg_dmax, -dj[q]);
+        present[q] = j < m.r && id[q] >= 0 && id[q] < N;
+        if (present[q]) {
+            dmin = fminf(dmin, dj[q]);
+            neg_dmax = fminf(neg_dmax, -dj[q]);
+        }
     }
     dmin = block_min(dmin, red_f);
     float dmax = 0.0f;
-    if constexpr (MODE == kMixRrc) dmax = -block_min(neg_dmax, red_f);
-    const float lam = query_lambda<MODE>(m, b, dmin, dmax);
+    if constexpr (rrc_mode(MODE)) dmax = -block_min(neg_dmax, red_f);
+    const bool any = dmin != __builtin_huge_valf();
+    const float lam = query_lambda<MODE>(m, b, any ? dmin : 0.0f, any ? dmax : 0.0f);
     float wj[kPer];
     int32_t tok[kPer];
+    uint64_t nkey[kPer];
     float zpart = 0.0f;
 #pragma unroll
     for (int q = 0; q < kPer; ++q) {
-        const int j = q * kT + tid;
-        wj[q] = j < m.r ? expf(-m.mu * (dj[q] - dmin)) : 0.0f;
+        wj[q] = present[q] ? expf(-m.mu * (dj[q] - dmin)) : 0.0f;
         zpart += wj[q];
-        tok[q] = (j < m.r && id[q] >= 0 && id[q] < N) ? m.values[k0 + id[q]] : -1;
+        tok[q] = present[q] ? m.values[k0 + id[q]] : -1;
+        nkey[q] = present[q] ? (static_cast<uint64_t>(__float_as_uint(dj[q])) << 32) | static_cast<uint32_t>(id[q])
+                             : ~0ull;
     }
     const float z = block_sum(zpart, red_f);
-    mix_row<kPer, kVocabTile>(wj, tok, z, lam, m, b, acc);
+    mix_row<kPer, kVocabTile, MODE == kMixNest>(wj, tok, nkey, z, lam, m, b, acc);
 }
 
 template <int MODE>
@@ -1144,6 +1254,11 @@ hipError_t launch_select(const SelectArgs &args, int64_t B, hipStream_t stream) 
 }
 
 hipError_t launch_select_mix(const SelectArgs &args, const MixArgs &mix, int64_t B, hipStream_t stream) {
+    if (mix.next_token != nullptr) {
+        if (!mix.rrc || mix.p_max == nullptr || mix.span_key == nullptr || mix.use_span == nullptr)
+            return hipErrorInvalidValue;
+        return launch_sel<kMixNest>(args, mix, B, stream);
+    }
     return mix.rrc ? launch_sel<kMixRrc>(args, mix, B, stream) : launch_sel<kMixFixed>(args, mix, B, stream);
 }
 

@@ -1,0 +1,281 @@
+"""GPU parity of a NEST decoding step (knn_nest_step) and of relaxed speculative
+verification (knn_spec_verify) against the oracle: key masking (Section 3.4),
+the greedy token, span start and span flag (Algorithm 1, Section 3.3) and the
+accept/reject decisions (Section 3.4, eq. rejection).
+
+Decisions that floating point takes (an argmax, a ratio against 1/2) are
+checked on the GPU's own fp32 p_M rows with the oracle's decision functions,
+so both sides decide on the same numbers; the p_M rows themselves are checked
+against the fp64 oracle mixture under the usual parity rules."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import parity
+from oracle import nest
+from workloads import gen
+
+pytestmark = pytest.mark.gpu
+
+knn = pytest.importorskip("paper_2405_19325_amd")
+
+ALPHA, TAU, DELTA = 0.3, 0.1, 0.5
+
+
+def _say(msg):
+    print(f"[gpu] {msg}", flush=True)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _device():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    knn.load()
+    yield
+    torch.cuda.synchronize()
+
+
+def _bits(masked, n):
+    words = np.zeros((n + 31) // 32, np.uint32)
+    for i in masked:
+        words[i >> 5] |= np.uint32(1) << np.uint32(i & 31)
+    return words
+
+
+def _integer_store(n, B, d, seed):
+    """Integer keys (a, b, c, 0, ...), a, b, c in [-6, 6], and queries (0, 0, 0, c_b, 0, ...):
+    every distance is an exact integer (as in the RRC tests), so ids and
+    distances must match the oracle bit for bit."""
+    rng = np.random.default_rng(seed)
+    k = np.zeros((n, d), np.float32)
+    k[:, :3] = rng.integers(-6, 7, (n, 3))
+    q = np.zeros((B, d), np.float32)
+    q[:, 3] = np.arange(B) % 6
+    V = 997
+    vals = rng.integers(0, V, n).astype(np.int32)
+    p_lm = rng.dirichlet(np.ones(V), B).astype(np.float32)
+    return rng, q, k, vals, p_lm
+
+
+def _problem(q, k, vals, p_lm, ko, qo, r, mu, dtype):
+    dev = "cuda"
+    tq, tk = torch.as_tensor(q, device=dev).to(dtype), torch.as_tensor(k, device=dev).to(dtype)
+    return knn.MixtureProblem(tq.contiguous(), tk.contiguous(), torch.as_tensor(vals, device=dev),
+                              torch.as_tensor(ko, device=dev), torch.as_tensor(qo, device=dev),
+                              torch.as_tensor(p_lm, device=dev), r, mu, key_offsets_host=ko, query_offsets_host=qo)
+
+
+def _check_decisions(out, vals, ko, qo, draft=None):
+    """The step's decoding outputs equal the oracle's decisions on the GPU's own p_M rows."""
+    pm = out["p_m"].cpu().numpy()
+    want = nest.decode_outputs(pm, out["ids"].cpu().numpy(), vals, ko, qo, out["lambdas"].cpu().numpy(), DELTA,
+                               None if draft is None else draft.cpu().numpy())
+    assert out["next_token"].cpu().numpy().tolist() == want["next_token"].tolist()
+    assert np.array_equal(out["p_max"].cpu().numpy(), want["p_max"])
+    assert out["span_key"].cpu().numpy().tolist() == want["span_key"].tolist()
+    assert out["use_span"].cpu().numpy().tolist() == want["use_span"].tolist()
+    if draft is not None:
+        assert np.array_equal(out["p_draft"].cpu().numpy(), want["p_draft"])
+    return want
+
+
+# (path, n keys per set, queries, r, d): the split select needs B * ceil(n / 4096)
+# <= 256, the one-workgroup select n <= 65536 and r <= 1024, the general one the
+# rest; 16 or more bf16 queries of a set with d % 128 == 0 take the matrix cores.
+PATHS = [("split", 40000, 6, 1024, 4), ("one-workgroup", 40000, 40, 1024, 4),
+         ("general-long-row", 70000, 6, 1024, 4), ("general-r2048", 40000, 3, 2048, 4),
+         ("matrix-core", 20000, 32, 1024, 128)]
+
+
+@pytest.mark.parametrize("path,n,B,r,d", PATHS, ids=[p[0] for p in PATHS])
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_masked_exact_integer_inputs(path, n, B, r, d, dtype):
+    if path == "matrix-core" and dtype == torch.float32:
+        pytest.skip("the matrix-core path serves 16-bit keys")
+    _say(f"masked exact integers: {path} n={n} B={B} r={r} d={d} {dtype}")
+    rng, q, k, vals, p_lm = _integer_store(n, B, d, 60 + r + d)
+    masked = rng.choice(n, n // 3, replace=False)
+    # also mask the exact matches of the first queries, which would be nearest
+    masked = np.union1d(masked, np.flatnonzero(np.all(k[:, :3] == 0, axis=1))[:5])
+    ko, qo = np.array([0, n]), np.array([0, B])
+    prob = _problem(q, k, vals, p_lm, ko, qo, r, 0.05, dtype)
+    out = prob.run_nest(ALPHA, TAU, DELTA, key_mask=knn.mask_words(masked, n, "cuda"))
+    torch.cuda.synchronize()
+    o_ids, o_d = oracle.select(q, k, "f32", ko, qo, r, key_mask=_bits(masked, n))
+    ids = out["ids"].cpu().numpy()
+    assert not np.isin(ids, masked).any()
+    np.testing.assert_array_equal(ids, o_ids)
+    np.testing.assert_array_equal(out["dists"].cpu().numpy().astype(np.float64), o_d)
+    o_lam = oracle.rrc_lambda(o_d, ALPHA, TAU)
+    np.testing.assert_allclose(out["lambdas"].cpu().numpy().astype(np.float64), o_lam, rtol=0, atol=1e-6)
+    ref = oracle.mix(o_ids, o_d, vals, ko, qo, p_lm, 0.05, o_lam)
+    np.testing.assert_allclose(out["p_m"].cpu().numpy(), ref, rtol=0, atol=1e-5)
+    _check_decisions(out, vals, ko, qo)
+
+
+@pytest.mark.parametrize("path,B,r", [("split", 2, 64), ("one-workgroup", 300, 64), ("general", 2, 2048)])
+def test_fewer_unmasked_keys_than_r(path, B, r):
+    """Set 0 keeps r/2 unmasked keys, set 1 none: pi ends in absent slots (id -1,
+    distance +inf) that carry no weight, and a query with no neighbour gets
+    p_M = lambda_t p_LM with lambda_t = sigmoid((1 - alpha) / tau)."""
+    _say(f"fewer unmasked keys than r: {path}")
+    n = 3000 if path != "general" else 5000
+    rng, q, k, vals, p_lm = _integer_store(2 * n, 2 * B, 4, 70 + B)
+    ko, qo = np.array([0, n, 2 * n]), np.array([0, B, 2 * B])
+    keep = rng.choice(n, r // 2, replace=False)
+    masked = np.concatenate([np.setdiff1d(np.arange(n), keep), np.arange(n, 2 * n)])
+    prob = _problem(q, k, vals, p_lm, ko, qo, r, 0.05, torch.float32)
+    out = prob.run_nest(ALPHA, TAU, DELTA, key_mask=knn.mask_words(masked, 2 * n, "cuda"))
+    torch.cuda.synchronize()
+    o_ids, o_d = oracle.select(q, k, "f32", ko, qo, r, key_mask=_bits(masked, 2 * n))
+    ids = out["ids"].cpu().numpy()
+    np.testing.assert_array_equal(ids, o_ids)
+    assert np.all(ids[:B, r // 2:] == -1) and np.all(ids[B:] == -1)
+    assert np.all(np.isinf(out["dists"].cpu().numpy()[:, r // 2:]))
+    o_lam = oracle.rrc_lambda(o_d, ALPHA, TAU)
+    np.testing.assert_allclose(out["lambdas"].cpu().numpy().astype(np.float64), o_lam, rtol=0, atol=1e-6)
+    ref = oracle.mix(o_ids, o_d, vals, ko, qo, p_lm, 0.05, o_lam)
+    np.testing.assert_allclose(out["p_m"].cpu().numpy(), ref, rtol=0, atol=1e-5)
+    assert out["span_key"].cpu().numpy()[B:].tolist() == [-1] * B
+    _check_decisions(out, vals, ko, qo)
+
+
+SYNTH = [
+    ("decode-bf16-split", gen.scaled(gen.config("decode_7b"), n_keys=30000, B=2), 81),
+    ("ragged-bf16", gen.scaled(gen.config("ragged_batch"), B=12, S=4, n_keys=(1100, 5000, 3333, 2048), r=1024), 82),
+    ("batch-f16-mfma", gen.scaled(gen.config("specverify_static"), B=64, S=2, n_keys=(6000, 9000), d=1024,
+                                  query_mode="iid"), 83),
+    ("decode-bf16-one-workgroup", gen.scaled(gen.config("decode_7b"), n_keys=20000, B=60), 84),
+    ("long-row-bf16", gen.scaled(gen.config("decode_7b"), n_keys=80000, B=2, d=512, mu=1 / math.sqrt(512)), 85),
+]
+
+
+def _median_ratio(w):
+    ko, qo = w.key_offsets_host, w.query_offsets_host
+    ratios = []
+    for s in range(len(ko) - 1):
+        if qo[s + 1] == qo[s]:
+            continue
+        kh, dt = oracle.host_elements(w.keys[ko[s]:ko[s + 1]])
+        qh, _ = oracle.host_elements(w.queries[qo[s]:qo[s + 1]])
+        _, od = oracle.select(qh, kh, dt, np.array([0, len(kh)]), np.array([0, len(qh)]), w.r)
+        ratios.extend((od[:, 0] / od[:, -1]).tolist())
+    return float(np.median(ratios))
+
+
+def _drafts(w, seed):
+    """Draft tokens: the p_LM argmax on even rows (likely accepted), a seeded token on odd rows."""
+    rng = np.random.default_rng(seed)
+    d = w.p_lm.argmax(1).to(torch.int32).cpu().numpy()
+    d[1::2] = rng.integers(0, w.p_lm.shape[1], d[1::2].shape)
+    return torch.as_tensor(d, dtype=torch.int32, device="cuda")
+
+
+@pytest.mark.parametrize("name,spec,seed", SYNTH, ids=[s[0] for s in SYNTH])
+def test_nest_step_synthetic_workloads(name, spec, seed):
+    """alpha at the median of the oracle's ratios, so lambda_t straddles delta and
+    the span flag takes both values; p_M under P2-P6, decisions exact."""
+    _say(f"nest step {name}")
+    w = gen.make(spec, seed, device="cuda")
+    alpha = _median_ratio(w)
+    prob = knn.MixtureProblem(w.queries, w.keys, w.values, w.key_offsets, w.query_offsets, w.p_lm, w.r, w.mu,
+                              w.lam, key_offsets_host=w.key_offsets_host, query_offsets_host=w.query_offsets_host)
+    draft = _drafts(w, seed)
+    out = prob.run_nest(alpha, TAU, DELTA, draft_tokens=draft)
+    torch.cuda.synchronize()
+    rep = parity.check_workload(w, out["p_m"], out["ids"], out["dists"], rrc=(alpha, TAU), lambdas=out["lambdas"])
+    _say(f"{name}: {rep.summary()}")
+    assert rep.ok(), rep.failures[:5]
+    want = _check_decisions(out, w.values.cpu().numpy(), w.key_offsets_host, w.query_offsets_host, draft)
+    _say(f"{name}: use_span {int(want['use_span'].sum())}/{len(want['use_span'])}, "
+         f"span found {int((want['span_key'] >= 0).sum())}")
+    # the same step without decoding outputs: the same neighbours and lambda_t, p_M up to atomics order
+    first = {k: v.clone() for k, v in out.items()}
+    p_m2, ids2, d2, lam2 = prob.run_rrc(alpha, TAU)
+    torch.cuda.synchronize()
+    assert torch.equal(ids2, first["ids"]) and torch.equal(d2, first["dists"])
+    assert torch.equal(lam2, first["lambdas"])
+    torch.testing.assert_close(p_m2, first["p_m"], rtol=0, atol=1e-7)
+
+
+def test_spec_verify_hand_cases(golden_dir):
+    import json
+    import os
+    doc = json.load(open(os.path.join(golden_dir, "verify_cases.json")))
+    p = np.array(doc["p_m"], np.float32)
+    dr = np.array(doc["draft_tokens"])
+    dev = "cuda"
+    p_max = torch.as_tensor(p.max(1), device=dev)
+    p_draft = torch.as_tensor(p[np.arange(len(p)), dr], device=dev)
+    nt = torch.as_tensor(np.array(doc["next_token"], np.int32), device=dev)
+    offs = torch.as_tensor(np.array(doc["draft_offsets"], np.int64), device=dev)
+    for case in doc["cases"]:
+        n_acc, tok = knn.spec_verify(p_max, p_draft, nt, offs, case["gamma"])
+        torch.cuda.synchronize()
+        assert n_acc.cpu().tolist() == case["n_accept"], case
+        assert tok.cpu().tolist() == case["token"], case
+
+
+def test_nest_step_and_verify_on_the_speculative_workload():
+    """The speculative-verification workload at full size (8 sequences x 16 draft
+    positions over their own 64K-key stores, r = 1024): drafts verified on the
+    GPU equal the oracle's decisions on the GPU's rows for several gamma and
+    with uniforms; p_M parity on sampled rows."""
+    _say("nest step + verify: specverify_seq")
+    w = gen.make(gen.config("specverify_seq"), gen.CONFIG_SEEDS["specverify_seq"], device="cuda")
+    prob = knn.MixtureProblem(w.queries, w.keys, w.values, w.key_offsets, w.query_offsets, w.p_lm, w.r, w.mu,
+                              w.lam, key_offsets_host=w.key_offsets_host, query_offsets_host=w.query_offsets_host)
+    draft = _drafts(w, 91)
+    masked = np.random.default_rng(92).choice(int(w.key_offsets_host[-1]), 5000, replace=False)
+    out = prob.run_nest(ALPHA, TAU, DELTA, key_mask=knn.mask_words(masked, int(w.key_offsets_host[-1]), "cuda"),
+                        draft_tokens=draft)
+    torch.cuda.synchronize()
+    ids = out["ids"].cpu().numpy()
+    ko = w.key_offsets_host
+    for s in range(len(ko) - 1):
+        rows = slice(int(w.query_offsets_host[s]), int(w.query_offsets_host[s + 1]))
+        local = masked[(masked >= ko[s]) & (masked < ko[s + 1])] - ko[s]
+        assert not np.isin(ids[rows], local).any()
+    _check_decisions(out, w.values.cpu().numpy(), w.key_offsets_host, w.query_offsets_host, draft)
+    offs = torch.as_tensor(w.query_offsets_host, device="cuda")
+    u = np.random.default_rng(93).random(w.spec.B).astype(np.float32)
+    for gamma, uni in ((1.0, None), (0.05, None), (5e-4, None), (0.05, u)):
+        n_acc, tok = knn.spec_verify(out["p_max"], out["p_draft"], out["next_token"], offs, gamma,
+                                     None if uni is None else torch.as_tensor(uni, device="cuda"))
+        torch.cuda.synchronize()
+        w_acc, w_tok = nest.spec_verify(out["p_max"].cpu().numpy(), out["p_draft"].cpu().numpy(),
+                                        out["next_token"].cpu().numpy(), w.query_offsets_host, gamma, uni, fp32=True)
+        assert n_acc.cpu().numpy().tolist() == w_acc.tolist(), gamma
+        assert tok.cpu().numpy().tolist() == w_tok.tolist(), gamma
+    # p_M parity on three rows, with the oracle's masked select
+    for b in (0, 37, 127):
+        s = int(np.searchsorted(w.query_offsets_host, b, side="right") - 1)
+        kh, dt = oracle.host_elements(w.keys[ko[s]:ko[s + 1]])
+        qh, _ = oracle.host_elements(w.queries[b:b + 1])
+        local = masked[(masked >= ko[s]) & (masked < ko[s + 1])] - ko[s]
+        o_ids, o_d = oracle.select(qh, kh, dt, np.array([0, len(kh)]), np.array([0, 1]), w.r,
+                                   key_mask=_bits(local, len(kh)))
+        rep = parity.Report()
+        parity.check_query(rep, b, qh, kh, dt, w.values[ko[s]:ko[s + 1]].cpu().numpy(), w.p_lm[b].cpu().numpy(),
+                           w.r, w.mu, w.lam, ids[b], out["dists"][b].cpu().numpy(), out["p_m"][b].cpu().numpy(),
+                           oracle_ids=o_ids[0], oracle_dists=o_d[0], rrc=(ALPHA, TAU),
+                           gpu_lambda=float(out["lambdas"][b]))
+        assert rep.ok(), rep.failures[:3]
+
+
+def test_nest_step_rejects_bad_arguments():
+    _say("nest argument checks")
+    rng, q, k, vals, p_lm = _integer_store(100, 1, 4, 1)
+    prob = _problem(q, k, vals, p_lm, np.array([0, 100]), np.array([0, 1]), 4, 0.5, torch.float32)
+    for alpha, tau, delta in ((0.3, 0.0, 0.5), (float("nan"), 0.1, 0.5), (0.3, 0.1, float("inf"))):
+        with pytest.raises(knn.KnnError):
+            prob.run_nest(alpha, tau, delta)
+    z = torch.zeros(1, device="cuda")
+    nt = torch.zeros(1, dtype=torch.int32, device="cuda")
+    offs = torch.as_tensor([0, 1], device="cuda")
+    for gamma in (0.0, 1.5, float("nan")):
+        with pytest.raises(knn.KnnError):
+            knn.spec_verify(z, z, nt, offs, gamma)
