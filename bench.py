@@ -181,6 +181,30 @@ def main():
     rrc = {"ms_per_step": round(rrc_ms, 5), "queries_per_s": round(B / (rrc_ms / 1e3), 1), "steps": n_rrc,
            "alpha": 0.3, "tau": 0.1}
 
+    # One NEST decoding step (knn_nest_step: masked keys left out, lambda_t,
+    # greedy token, span start, draft probability; then knn_spec_verify over
+    # each set's rows as one draft), 1% of the keys masked, the p_LM argmax as
+    # each row's draft token, the same way.
+    n_nest = min(a.steps, 200)
+    masked = np.random.default_rng(seed + 1).choice(total_keys, total_keys // 100, replace=False)
+    mask = knn.mask_words(masked, total_keys, dev)
+    draft = w.p_lm.argmax(1).to(torch.int32)
+    offs = w.query_offsets
+    for i in range(4):
+        o = probs[i % 2].run_nest(0.3, 0.1, 0.5, key_mask=mask, draft_tokens=draft)
+        knn.spec_verify(o["p_max"], o["p_draft"], o["next_token"], offs, 5e-2)
+    torch.cuda.synchronize()
+    n_start, n_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    n_start.record(stream)
+    for i in range(n_nest):
+        o = probs[i % 2].run_nest(0.3, 0.1, 0.5, key_mask=mask, draft_tokens=draft)
+        knn.spec_verify(o["p_max"], o["p_draft"], o["next_token"], offs, 5e-2)
+    n_end.record(stream)
+    torch.cuda.synchronize()
+    nest_ms = n_start.elapsed_time(n_end) / n_nest
+    nest_step = {"ms_per_step": round(nest_ms, 5), "queries_per_s": round(B / (nest_ms / 1e3), 1), "steps": n_nest,
+                 "alpha": 0.3, "tau": 0.1, "delta": 0.5, "gamma": 0.05, "masked_keys": int(len(masked))}
+
     max_q = int(np.diff(w.query_offsets_host).max())
     matrix_core = spec.dtype in ("bf16", "f16") and spec.d % 8 == 0 and max_q >= 16
     achieved = dist_alg_bytes / (dist_launch_ms / 1e3) / 1e9
@@ -232,6 +256,7 @@ def main():
         "step_hbm_frac": round(step_alg_bytes / (ms_per_step / 1e3) / 1e9 / PEAK_HBM_GBS, 4),
         "distance_topr": topr,
         "rrc_step": rrc,
+        "nest_step": nest_step,
         "host_wall_s": round(wall, 3),
         "roofline": roofline,
         "cpu_baseline": cpu,
