@@ -5,7 +5,7 @@
 #include <stdint.h>
 
 #include "knnlm.h"
-#include "knnlm_internal.h"
+#include "select_internal.h"
 
 namespace {
 

@@ -132,6 +132,18 @@ __device__ __forceinline__ float wave_allmin(float v) {
     return fminf(fminf(r0, r1), fminf(r2, r3));
 }
 
+__device__ __forceinline__ float wave_allmax(float v) {
+    v = fmaxf(v, dpp_f32<0xB1>(v));
+    v = fmaxf(v, dpp_f32<0x4E>(v));
+    v = fmaxf(v, dpp_f32<0x141>(v));
+    v = fmaxf(v, dpp_f32<0x140>(v));
+    const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+    const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+    const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+    const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+    return fmaxf(fmaxf(r0, r1), fmaxf(r2, r3));
+}
+
 __device__ __forceinline__ uint32_t wave_allmin_u32(uint32_t v) {
     v = min(v, dpp_u32<0xB1>(v, v));
     v = min(v, dpp_u32<0x4E>(v, v));

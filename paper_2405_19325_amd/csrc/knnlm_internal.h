@@ -1,4 +1,6 @@
-// Internal interfaces between the C ABI (knnlm_api.hip) and the kernels.
+// Internal interfaces between the C ABI (knnlm_api.hip) and the kernels:
+// shared constants and the distance stage (the select and mixture stages are
+// in select_internal.h).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -54,56 +56,6 @@ __device__ __forceinline__ bool key_masked(const uint32_t *mask, int64_t g) {
     return ((mask[g >> 5] >> (g & 31)) & 1u) != 0u;
 }
 
-struct SelectArgs {
-    const float *dist;           // [B, ld]
-    const float *tile_min;       // [B, tiles_per_set] or null
-    const float *tile_max;
-    const int64_t *key_offsets;
-    const int64_t *query_offsets;
-    int64_t S;
-    int64_t ld;
-    int64_t tiles_per_set;
-    int rows_per_tile;
-    int r;
-    int32_t *ids;                // [B, r]
-    float *dists;                // [B, r]
-    uint64_t *cand;              // split select: [B, parts, kSplitKeys] candidate keys, or null
-    uint32_t *part_count;        // split select: [B, parts] candidates per part
-    uint32_t *part_min;          // split select: [B, parts] smallest candidate distance bits per part
-    uint32_t *part_thr;          // split select: [B] threshold on the distance bits
-};
-
-struct MixArgs {
-    const int32_t *ids;          // [B, r]
-    const float *dists;          // [B, r]
-    const int32_t *values;
-    const int64_t *key_offsets;
-    const int64_t *query_offsets;
-    const float *p_lm;           // [B, V]
-    float *p_m;                  // [B, V]
-    int64_t S;
-    int64_t V;
-    int r;
-    float mu;
-    float lambda;                // weight of p_LM (rrc == 0)
-    int rrc;                     // 1: a weight per query from relative retrieval confidence
-    float alpha, tau;            // its parameters (rrc == 1; tau > 0)
-    float *lambda_out;           // [B] the weight each query used, or null (rrc == 1)
-    // Decoding outputs of a NEST step (rrc == 1; all null, or next_token,
-    // p_max, span_key and use_span given):
-    const int32_t *draft;        // [B] the draft token each row checks, or null
-    float *p_draft;              // [B] p_M(draft[b]) (0 for a token outside [0, V)); with draft
-    float *p_max;                // [B] max_w p_M(w)
-    int32_t *next_token;         // [B] the lowest w with p_M(w) = p_max
-    int32_t *span_key;           // [B] the nearest neighbour in pi whose value is next_token, or -1
-    int32_t *use_span;           // [B] 1 if lambda_t <= delta and span_key >= 0
-    float delta;
-};
-
-hipError_t launch_spec_verify(const float *p_max, const float *p_draft, const int32_t *next_token,
-                              const int64_t *draft_offsets, int64_t n_drafts, float gamma, const float *uniforms,
-                              int32_t *n_accept, int32_t *out_token, hipStream_t stream);
-
 DistPlan plan_distances(int64_t d, knn_dtype dtype, int64_t max_queries, const void *queries,
                         const void *keys);
 
@@ -121,19 +73,4 @@ hipError_t launch_distances_mfma(int mq, knn_dtype dtype, const DistArgs &args, 
                                  hipStream_t stream);
 hipError_t launch_key_sqnorms(const void *keys, int64_t n, int64_t d, knn_dtype dtype, float *out,
                               hipStream_t stream);
-int select_capacity(int r);
-// Split select: rows of at most kSplitMaxN keys are cut into parts of
-// kSplitKeys keys, one workgroup each, when r <= kSplitMaxR and the parts of
-// all queries fit in one pass of the chip.  Returns the parts per query, or 0
-// when a query's row is selected by a single workgroup.
-constexpr int kSplitKeys = 4096;
-constexpr int kSplitCap = 4096;
-constexpr int64_t kSplitMaxN = 65536;
-constexpr int kSplitMaxR = 1024;
-constexpr int64_t kSplitMaxBlocks = 256;
-int select_split_parts(int64_t B, int64_t ld, int r);
-hipError_t launch_select(const SelectArgs &args, int64_t B, hipStream_t stream);
-hipError_t launch_select_mix(const SelectArgs &args, const MixArgs &mix, int64_t B, hipStream_t stream);
-hipError_t launch_mix(const MixArgs &args, int64_t B, hipStream_t stream);
-
 }  // namespace knnlm

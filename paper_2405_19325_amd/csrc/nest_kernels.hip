@@ -9,37 +9,49 @@
 // replacement) are written; with no rejection every token is accepted and the
 // replacement is -1.  All arithmetic in fp32, as ratio = p / (gamma * max).
 //
-// One thread per draft: the rows are a handful per draft and the data a few
-// bytes each, so the kernel is launch-bound.
+// One wave per draft: 64 rows at a time load together (nothing waits on a
+// decision before the loads), a ballot finds the first rejection.
 #include "knnlm_device.h"
-#include "knnlm_internal.h"
+#include "select_internal.h"
 
 namespace knnlm {
 
 namespace {
 
-constexpr int kVerifyThreads = 256;
+constexpr int kVerifyWaves = 4;  // drafts per workgroup
 
-__global__ __launch_bounds__(kVerifyThreads) void k_spec_verify(const float *p_max, const float *p_draft,
-                                                                const int32_t *next_token,
-                                                                const int64_t *draft_offsets, int64_t n_drafts,
-                                                                float gamma, const float *uniforms,
-                                                                int32_t *n_accept, int32_t *out_token) {
-    const int64_t j = static_cast<int64_t>(blockIdx.x) * kVerifyThreads + threadIdx.x;
-    if (j >= n_drafts) return;
+__global__ __launch_bounds__(kVerifyWaves * kWave) void k_spec_verify(const float *p_max, const float *p_draft,
+                                                                     const int32_t *next_token,
+                                                                     const int64_t *draft_offsets, int64_t n_drafts,
+                                                                     float gamma, const float *uniforms,
+                                                                     int32_t *n_accept, int32_t *out_token) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t j = static_cast<int64_t>(blockIdx.x) * kVerifyWaves + threadIdx.x / kWave;
+    if (j >= n_drafts) return;  // the whole wave
     const int64_t r0 = draft_offsets[j], r1 = draft_offsets[j + 1];
-    int32_t accepted = static_cast<int32_t>(r1 - r0), token = -1;
-    for (int64_t i = r0; i < r1; ++i) {
-        const float ratio = p_draft[i] / (gamma * p_max[i]);
-        const bool ok = uniforms != nullptr ? uniforms[i] < fminf(1.0f, ratio) : ratio > 0.5f;
-        if (!ok) {
-            accepted = static_cast<int32_t>(i - r0);
-            token = next_token[i];
+    int64_t accepted = r1 - r0;
+    int32_t token = -1;
+    for (int64_t base = r0; base < r1; base += kWave) {
+        const int64_t i = base + lane;
+        const bool in = i < r1;
+        const int64_t at = in ? i : r0;  // rows past the draft read its first row (unused)
+        const float pd = p_draft[at], pm = p_max[at];
+        const int32_t nt = next_token[at];
+        const float u = uniforms != nullptr ? uniforms[at] : 0.0f;
+        const float ratio = pd / (gamma * pm);
+        const bool ok = uniforms != nullptr ? u < fminf(1.0f, ratio) : ratio > 0.5f;
+        const uint64_t rejected = __ballot(in && !ok);
+        if (rejected != 0ull) {
+            const int first = __ffsll(static_cast<unsigned long long>(rejected)) - 1;
+            accepted = base - r0 + first;
+            token = __shfl(nt, first);
             break;
         }
     }
-    n_accept[j] = accepted;
-    out_token[j] = token;
+    if (lane == 0) {
+        n_accept[j] = static_cast<int32_t>(accepted);
+        out_token[j] = token;
+    }
 }
 
 }  // namespace
@@ -48,9 +60,9 @@ hipError_t launch_spec_verify(const float *p_max, const float *p_draft, const in
                               const int64_t *draft_offsets, int64_t n_drafts, float gamma, const float *uniforms,
                               int32_t *n_accept, int32_t *out_token, hipStream_t stream) {
     if (n_drafts <= 0) return hipSuccess;
-    const int64_t blocks = (n_drafts + kVerifyThreads - 1) / kVerifyThreads;
+    const int64_t blocks = (n_drafts + kVerifyWaves - 1) / kVerifyWaves;
     if (blocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL(k_spec_verify, dim3(static_cast<unsigned>(blocks)), dim3(kVerifyThreads), 0, stream, p_max,
+    hipLaunchKernelGGL(k_spec_verify, dim3(static_cast<unsigned>(blocks)), dim3(kVerifyWaves * kWave), 0, stream, p_max,
                        p_draft, next_token, draft_offsets, n_drafts, gamma, uniforms, n_accept, out_token);
     return hipGetLastError();
 }

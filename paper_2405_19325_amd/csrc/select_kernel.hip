@@ -42,7 +42,7 @@
 #include <math.h>
 
 #include "knnlm_device.h"
-#include "knnlm_internal.h"
+#include "select_internal.h"
 
 namespace knnlm {
 
@@ -501,6 +501,50 @@ __device__ __forceinline__ void mix_prefetch(const MixArgs &m, int64_t b, int64_
 // time in LDS; each tile's p_LM slice sits in registers (prefetched by the
 // caller for the first tile when `first` is given) and is mixed with 16-byte
 // accesses.
+// The largest value over the block and the lowest index holding it (every
+// thread gets both): v >= 0 or -1 for "none"; red holds 2 * kNumWaves words
+// and is free again on return.
+__device__ __forceinline__ void block_argmax(float &v, uint32_t &i, uint32_t *red) {
+    const float m = wave_allmax(v);
+    const uint32_t j = wave_allmin_u32(v == m ? i : ~0u);
+    const int wave = threadIdx.x / kWave;
+    if ((threadIdx.x & (kWave - 1)) == 0) {
+        red[wave] = __float_as_uint(m);
+        red[kNumWaves + wave] = j;
+    }
+    __syncthreads();
+    float bm = __uint_as_float(red[0]);
+    uint32_t bj = red[kNumWaves];
+#pragma unroll
+    for (int w = 1; w < kNumWaves; ++w) {
+        const float x = __uint_as_float(red[w]);
+        const uint32_t y = red[kNumWaves + w];
+        if (x > bm || (x == bm && y < bj)) {
+            bm = x;
+            bj = y;
+        }
+    }
+    __syncthreads();
+    v = bm;
+    i = bj;
+}
+
+// Entry (v, w) of a p_M row seen by this thread: entries come in increasing w,
+// so a strictly larger value keeps the lowest token among equal values.
+template <bool NEST>
+__device__ __forceinline__ void note_entry(float v, int32_t w, int32_t dtok, float &bv, int32_t &bw, float &pd) {
+    if constexpr (NEST) {
+        bw = v > bv ? w : bw;
+        bv = v > bv ? v : bv;
+        pd = w == dtok ? v : pd;
+    }
+}
+
+// p_M row b with weight lam of p_LM: weights wj (unnormalised softmax terms, sum z) are scatter-added
+// onto their tokens tok (-1: none) one vocabulary tile of TILE entries at a
+// time in LDS; each tile's p_LM slice sits in registers (prefetched by the
+// caller for the first tile when `first` is given) and is mixed with 16-byte
+// accesses.
 // 64-bit max / min over the block (every thread gets the result); red holds
 // kNumWaves entries and is free again on return.
 __device__ __forceinline__ uint64_t block_max_u64(uint64_t v, uint64_t *red) {
@@ -559,8 +603,9 @@ __device__ __forceinline__ void mix_row(const float (&wj)[PER], const int32_t (&
     float *pm = m.p_m + b * m.V;
     const bool vec4 = mix_vec4(m, b);
     const int32_t dtok = (NEST && m.draft != nullptr) ? m.draft[b] : -1;
-    uint64_t best = 0;
-    float pd = 0.0f;  // p_M(dtok), held by the thread that writes it
+    float bv = -1.0f;  // this thread's largest entry and its token
+    int32_t bw = 0;
+    float pd = 0.0f;   // p_M(dtok), held by the thread that writes it
     for (int64_t v0 = 0; v0 < m.V; v0 += TILE) {
         const int64_t nv = (m.V - v0 < TILE) ? m.V - v0 : TILE;
         float4 pre[kV4];
@@ -589,30 +634,42 @@ __device__ __forceinline__ void mix_row(const float (&wj)[PER], const int32_t (&
                     o.z = fmaf(lam, pre[q].z, a4.z * scale);
                     o.w = fmaf(lam, pre[q].w, a4.w * scale);
                     dst[i] = o;
-                    const int64_t w = v0 + 4 * i;
-                    note_entry<NEST>(o.x, w, dtok, best, pd);
-                    note_entry<NEST>(o.y, w + 1, dtok, best, pd);
-                    note_entry<NEST>(o.z, w + 2, dtok, best, pd);
-                    note_entry<NEST>(o.w, w + 3, dtok, best, pd);
+                    const int32_t w = static_cast<int32_t>(v0 + 4 * i);
+                    note_entry<NEST>(o.x, w, dtok, bv, bw, pd);
+                    note_entry<NEST>(o.y, w + 1, dtok, bv, bw, pd);
+                    note_entry<NEST>(o.z, w + 2, dtok, bv, bw, pd);
+                    note_entry<NEST>(o.w, w + 3, dtok, bv, bw, pd);
                 }
             }
         } else {
             for (int64_t i = tid; i < nv; i += kT) {
                 const float o = fmaf(lam, plm[v0 + i], acc[i] * scale);
                 pm[v0 + i] = o;
-                note_entry<NEST>(o, v0 + i, dtok, best, pd);
+                note_entry<NEST>(o, static_cast<int32_t>(v0 + i), dtok, bv, bw, pd);
             }
         }
         __syncthreads();
     }
     if constexpr (NEST) {
-        uint64_t *red = reinterpret_cast<uint64_t *>(acc);  // free after the last tile
-        const uint64_t top = block_max_u64(best, red);
-        const int32_t wt = static_cast<int32_t>(0xffffffffu - static_cast<uint32_t>(top));
-        uint64_t near = ~0ull;
+        uint32_t *red = reinterpret_cast<uint32_t *>(acc);  // free after the last tile
+        float top = bv;
+        uint32_t wtu = static_cast<uint32_t>(bw);
+        block_argmax(top, wtu, red);
+        const int32_t wt = static_cast<int32_t>(wtu);
+        // the nearest neighbour carrying wt: smallest (distance bits, id)
+        uint32_t nd = ~0u, ni = ~0u;
 #pragma unroll
-        for (int q = 0; q < PER; ++q) near = (tok[q] == wt && nkey[q] < near) ? nkey[q] : near;
-        near = block_min_u64(near, red);
+        for (int q = 0; q < PER; ++q) {
+            const uint32_t kd = static_cast<uint32_t>(nkey[q] >> 32), ki = static_cast<uint32_t>(nkey[q]);
+            const bool better = tok[q] == wt && (kd < nd || (kd == nd && ki < ni));
+            nd = better ? kd : nd;
+            ni = better ? ki : ni;
+        }
+        // over the block: the argmax of 0x7f800000 - bits (a nonnegative float
+        // that grows as the distance shrinks), lowest id among equals
+        float nearness = nd == ~0u ? -1.0f : __uint_as_float(kMaskedBits - nd);
+        block_argmax(nearness, ni, red);
+        const uint64_t near = nearness < 0.0f ? ~0ull : static_cast<uint64_t>(ni);
         if (m.p_draft != nullptr) {
             // entry w was written by thread (w / 4) % kT on the 16-byte path, w % kT otherwise
             const bool mine = dtok >= 0 && dtok < m.V &&
@@ -623,7 +680,7 @@ __device__ __forceinline__ void mix_row(const float (&wj)[PER], const int32_t (&
         if (tid == 0) {
             const int32_t span = near == ~0ull ? -1 : static_cast<int32_t>(static_cast<uint32_t>(near));
             m.next_token[b] = wt;
-            m.p_max[b] = __uint_as_float(static_cast<uint32_t>(top >> 32));
+            m.p_max[b] = top;
             m.span_key[b] = span;
             m.use_span[b] = (lam <= m.delta && span >= 0) ? 1 : 0;
         }

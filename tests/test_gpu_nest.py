@@ -279,3 +279,39 @@ def test_nest_step_rejects_bad_arguments():
     for gamma in (0.0, 1.5, float("nan")):
         with pytest.raises(knn.KnnError):
             knn.spec_verify(z, z, nt, offs, gamma)
+
+
+def test_spec_verify_long_and_empty_drafts():
+    """Drafts of 0, 1, 63, 64, 65 and 300 rows (one wave reads 64 rows at a time)
+    with p_M(draft) = 0.9 max everywhere but at planted rows (0.1 max): row 0 of
+    the 1-row draft, the last row of the 64-row draft, row 64 of the 65-row
+    draft, rows 130 and 200 of the 300-row draft.  Exact expected counts at
+    gamma = 1 and 0.6; with uniforms the GPU's decisions equal the oracle's in
+    fp32."""
+    _say("spec verify: long and empty drafts")
+    rng = np.random.default_rng(94)
+    lens = [0, 1, 63, 64, 65, 300]
+    offs = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    n = int(offs[-1])
+    p_max = rng.uniform(0.05, 0.9, n).astype(np.float32)
+    f = np.full(n, 0.9, np.float32)
+    for dft, row in ((1, 0), (3, 63), (4, 64), (5, 130), (5, 200)):
+        f[offs[dft] + row] = 0.1
+    p_draft = (p_max * f).astype(np.float32)
+    nt = rng.integers(0, 32000, n).astype(np.int32)
+    u = rng.random(n).astype(np.float32)
+    dev = "cuda"
+    t = lambda a: torch.as_tensor(a, device=dev)
+    want_acc = [0, 0, 63, 63, 64, 130]
+    want_tok = [-1, int(nt[offs[1]]), -1, int(nt[offs[3] + 63]), int(nt[offs[4] + 64]), int(nt[offs[5] + 130])]
+    for gamma in (1.0, 0.6):
+        n_acc, tok = knn.spec_verify(t(p_max), t(p_draft), t(nt), t(offs), gamma)
+        torch.cuda.synchronize()
+        assert n_acc.cpu().numpy().tolist() == want_acc, gamma
+        assert tok.cpu().numpy().tolist() == want_tok, gamma
+    for gamma in (1.0, 0.95):
+        n_acc, tok = knn.spec_verify(t(p_max), t(p_draft), t(nt), t(offs), gamma, t(u))
+        torch.cuda.synchronize()
+        w_acc, w_tok = nest.spec_verify(p_max, p_draft, nt, offs, gamma, u, fp32=True)
+        assert n_acc.cpu().numpy().tolist() == w_acc.tolist(), gamma
+        assert tok.cpu().numpy().tolist() == w_tok.tolist(), gamma
