@@ -399,15 +399,17 @@ bool vector_path_ok(int64_t d, knn_dtype dtype, const void *queries, const void 
 }  // namespace
 
 bool mfma_shape(int64_t d, knn_dtype dtype, int64_t max_queries) {
-    return (dtype == KNN_BF16 || dtype == KNN_F16) && d % kMfmaSpan == 0 && max_queries >= kMfmaMinQueries;
+    return (dtype == KNN_BF16 || dtype == KNN_F16) && d % kMfmaSpan == 0 && d <= kMfmaMaxD &&
+           max_queries >= kMfmaMinQueries;
 }
 
 // Key rows per distance workgroup.  Streaming path: about 1 MiB of keys, fewer
 // when the launch would otherwise have under 512 workgroups (two per CU,
-// measured best).  Matrix-core path: one 256-key pass.  A multiple of 8 rows.
+// measured best).  Matrix-core path: whole 128-key passes, enough of them for
+// a deep pipeline.  A multiple of 8 rows.
 // Depends on sizes only, so the workspace size does not depend on pointers.
 int dist_tile_rows(int64_t d, knn_dtype dtype, int64_t S, int64_t max_keys, int64_t max_queries) {
-    if (mfma_shape(d, dtype, max_queries)) return mfma_keys_per_pass();
+    if (mfma_shape(d, dtype, max_queries)) return mfma_tile_rows(d);
     const int64_t step = 8;
     const int64_t row_bytes = d * elem_bytes(dtype);
     int64_t rpt = (1024 * 1024) / (row_bytes > 0 ? row_bytes : 1);

@@ -59,12 +59,13 @@ __device__ __forceinline__ bool key_masked(const uint32_t *mask, int64_t g) {
 DistPlan plan_distances(int64_t d, knn_dtype dtype, int64_t max_queries, const void *queries,
                         const void *keys);
 
-// The matrix-core path serves 16-bit keys with d % kMfmaSpan == 0 when at
-// least kMfmaMinQueries queries share a key set.
+// The matrix-core path serves 16-bit keys with d % kMfmaSpan == 0 and
+// d <= kMfmaMaxD when at least kMfmaMinQueries queries share a key set.
 constexpr int kMfmaMinQueries = 16;
 constexpr int kMfmaSpan = 128;
+constexpr int64_t kMfmaMaxD = 65536;  // a 4096-row tile stays under 2^31 bytes
 bool mfma_shape(int64_t d, knn_dtype dtype, int64_t max_queries);
-int mfma_keys_per_pass();
+int mfma_tile_rows(int64_t d);
 int dist_tile_rows(int64_t d, knn_dtype dtype, int64_t S, int64_t max_keys, int64_t max_queries);
 
 hipError_t launch_distances(const DistPlan &plan, knn_dtype dtype, const DistArgs &args, int64_t S,

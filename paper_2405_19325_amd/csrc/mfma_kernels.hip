@@ -7,26 +7,25 @@
 // products form a dense [queries x d] . [d x keys] contraction: every key
 // element is used by up to 128 queries, so streaming the keys from HBM once
 // needs up to 128 flop per byte -- beyond the vector ALUs, within the
-// matrix cores.  A workgroup of 4 waves takes passes of 4 * KB blocks of 16
-// keys of one set (KB per wave) against up to 128 of the set's queries (MQ
-// blocks of 16).  d is walked in spans of 128 elements.  In MFMA step c of a
-// span, lane l holds key (or query) row l % 16 and elements 32c + 8 (l / 16)
-// .. +8 -- the same elements for both operands, so the contraction is exact
-// up to fp32 rounding -- and one 16-byte non-temporal load per (key block, c)
-// reads 64 contiguous bytes of each of 16 rows.  The workgroup stages each
-// span of its queries (read from cache: every workgroup of the set shares
-// them) in LDS in exactly the A-operand lane order, so staging and reading
-// are contiguous 1 KB accesses.  The next span's keys and queries load while
-// v_mfma_f32_16x16x32 (bf16 or f16, fp32 accumulate) runs over the current
-// one for every (query block, key block) pair; every load is unconditional,
-// since a branch around loads makes the compiler wait for all loads in flight.
+// matrix cores.  A workgroup of 4 waves takes passes of 128 keys of one set
+// (two blocks of 16 per wave) against up to 128 of the set's queries (MQ
+// blocks of 16), walking d in spans of 128 elements (256 bytes of a row).
 //
-// ||k||^2 (unless precomputed) and ||q||^2 are dot2 chains over the same
-// elements.  The summation order differs from the matrix cores', so unlike the
-// streaming kernel a query equal to a key gives a distance of a few ulps of
-// ||q||^2 + ||k||^2 rather than exactly 0 (clamped at 0 from below).
-#include <type_traits>
-
+// Each span of the pass's keys and queries goes HBM -> registers -> LDS -> the
+// matrix cores.  The global loads are coalesced: 16 lanes read one row's
+// 256-byte span, a wave instruction four whole rows.  The LDS copy is
+// swizzled -- chunk c (16 bytes) of row n sits at slot n * 16 + (c ^ (n % 16))
+// -- so that both the row-wise writes and the fragment reads (lane l reads
+// row l % 16, chunk 4 * step + l / 16) touch every bank once.  In MFMA step c
+// lane l holds key (or query) row l % 16 and elements 32c + 8 (l / 16) .. +8
+// of the span -- the same elements for both operands, so the contraction is
+// exact up to fp32 rounding -- for v_mfma_f32_16x16x32 (bf16 or f16, fp32
+// accumulate).  Two LDS buffers alternate: while the matrix cores work on
+// span t, span t + 1 is written to the other buffer, and spans t + 2 and
+// t + 3 load into two register sets.  The loads are never guarded by a
+// branch, since a branch around loads makes the compiler wait for every load
+// in flight: rows past the data read the tile's first row, and steps past the
+// tile's end re-read its last span (from L2).
 #include "knnlm_device.h"
 #include "knnlm_internal.h"
 
@@ -38,13 +37,10 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
-constexpr int kMfmaWaves = 4;
-// Key rows per distance tile: a multiple of every variant's keys per pass
-// (kMfmaWaves * KB * 16 for KB = 2 or 4).
-constexpr int kMfmaTileRows = 256;
+constexpr int kPassKeys = 128;  // keys per pass: 8 blocks of 16, two per wave
 
 template <knn_dtype DT>
-__device__ __forceinline__ f32x4_t mfma16(const uint4 a, const uint4 b, f32x4_t c) {
+__device__ __forceinline__ f32x4_t mfma16(const u32x4_t a, const u32x4_t b, f32x4_t c) {
     if constexpr (DT == KNN_BF16) {
         return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b),
                                                        c, 0, 0, 0);
@@ -52,6 +48,15 @@ __device__ __forceinline__ f32x4_t mfma16(const uint4 a, const uint4 b, f32x4_t 
         return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, a), __builtin_bit_cast(f16x8_t, b),
                                                       c, 0, 0, 0);
     }
+}
+
+// Sum of squares of a 16-byte chunk added to acc, word by word (dot2).
+template <knn_dtype DT>
+__device__ __forceinline__ float dot_vec(const u32x4_t v, float acc) {
+    acc = dot_word<DT>(v.x, v.x, acc);
+    acc = dot_word<DT>(v.y, v.y, acc);
+    acc = dot_word<DT>(v.z, v.z, acc);
+    return dot_word<DT>(v.w, v.w, acc);
 }
 
 // min / max over the 16 lanes of a row (every lane of the row gets it).
@@ -76,22 +81,27 @@ __device__ __forceinline__ float group4_sum(float v) {
     return v;
 }
 
-constexpr int kSpan = kMfmaSpan;          // elements of d per pipeline step (256 bytes of a row)
-constexpr int kFragBytes = kWave * 16;    // one MFMA operand fragment: 64 lanes x 16 bytes
+constexpr int kSpan = kMfmaSpan;                 // elements of d per pipeline step (256 bytes of a row)
+constexpr int kChunks = kSpan * 2 / 16;          // 16-byte chunks per row and span
 
-// MQ: 16-query blocks per workgroup; KB: 16-key blocks per wave and pass;
-// NORMS: ||k||^2 comes precomputed; OCC: waves per SIMD the registers must
-// allow (measured best: 4 for one query block, 2 otherwise).
-template <knn_dtype DT, int MQ, int KB, bool NORMS, int OCC>
-__global__ __launch_bounds__(kMfmaWaves * kWave, OCC) void k_dist_mfma(DistArgs a, int64_t n_tiles, int64_t groups) {
+// Slot of chunk c of row n in a swizzled LDS span buffer.
+__device__ __forceinline__ int swz(int n, int c) { return n * kChunks + (c ^ (n & 15)); }
+
+// MQ: 16-query blocks per workgroup; QW: groups of waves that split the
+// query blocks (4 * QW waves: each wave takes MQ / QW query blocks and two of
+// the pass's eight key blocks); NORMS: ||k||^2 comes precomputed.
+template <knn_dtype DT, int MQ, int QW, bool NORMS>
+__global__ __launch_bounds__(4 * QW * kWave, 1) void k_dist_mfma(DistArgs a, int64_t n_tiles, int64_t groups) {
+    constexpr int kThreads = 4 * QW * kWave;
     constexpr int QB = MQ * 16;
-    constexpr int KEYS = kMfmaWaves * KB * 16;  // keys per pass
-    // Staged query span, double-buffered.  Fragment (j, c) -- rows j*16 .. +16,
-    // elements 32c .. +32 of the span -- sits lane-major at (j * 4 + c) * kFragBytes,
-    // exactly as the MFMA A operand wants it, so staging and reading are both
-    // contiguous 1 KB accesses.
-    __shared__ __align__(16) unsigned char qlds[2][MQ * 4 * kFragBytes];
-    __shared__ float sqq[kMfmaWaves][QB];
+    constexpr int MQW = MQ / QW;                         // query blocks per wave
+    constexpr int KCH = kPassKeys * kChunks / kThreads;  // key chunks per thread and step
+    constexpr int QCH = QB * kChunks / kThreads;         // query chunks per thread and step
+    static_assert(MQ % QW == 0 && KCH >= 1 && QCH >= 1, "whole blocks and chunks");
+    // native 4 x u32 vectors throughout, so that every 16-byte LDS access is
+    // one ds_read_b128 / ds_write_b128 (a struct is split by the compiler)
+    __shared__ __align__(16) u32x4_t klds[2][kPassKeys * kChunks];
+    __shared__ __align__(16) u32x4_t qlds[2][QB * kChunks];
     __shared__ uint32_t smin[QB], smax[QB];
 
     // Consecutive workgroups land on different XCDs (round robin over 8).  The
@@ -116,179 +126,200 @@ __global__ __launch_bounds__(kMfmaWaves * kWave, OCC) void k_dist_mfma(DistArgs 
 
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
-    const int wave = tid / kWave;
+    const int wave = (tid / kWave) / QW;  // this wave's pair of key blocks
+    const int jq = ((tid / kWave) % QW) * MQW;  // its first query block
     const int g = lane >> 4, lr = lane & 15;
     const int64_t row_bytes = a.d * 2;
     const int64_t nspan = a.d / kSpan;
+    const int64_t npass = (r1 - r0 + kPassKeys - 1) / kPassKeys;
+    const int64_t T = npass * nspan;  // pipeline steps of this tile
     const char *qbase = static_cast<const char *>(a.queries) + qb * row_bytes;
     const char *kset = static_cast<const char *>(a.keys) + k0 * row_bytes;
 
-    for (int q = tid; q < QB; q += kMfmaWaves * kWave) {
+    for (int q = tid; q < QB; q += kThreads) {
         smin[q] = 0xffffffffu;
         smax[q] = 0u;
     }
 
-    // Every load is unconditional (d is a multiple of kSpan; a query row or
-    // key row past the data reads row 0 of the block or tile instead, and the
-    // results of those lanes are never used), so that no branch makes the
-    // compiler wait for the loads already in flight.
-    //
-    // Query staging: wave `wave` stages fragments (m, wave) of a span -- query
-    // row m*16 + lr, elements 32*wave + 8g .. +8 -- and its lanes sum the
-    // squares of what they stage (||q||^2, completed over lanes and waves).
-    const char *qptr[MQ];
+    // Loads: chunk i of this thread is row i * 16 + tid / 16 of the pass (keys)
+    // or of the query block, 16-byte column tid % 16 of the span; its LDS slot
+    // swz(i * 16 + rsub, col) is i * 256 + slot0.
+    const int col = tid & (kChunks - 1);
+    const int rsub = tid / kChunks;
+    const int slot0 = swz(rsub, col);
+    constexpr int kRowsPerChunk = kThreads / kChunks;  // 16 rows per chunk index
+
+    // Two register sets (0, 1) take alternate steps, so that two steps are
+    // in flight while the matrix cores work on a third.
+    // Addresses: a uniform base per step plus a 32-bit offset per chunk (a
+    // tile is at most 4096 rows of at most 128 KiB).
+    u32x4_t kr[2][KCH], qr_[2][QCH];
+    const char *ktile = kset + r0 * row_bytes;
+    const uint32_t nrows = static_cast<uint32_t>(r1 - r0);
+    const uint32_t rb = static_cast<uint32_t>(row_bytes);
+    uint32_t qoff[QCH];
 #pragma unroll
-    for (int m = 0; m < MQ; ++m) {
-        const int qr = m * 16 + lr;
-        qptr[m] = qbase + (qr < nq ? qr : 0) * row_bytes + 64 * wave + 16 * g;
+    for (int i = 0; i < QCH; ++i) {
+        const int qrow = i * kRowsPerChunk + rsub;
+        qoff[i] = static_cast<uint32_t>(qrow < nq ? qrow : 0) * rb + static_cast<uint32_t>(col * 16);
     }
-
-    for (int64_t c0 = r0; c0 < r1; c0 += KEYS) {
-        float qqp[MQ];
+    const uint32_t ns = static_cast<uint32_t>(nspan);  // steps fit 32 bits: at most 32 passes of 512 spans
+    auto load = [&](int set, int64_t t) __attribute__((always_inline)) {
+        const uint32_t p = static_cast<uint32_t>(t) / ns, sp = static_cast<uint32_t>(t) - p * ns;
+        const char *kspan = ktile + static_cast<int64_t>(sp) * (2 * kSpan);
+        const char *qspan = qbase + static_cast<int64_t>(sp) * (2 * kSpan);
+        const uint32_t prow = p * kPassKeys + static_cast<uint32_t>(rsub);
 #pragma unroll
-        for (int m = 0; m < MQ; ++m) qqp[m] = 0.0f;
-        auto load_q = [&](int64_t sp, uint4 (&qn)[MQ]) {
-#pragma unroll
-            for (int m = 0; m < MQ; ++m) qn[m] = *reinterpret_cast<const uint4 *>(qptr[m] + sp * (2 * kSpan));
-        };
-        auto stage_q = [&](int buf, const uint4 (&qn)[MQ]) {
-#pragma unroll
-            for (int m = 0; m < MQ; ++m) {
-                *reinterpret_cast<uint4 *>(&qlds[buf][((m * 4 + wave) * kWave + lane) * 16]) = qn[m];
-                qqp[m] = dot_chunk<DT>(qn[m], qn[m], qqp[m]);
-            }
-        };
-        // Key chunk (kb, c) of span sp for this lane: row wrow + 16 kb, elements
-        // 32c + 8g .. +8, so one load instruction reads 64 contiguous bytes of
-        // each of 16 rows.
-        const int64_t wrow = c0 + wave * (KB * 16) + lr;
-        const char *kptr[KB];  // this lane's byte 16g of its row in each key block
-#pragma unroll
-        for (int kb = 0; kb < KB; ++kb) {
-            const int64_t row = wrow + kb * 16;
-            kptr[kb] = kset + (row < r1 ? row : r0) * row_bytes + 16 * g;
+        for (int i = 0; i < KCH; ++i) {
+            const uint32_t rr = prow + static_cast<uint32_t>(i * kRowsPerChunk);
+            const uint32_t off = (rr < nrows ? rr : 0u) * rb + static_cast<uint32_t>(col * 16);
+            kr[set][i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(kspan + off));
         }
-        auto load_k = [&](int64_t sp, int kb, int c) {
-            return load_stream(reinterpret_cast<const uint4 *>(kptr[kb] + sp * (2 * kSpan) + 64 * c));
-        };
+#pragma unroll
+        for (int i = 0; i < QCH; ++i) qr_[set][i] = *reinterpret_cast<const u32x4_t *>(qspan + qoff[i]);
+    };
+    auto write = [&](int set, int buf) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < KCH; ++i) klds[buf][i * kRowsPerChunk * kChunks + slot0] = kr[set][i];
+#pragma unroll
+        for (int i = 0; i < QCH; ++i) qlds[buf][i * kRowsPerChunk * kChunks + slot0] = qr_[set][i];
+    };
 
-        f32x4_t acc[MQ][KB];
+    f32x4_t acc[MQW][2];
+    float kkp[2], qqp[MQW];
+    // per lane: the smallest and largest distance of each of its queries over
+    // the tile (reduced across lanes once, at the end)
+    float tmn[MQW][4], tmx[MQW][4];
 #pragma unroll
-        for (int j = 0; j < MQ; ++j)
+    for (int j = 0; j < MQW; ++j) {
+        qqp[j] = 0.0f;  // ||q||^2 partials: the first pass adds them up, later passes reuse them
 #pragma unroll
-            for (int kb = 0; kb < KB; ++kb) acc[j][kb] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
-        float kkp[KB];
-#pragma unroll
-        for (int kb = 0; kb < KB; ++kb) kkp[kb] = 0.0f;
-
-        uint4 bk[KB][4];
-#pragma unroll
-        for (int kb = 0; kb < KB; ++kb)
-#pragma unroll
-            for (int c = 0; c < 4; ++c) bk[kb][c] = load_k(0, kb, c);
-        {
-            uint4 qn[MQ];
-            load_q(0, qn);
-            stage_q(0, qn);
+        for (int i = 0; i < 4; ++i) {
+            tmn[j][i] = __builtin_huge_valf();
+            tmx[j][i] = 0.0f;
         }
-        __syncthreads();
-
-        // One span; with MORE the next one's keys and queries load meanwhile.
-        // The last span is peeled off so that the loop body has no branch (a
-        // branch around loads makes the compiler wait for every load in flight).
-        auto span = [&](int64_t sp, auto more_tag) {
-            constexpr bool MORE = decltype(more_tag)::value;
-            const int cur = static_cast<int>(sp & 1);
-            uint4 qn[MQ];
-            if constexpr (MORE) load_q(sp + 1, qn);
+    }
+    auto clear = [&]() __attribute__((always_inline)) {
 #pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                uint4 af[MQ];
-#pragma unroll
-                for (int j = 0; j < MQ; ++j)
-                    af[j] = *reinterpret_cast<const uint4 *>(&qlds[cur][((j * 4 + c) * kWave + lane) * 16]);
-#pragma unroll
-                for (int j = 0; j < MQ; ++j)
-#pragma unroll
-                    for (int kb = 0; kb < KB; ++kb) acc[j][kb] = mfma16<DT>(af[j], bk[kb][c], acc[j][kb]);
-                if constexpr (!NORMS) {
-#pragma unroll
-                    for (int kb = 0; kb < KB; ++kb) kkp[kb] = dot_chunk<DT>(bk[kb][c], bk[kb][c], kkp[kb]);
-                }
-                // chunk c of this span is consumed: start loading it for the next
-                if constexpr (MORE) {
-#pragma unroll
-                    for (int kb = 0; kb < KB; ++kb) bk[kb][c] = load_k(sp + 1, kb, c);
-                }
-            }
-            if constexpr (MORE) stage_q(cur ^ 1, qn);
-            __syncthreads();
-        };
-        for (int64_t sp = 0; sp + 1 < nspan; ++sp) span(sp, std::true_type{});
-        span(nspan - 1, std::false_type{});
-
-        // ||q||^2 for the epilogue: lane (g, lr) needs query j*16 + 4g + i;
-        // lanes g share a row, waves share the rest.
-#pragma unroll
-        for (int m = 0; m < MQ; ++m) {
-            const float t = group4_sum(qqp[m]);
-            if (g == 0) sqq[wave][m * 16 + lr] = t;
+        for (int j = 0; j < MQW; ++j) {
+            acc[j][0] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+            acc[j][1] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
         }
-        __syncthreads();
-        float qsel[MQ][4];
-#pragma unroll
-        for (int j = 0; j < MQ; ++j)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int q = j * 16 + g * 4 + i;
-                float t = sqq[0][q];
-#pragma unroll
-                for (int w = 1; w < kMfmaWaves; ++w) t += sqq[w][q];
-                qsel[j][i] = t;
-            }
+        kkp[0] = kkp[1] = 0.0f;
+    };
+    clear();
 
-        // Epilogue: lane (g, lr) holds dot(query j*16 + 4g + i, key wrow + 16 kb)
-        // in acc[j][kb][i].
-        float kk[KB];
-        bool mk[KB];  // masked key rows (Section 3.4): distance +infinity, no part in the extrema
+    // The matrix cores over one span in LDS buffer buf (with QN, also the
+    // query norms).
+    auto compute = [&](int buf, bool qn_pass) __attribute__((always_inline)) {
+        // one MFMA step at a time for wide query batches, so that only one
+        // step's fragments are live
+#pragma unroll(MQW >= 4 ? 1 : 4)
+        for (int c = 0; c < 4; ++c) {
+            const int ch = (4 * c + g) ^ lr;
+            u32x4_t bk[2], af[MQW];
 #pragma unroll
-        for (int kb = 0; kb < KB; ++kb) {
-            const int64_t row = wrow + kb * 16;
+            for (int kb = 0; kb < 2; ++kb) bk[kb] = klds[buf][((wave * 2 + kb) * 16 + lr) * kChunks + ch];
+#pragma unroll
+            for (int j = 0; j < MQW; ++j) af[j] = qlds[buf][((jq + j) * 16 + lr) * kChunks + ch];
+#pragma unroll
+            for (int j = 0; j < MQW; ++j)
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb) acc[j][kb] = mfma16<DT>(af[j], bk[kb], acc[j][kb]);
+            if constexpr (!NORMS) {
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb) kkp[kb] = dot_vec<DT>(bk[kb], kkp[kb]);
+            }
+            if (qn_pass) {
+#pragma unroll
+                for (int j = 0; j < MQW; ++j) qqp[j] = dot_vec<DT>(af[j], qqp[j]);
+            }
+        }
+    };
+
+    // Distances of pass p: lane (g, lr) holds dot(query (jq + j)*16 + 4g + i,
+    // key c0 + (wave*2 + kb)*16 + lr) in acc[j][kb][i].
+    auto epilogue = [&](int64_t p) __attribute__((always_inline)) {
+        const int64_t c0 = r0 + p * kPassKeys;
+        float kk[2];
+        bool mk[2];  // masked key rows (Section 3.4): distance +infinity, no part in the extrema
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+            const int64_t row = c0 + (wave * 2 + kb) * 16 + lr;
             kk[kb] = NORMS ? (row < r1 ? a.key_sqnorms[k0 + row] : 0.0f) : group4_sum(kkp[kb]);
             mk[kb] = a.key_mask != nullptr && row < r1 && key_masked(a.key_mask, k0 + row);
         }
 #pragma unroll
-        for (int j = 0; j < MQ; ++j) {
+        for (int j = 0; j < MQW; ++j) {
+            const float qsum = group4_sum(qqp[j]);  // ||q||^2 of query (jq + j)*16 + lr
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const int q = j * 16 + g * 4 + i;
-                float mn = __builtin_huge_valf(), mx = 0.0f;
+                const int q = (jq + j) * 16 + g * 4 + i;
+                const float qn = __shfl(qsum, g * 4 + i);
 #pragma unroll
-                for (int kb = 0; kb < KB; ++kb) {
-                    const int64_t row = wrow + kb * 16;
+                for (int kb = 0; kb < 2; ++kb) {
+                    const int64_t row = c0 + (wave * 2 + kb) * 16 + lr;
                     const float dist = mk[kb] ? __uint_as_float(kMaskedBits)
-                                              : clamp_nonneg(fmaf(-2.0f, acc[j][kb][i], qsel[j][i] + kk[kb]));
+                                              : clamp_nonneg(fmaf(-2.0f, acc[j][kb][i], qn + kk[kb]));
                     const bool ok = q < nq && row < r1;
                     if (ok) a.dist[(qb + q) * a.ld + row] = dist;
                     if (ok && !mk[kb]) {
-                        mn = fminf(mn, dist);
-                        mx = fmaxf(mx, dist);
+                        tmn[j][i] = fminf(tmn[j][i], dist);
+                        tmx[j][i] = fmaxf(tmx[j][i], dist);
                     }
-                }
-                mn = row16_min(mn);
-                mx = row16_max(mx);
-                if (lr == 0 && q < nq) {
-                    atomicMin(&smin[q], __float_as_uint(mn));
-                    atomicMax(&smax[q], __float_as_uint(mx));
                 }
             }
         }
-        __syncthreads();  // sqq and the query buffers are reused by the next pass
+        clear();
+    };
+
+    // Step t: the matrix cores on span t (LDS buffer t % 2); span t + 1 goes
+    // from its register set (t + 1) % 2 to the other LDS buffer, and that set
+    // starts loading span t + 3; the barrier orders the LDS buffers between
+    // the waves.  Steps past the tile's last span load that span again (from
+    // L2) and write a buffer no one reads, and an odd step count gets one
+    // extra step whose products are never stored, so that no branch guards
+    // the loads.
+    auto step = [&](int64_t t, int set) __attribute__((always_inline)) {
+        compute(static_cast<int>(t & 1), t < nspan);
+        write(set, static_cast<int>((t + 1) & 1));
+        load(set, t + 3 < T ? t + 3 : T - 1);
+        __syncthreads();
+    };
+    // after step t: the epilogue of its pass when t is the pass's last span (a
+    // padding step is pass npass: rows past r1, nothing is stored)
+    auto pass_end = [&](int64_t t) __attribute__((always_inline)) {
+        const uint32_t p = static_cast<uint32_t>(t) / ns;
+        if (static_cast<uint32_t>(t) - p * ns == ns - 1) epilogue(p);
+    };
+    load(0, 0);
+    write(0, 0);
+    load(1, T > 1 ? 1 : 0);
+    load(0, T > 2 ? 2 : T - 1);
+    __syncthreads();
+    for (int64_t t = 0; t < T; t += 2) {
+        step(t, 1);
+        pass_end(t);
+        step(t + 1, 0);
+        pass_end(t + 1);
     }
 
+    // the tile's extrema of each query: over the 16 keys of a lane row, then
+    // over the lanes and waves with LDS atomics
+#pragma unroll
+    for (int j = 0; j < MQW; ++j)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int q = (jq + j) * 16 + g * 4 + i;
+            const float mn = row16_min(tmn[j][i]), mx = row16_max(tmx[j][i]);
+            if (lr == 0 && q < nq) {
+                atomicMin(&smin[q], __float_as_uint(mn));
+                atomicMax(&smax[q], __float_as_uint(mx));
+            }
+        }
     if (a.tile_min != nullptr) {
         __syncthreads();
-        for (int q = tid; q < nq; q += kMfmaWaves * kWave) {
+        for (int q = tid; q < nq; q += kThreads) {
             a.tile_min[(qb + q) * tiles + tile] = __uint_as_float(smin[q]);
             a.tile_max[(qb + q) * tiles + tile] = __uint_as_float(smax[q]);
         }
@@ -297,12 +328,12 @@ __global__ __launch_bounds__(kMfmaWaves * kWave, OCC) void k_dist_mfma(DistArgs 
 
 template <knn_dtype DT, bool NORMS>
 hipError_t launch_mq(int mq, const DistArgs &a, int64_t n_tiles, int64_t groups, dim3 grid, hipStream_t st) {
-    const dim3 block(kMfmaWaves * kWave);
+    const dim3 b4(4 * kWave), b8(8 * kWave);
     switch (mq) {
-    case 1: hipLaunchKernelGGL((k_dist_mfma<DT, 1, 2, NORMS, 4>), grid, block, 0, st, a, n_tiles, groups); break;
-    case 2: hipLaunchKernelGGL((k_dist_mfma<DT, 2, 4, NORMS, 2>), grid, block, 0, st, a, n_tiles, groups); break;
-    case 4: hipLaunchKernelGGL((k_dist_mfma<DT, 4, 2, NORMS, 2>), grid, block, 0, st, a, n_tiles, groups); break;
-    case 8: hipLaunchKernelGGL((k_dist_mfma<DT, 8, 2, NORMS, 2>), grid, block, 0, st, a, n_tiles, groups); break;
+    case 1: hipLaunchKernelGGL((k_dist_mfma<DT, 1, 1, NORMS>), grid, b4, 0, st, a, n_tiles, groups); break;
+    case 2: hipLaunchKernelGGL((k_dist_mfma<DT, 2, 1, NORMS>), grid, b4, 0, st, a, n_tiles, groups); break;
+    case 4: hipLaunchKernelGGL((k_dist_mfma<DT, 4, 1, NORMS>), grid, b4, 0, st, a, n_tiles, groups); break;
+    case 8: hipLaunchKernelGGL((k_dist_mfma<DT, 8, 2, NORMS>), grid, b8, 0, st, a, n_tiles, groups); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -316,12 +347,20 @@ hipError_t launch_dt(int mq, const DistArgs &a, int64_t n_tiles, int64_t groups,
 
 }  // namespace
 
-int mfma_keys_per_pass() { return kMfmaTileRows; }
+// Key rows per workgroup: at least two passes, and enough passes that a tile
+// runs at least 64 pipeline steps (spans), at most 32 passes.
+int mfma_tile_rows(int64_t d) {
+    const int64_t nspan = d / kSpan > 0 ? d / kSpan : 1;
+    int64_t passes = (64 + nspan - 1) / nspan;
+    if (passes < 2) passes = 2;
+    if (passes > 32) passes = 32;
+    return static_cast<int>(passes * kPassKeys);
+}
 
 hipError_t launch_distances_mfma(int mq, knn_dtype dtype, const DistArgs &args, int64_t S, int64_t groups,
                                  hipStream_t stream) {
     const int64_t n_tiles = S * args.tiles_per_set;
-    if (groups < 1 || args.rows_per_tile % kMfmaTileRows != 0) return hipErrorInvalidConfiguration;
+    if (groups < 1 || args.rows_per_tile % kPassKeys != 0 || args.d % kSpan != 0) return hipErrorInvalidConfiguration;
     const int64_t nblocks = (n_tiles + 7) / 8 * 8 * groups;
     if (nblocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
     const dim3 grid(static_cast<unsigned>(nblocks));
