@@ -89,8 +89,9 @@ __device__ __forceinline__ int swz(int n, int c) { return n * kChunks + (c ^ (n 
 
 // MQ: 16-query blocks per workgroup; QW: groups of waves that split the
 // query blocks (4 * QW waves: each wave takes MQ / QW query blocks and two of
-// the pass's eight key blocks); NORMS: ||k||^2 comes precomputed.
-template <knn_dtype DT, int MQ, int QW, bool NORMS>
+// the pass's eight key blocks); NS: register sets of prefetched spans (NS
+// spans in flight); NORMS: ||k||^2 comes precomputed.
+template <knn_dtype DT, int MQ, int QW, int NS, bool NORMS>
 __global__ __launch_bounds__(4 * QW * kWave, 1) void k_dist_mfma(DistArgs a, int64_t n_tiles, int64_t groups) {
     constexpr int kThreads = 4 * QW * kWave;
     constexpr int QB = MQ * 16;
@@ -149,11 +150,11 @@ __global__ __launch_bounds__(4 * QW * kWave, 1) void k_dist_mfma(DistArgs a, int
     const int slot0 = swz(rsub, col);
     constexpr int kRowsPerChunk = kThreads / kChunks;  // 16 rows per chunk index
 
-    // Two register sets (0, 1) take alternate steps, so that two steps are
-    // in flight while the matrix cores work on a third.
     // Addresses: a uniform base per step plus a 32-bit offset per chunk (a
     // tile is at most 4096 rows of at most 128 KiB).
-    u32x4_t kr[2][KCH], qr_[2][QCH];
+    // NS register sets take the steps in turn, so that NS steps are in flight
+    // while the matrix cores work on another.
+    u32x4_t kr[NS][KCH], qr_[NS][QCH];
     const char *ktile = kset + r0 * row_bytes;
     const uint32_t nrows = static_cast<uint32_t>(r1 - r0);
     const uint32_t rb = static_cast<uint32_t>(row_bytes);
@@ -274,16 +275,16 @@ __global__ __launch_bounds__(4 * QW * kWave, 1) void k_dist_mfma(DistArgs a, int
     };
 
     // Step t: the matrix cores on span t (LDS buffer t % 2); span t + 1 goes
-    // from its register set (t + 1) % 2 to the other LDS buffer, and that set
-    // starts loading span t + 3; the barrier orders the LDS buffers between
-    // the waves.  Steps past the tile's last span load that span again (from
-    // L2) and write a buffer no one reads, and an odd step count gets one
-    // extra step whose products are never stored, so that no branch guards
-    // the loads.
+    // from its register set (t + 1) % NS to the other LDS buffer, and that set
+    // starts loading span t + NS + 1; the barrier orders the LDS buffers
+    // between the waves.  Steps past the tile's last span load that span
+    // again (from L2) and write a buffer no one reads, and the step count is
+    // padded to a multiple of NS with steps whose products are never stored,
+    // so that no branch guards the loads.
     auto step = [&](int64_t t, int set) __attribute__((always_inline)) {
         compute(static_cast<int>(t & 1), t < nspan);
         write(set, static_cast<int>((t + 1) & 1));
-        load(set, t + 3 < T ? t + 3 : T - 1);
+        load(set, t + NS + 1 < T ? t + NS + 1 : T - 1);
         __syncthreads();
     };
     // after step t: the epilogue of its pass when t is the pass's last span (a
@@ -294,14 +295,15 @@ __global__ __launch_bounds__(4 * QW * kWave, 1) void k_dist_mfma(DistArgs a, int
     };
     load(0, 0);
     write(0, 0);
-    load(1, T > 1 ? 1 : 0);
-    load(0, T > 2 ? 2 : T - 1);
+#pragma unroll
+    for (int k = 1; k <= NS; ++k) load(k % NS, k < T ? k : T - 1);
     __syncthreads();
-    for (int64_t t = 0; t < T; t += 2) {
-        step(t, 1);
-        pass_end(t);
-        step(t + 1, 0);
-        pass_end(t + 1);
+    for (int64_t t = 0; t < T; t += NS) {
+#pragma unroll
+        for (int k = 0; k < NS; ++k) {
+            step(t + k, (k + 1) % NS);
+            pass_end(t + k);
+        }
     }
 
     // the tile's extrema of each query: over the 16 keys of a lane row, then
@@ -330,10 +332,10 @@ template <knn_dtype DT, bool NORMS>
 hipError_t launch_mq(int mq, const DistArgs &a, int64_t n_tiles, int64_t groups, dim3 grid, hipStream_t st) {
     const dim3 b4(4 * kWave), b8(8 * kWave);
     switch (mq) {
-    case 1: hipLaunchKernelGGL((k_dist_mfma<DT, 1, 1, NORMS>), grid, b4, 0, st, a, n_tiles, groups); break;
-    case 2: hipLaunchKernelGGL((k_dist_mfma<DT, 2, 1, NORMS>), grid, b4, 0, st, a, n_tiles, groups); break;
-    case 4: hipLaunchKernelGGL((k_dist_mfma<DT, 4, 1, NORMS>), grid, b4, 0, st, a, n_tiles, groups); break;
-    case 8: hipLaunchKernelGGL((k_dist_mfma<DT, 8, 2, NORMS>), grid, b8, 0, st, a, n_tiles, groups); break;
+    case 1: hipLaunchKernelGGL((k_dist_mfma<DT, 1, 1, 3, NORMS>), grid, b4, 0, st, a, n_tiles, groups); break;
+    case 2: hipLaunchKernelGGL((k_dist_mfma<DT, 2, 1, 3, NORMS>), grid, b4, 0, st, a, n_tiles, groups); break;
+    case 4: hipLaunchKernelGGL((k_dist_mfma<DT, 4, 1, 3, NORMS>), grid, b4, 0, st, a, n_tiles, groups); break;
+    case 8: hipLaunchKernelGGL((k_dist_mfma<DT, 8, 2, 2, NORMS>), grid, b8, 0, st, a, n_tiles, groups); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
