@@ -21,7 +21,7 @@ struct Layout {
     int rows_per_tile;
     int64_t tiles_per_set;
     int64_t ld;  // distance row stride = tiles_per_set * rows_per_tile
-    int split_parts;  // > 0: the select runs split over parts (candidate lists and counts below)
+    int split_parts;  // > 0: the select runs split over parts, short rows or long (candidate lists and counts below)
     size_t off_dist, off_tmin, off_tmax, off_cand, off_count, off_thr, total;
 };
 
@@ -36,7 +36,8 @@ Layout layout(int64_t B, int64_t d, int64_t S, int64_t max_keys, int64_t max_que
     L.off_tmax = align_up(L.off_tmin + sizeof(float) * static_cast<size_t>(B) * static_cast<size_t>(L.tiles_per_set));
     L.off_cand = align_up(L.off_tmax + sizeof(float) * static_cast<size_t>(B) * static_cast<size_t>(L.tiles_per_set));
     L.split_parts = select_split_parts(B, L.ld, r);
-    const size_t np = static_cast<size_t>(L.split_parts) * static_cast<size_t>(B);  // 0 unless split
+    if (L.split_parts == 0) L.split_parts = select_wide_parts(B, L.ld, r, L.tiles_per_set);
+    const size_t np = static_cast<size_t>(L.split_parts) * static_cast<size_t>(B);  // 0 unless split or wide
     L.off_count = align_up(L.off_cand + sizeof(uint64_t) * kSplitKeys * np);
     L.off_thr = align_up(L.off_count + 2 * sizeof(uint32_t) * np);  // counts, then minima
     L.total = align_up(L.off_thr + (L.split_parts > 0 ? sizeof(uint32_t) * static_cast<size_t>(B) : 0));

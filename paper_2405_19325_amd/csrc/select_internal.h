@@ -66,6 +66,12 @@ constexpr int64_t kSplitMaxN = 65536;
 constexpr int kSplitMaxR = 1024;
 constexpr int64_t kSplitMaxBlocks = 256;
 int select_split_parts(int64_t B, int64_t ld, int r);
+// Wide select: rows longer than kSplitMaxN keys are cut into parts (their
+// candidate lists use the split layout, [B, parts, kSplitKeys]) when r <= 2048
+// and the row has at least 2 r distance tiles; returns the parts per query
+// (at most 64), or 0.
+constexpr int64_t kWideBlocks = 2048;  // workgroups the wide select aims at
+int select_wide_parts(int64_t B, int64_t ld, int r, int64_t tiles_per_set);
 hipError_t launch_select(const SelectArgs &args, int64_t B, hipStream_t stream);
 hipError_t launch_select_mix(const SelectArgs &args, const MixArgs &mix, int64_t B, hipStream_t stream);
 hipError_t launch_mix(const MixArgs &args, int64_t B, hipStream_t stream);

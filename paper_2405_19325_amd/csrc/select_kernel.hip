@@ -1261,6 +1261,221 @@ __global__ __launch_bounds__(kT) void k_mix(MixArgs m) {
     mix_row<kPer, kVocabTile, MODE == kMixNest>(wj, tok, nkey, z, lam, m, b, acc);
 }
 
+// Wide path: rows longer than the split path's (ld > kSplitMaxN), r <= kWideMaxR,
+// when the distance stage's tiles are fine enough (at least 2 r tiles per row).
+// Query b's row is cut into `parts` slices, one workgroup each, so that few
+// queries with long rows still fill the chip; two kernels, no atomics or
+// fences between workgroups.
+//
+// Parts kernel (blockIdx.x = b * parts + part): the threshold is the end of
+// the histogram bin (2048 bins over their range) that holds the r-th smallest
+// of the row's tile minima: at least r tiles have their minimum below it, so
+// at least r keys do.  With at least 2 r tiles it keeps about r to 1.5 r keys
+// of random data.  Every part computes it (from tiles_per_set floats); each
+// streams its slice once, 16 keys per thread per step with the next step's
+// loads in flight, and appends the keys below the threshold (distance bits
+// << 32 | key index) to its list, each wave reserving its slots with one LDS
+// atomic; the list keeps its first kWideCap keys and the count is the true one.
+//
+// Finish kernel (one workgroup per query): if the lists hold between r and
+// kWideCap keys in all, it gathers them into LDS and bucket-sorts them (4096
+// buckets over [smallest, threshold)), else it selects over the streamed row
+// (the general path's select); then pi and the mixture as on the general path.
+constexpr int kWideMaxR = 2048;
+constexpr int kWideCap = kSplitKeys;       // candidates per list and in all (the lists share the split layout)
+constexpr int kWideU = 4;                  // 16-byte loads per thread per step
+constexpr int64_t kWideStep = static_cast<int64_t>(kT) * 4 * kWideU;  // keys per step (16384)
+
+__global__ __launch_bounds__(kT) void k_select_wide_parts(SelectArgs a, int parts) {
+    __shared__ __align__(16) uint32_t hist[kSelectBins];
+    __shared__ Shared sh;
+    const int tid = threadIdx.x;
+    const int lane = tid & (kWave - 1);
+    const int64_t b = blockIdx.x / parts;
+    const int part = static_cast<int>(blockIdx.x - b * parts);
+    const int64_t s = set_of_query(a.query_offsets, a.S, b);
+    const int64_t k0 = a.key_offsets[s];
+    int64_t N = a.key_offsets[s + 1] - k0;
+    if (N > a.ld) N = a.ld;
+    const uint32_t r_eff = static_cast<uint32_t>(N < a.r ? N : a.r);
+    const float *drow = a.dist + b * a.ld;
+    if (tid == 0) sh.ccount = 0u;
+
+    // The threshold from the tile minima (masked keys, at +infinity, stay out).
+    const int64_t ntiles = (N + a.rows_per_tile - 1) / a.rows_per_tile;
+    const float *tmin = a.tile_min + b * a.tiles_per_set;
+    uint32_t lo = ~0u, hi = 0u;
+    for (int64_t t = tid; t < ntiles; t += kT) {
+        const uint32_t v = __float_as_uint(tmin[t]);
+        lo = v < kMaskedBits ? min(lo, v) : lo;
+        hi = v < kMaskedBits ? max(hi, v) : hi;
+    }
+    block_minmax_u32(lo, hi, sh);
+    uint32_t thr = 0u;  // no unmasked key: nothing below
+    if (lo <= hi) {
+        for (int i = tid; i < kSelectBins; i += kT) hist[i] = 0u;
+        __syncthreads();
+        const uint32_t w = hi + 1u - lo;
+        const int shift = range_shift(w);
+        for (int64_t t = tid; t < ntiles; t += kT) {
+            const uint32_t v = __float_as_uint(tmin[t]);
+            if (v < kMaskedBits) atomicAdd(&hist[(v - lo) >> shift], 1u);
+        }
+        __syncthreads();
+        if (tid < kWave) {
+            // fewer than r tiles: every unmasked key (the finish then selects over the row)
+            const uint32_t j = wave_pick_bin(hist, r_eff > 0 ? r_eff : 1u, lane);
+            const uint64_t end = static_cast<uint64_t>(lo) + ((static_cast<uint64_t>(j) + 1u) << shift);
+            if (lane == 0) sh.hi = j == ~0u ? kMaskedBits : static_cast<uint32_t>(end < hi + 1ull ? end : hi + 1ull);
+        }
+        __syncthreads();
+        thr = sh.hi;
+    }
+
+    // This part's slice: a multiple of kWideStep keys.
+    const int64_t slice = ((N + parts - 1) / parts + kWideStep - 1) / kWideStep * kWideStep;
+    const int64_t kb = static_cast<int64_t>(part) * slice;
+    const int64_t ke = kb + slice < N ? kb + slice : N;
+    uint64_t *list = a.cand + (b * parts + part) * static_cast<int64_t>(kWideCap);
+    auto load = [&](int64_t base, uint4 (&v)[kWideU]) {
+#pragma unroll
+        for (int u = 0; u < kWideU; ++u) {
+            const int64_t i = base + (static_cast<int64_t>(u) * kT + tid) * 4;
+            v[u] = *reinterpret_cast<const uint4 *>(drow + (i < ke ? i : kb));  // past the slice: read its start, unused
+        }
+    };
+    if (kb < ke) {
+        uint4 v[kWideU], nx[kWideU];
+        load(kb, v);
+        for (int64_t base = kb; base < ke; base += kWideStep) {
+            load(base + kWideStep < ke ? base + kWideStep : kb, nx);
+            uint32_t c = 0;
+#pragma unroll
+            for (int u = 0; u < kWideU; ++u)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int64_t i = base + (static_cast<int64_t>(u) * kT + tid) * 4 + e;
+                    c += (i < ke && lane_word(v[u], e) < thr) ? 1u : 0u;
+                }
+            const uint32_t incl = wave_incl_scan_u32(c, lane);
+            const uint32_t wtot = readlane_u32(incl, kWave - 1);
+            uint32_t wbase = 0u;
+            if (lane == 0 && wtot > 0) wbase = atomicAdd(&sh.ccount, wtot);
+            uint32_t pos = readlane_u32(wbase, 0) + incl - c;
+#pragma unroll
+            for (int u = 0; u < kWideU; ++u)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int64_t i = base + (static_cast<int64_t>(u) * kT + tid) * 4 + e;
+                    const uint32_t bits = lane_word(v[u], e);
+                    if (i < ke && bits < thr) {
+                        if (pos < static_cast<uint32_t>(kWideCap)) list[pos] = sort_key(bits, static_cast<uint32_t>(i));
+                        ++pos;
+                    }
+                }
+#pragma unroll
+            for (int u = 0; u < kWideU; ++u) v[u] = nx[u];
+        }
+    }
+    __syncthreads();
+    if (tid == 0) {
+        a.part_count[b * parts + part] = sh.ccount;
+        if (part == 0) a.part_thr[b] = thr;
+    }
+}
+
+template <int MODE>
+__global__ __launch_bounds__(kT) void k_select_wide_finish(SelectArgs a, MixArgs m, int parts) {
+    constexpr bool MIX = MODE != kNoMix;
+    constexpr int kBinsLog2 = 12;
+    __shared__ __align__(16) uint64_t cand[kWideCap];
+    __shared__ __align__(16) uint64_t tmp[kWideCap];  // sort scratch, then the mixture's vocabulary tile
+    __shared__ __align__(16) uint32_t bins[2 << kBinsLog2];
+    __shared__ Shared sh;
+    __shared__ uint32_t part_off[kWave + 1];
+    static_assert(kVocabTile * 4 <= kWideCap * 8, "the vocabulary tile fits over the sort scratch");
+    float *acc = reinterpret_cast<float *>(tmp);
+
+    const int tid = threadIdx.x;
+    const int lane = tid & (kWave - 1);
+    const int64_t b = blockIdx.x;
+    const int64_t s = set_of_query(a.query_offsets, a.S, b);
+    const int64_t k0 = a.key_offsets[s];
+    int64_t N = a.key_offsets[s + 1] - k0;
+    if (N > a.ld) N = a.ld;
+    const uint32_t r_eff = static_cast<uint32_t>(N < a.r ? N : a.r);
+    const uint64_t *lists = a.cand + b * parts * static_cast<int64_t>(kWideCap);
+    if (tid < kWave) {
+        const uint32_t cnt = lane < parts ? a.part_count[b * parts + lane] : 0u;
+        const uint32_t incl = wave_incl_scan_u32(cnt, lane);
+        if (lane < parts) part_off[lane] = incl - cnt;
+        if (lane == parts - 1) part_off[parts] = incl;
+    }
+    __syncthreads();
+    const uint32_t total = part_off[parts];
+    uint32_t n;
+    if (total >= r_eff && total <= static_cast<uint32_t>(kWideCap)) {
+        uint32_t mn = ~0u;
+        for (uint32_t e = tid; e < total; e += kT) {
+            int p = 0;
+            while (p + 1 < parts && part_off[p + 1] <= e) ++p;
+            const uint64_t key = lists[p * static_cast<int64_t>(kWideCap) + (e - part_off[p])];
+            cand[e] = key;
+            mn = min(mn, static_cast<uint32_t>(key >> 32));
+        }
+        uint32_t mx = 0u;
+        block_minmax_u32(mn, mx, sh);  // also orders the gather before the sort
+        const uint32_t thr = a.part_thr[b];
+        bucket_sort<kWideCap / kT, kBinsLog2>(cand, total, mn, thr > mn ? thr - mn : 1u, bins, bins + (1 << kBinsLog2),
+                                             tmp, sh, NoHook(), r_eff);
+        n = total;
+    } else {
+        // The threshold kept too few or too many keys: select over the streamed row.
+        uint32_t bmin, bmax;
+        row_range(a, b, N, bmin, bmax, sh);
+        n = select_stream<kWideCap>(a.dist + b * a.ld, N, r_eff, bmin, bmax, cand, bins, sh);
+    }
+
+    int32_t *out_ids = a.ids + b * a.r;
+    float *out_d = a.dists + b * a.r;
+    const uint32_t rn = r_eff < n ? r_eff : n;
+    for (int j = tid; j < a.r; j += kT) {
+        if (static_cast<uint32_t>(j) < rn) {
+            const uint64_t key = cand[j];
+            out_ids[j] = static_cast<int32_t>(key & 0xffffffffu);
+            out_d[j] = __uint_as_float(static_cast<uint32_t>(key >> 32));
+        } else {  // fewer than r unmasked keys, or a key set smaller than r (a false hint)
+            out_ids[j] = -1;
+            out_d[j] = __builtin_huge_valf();
+        }
+    }
+    if constexpr (MIX) {
+        const float dmin = rn > 0 ? __uint_as_float(static_cast<uint32_t>(cand[0] >> 32)) : 0.0f;
+        const float dlast = rn > 0 ? __uint_as_float(static_cast<uint32_t>(cand[rn - 1] >> 32)) : 0.0f;
+        const float lam = query_lambda<MODE>(m, b, dmin, dlast);
+        float wj[kPer];
+        int32_t tok[kPer];
+        uint64_t nkey[kPer];
+        float zpart = 0.0f;
+#pragma unroll
+        for (int q = 0; q < kPer; ++q) {
+            const uint32_t j = static_cast<uint32_t>(q * kT + tid);
+            tok[q] = -1;
+            wj[q] = 0.0f;
+            nkey[q] = ~0ull;
+            if (j < rn) {
+                const uint64_t key = cand[j];
+                wj[q] = expf(-m.mu * (__uint_as_float(static_cast<uint32_t>(key >> 32)) - dmin));
+                zpart += wj[q];
+                tok[q] = m.values[k0 + static_cast<int32_t>(key & 0xffffffffu)];
+                nkey[q] = key;
+            }
+        }
+        const float z = block_sum(zpart, sh.red_f);  // its barrier also ends the sort scratch's use
+        mix_row<kPer, kVocabTile, MODE == kMixNest>(wj, tok, nkey, z, lam, m, b, acc);
+    }
+}
+
 template <int MODE>
 hipError_t launch_sel(const SelectArgs &a, const MixArgs &m, int64_t B, hipStream_t st) {
     if (B == 0) return hipSuccess;
@@ -1274,6 +1489,15 @@ hipError_t launch_sel(const SelectArgs &a, const MixArgs &m, int64_t B, hipStrea
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
         hipLaunchKernelGGL((k_select_finish<MODE>), grid, block, 0, st, a, m, parts);
+        return hipGetLastError();
+    }
+    const int wparts = select_wide_parts(B, a.ld, a.r, a.tiles_per_set);
+    if (wparts > 0) {
+        if (a.cand == nullptr || a.part_count == nullptr || a.part_thr == nullptr) return hipErrorInvalidValue;
+        hipLaunchKernelGGL(k_select_wide_parts, dim3(static_cast<unsigned>(B * wparts)), block, 0, st, a, wparts);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL((k_select_wide_finish<MODE>), grid, block, 0, st, a, m, wparts);
         return hipGetLastError();
     }
     if (a.ld <= kFastMaxN && a.r <= kT) {
@@ -1295,6 +1519,15 @@ int select_split_parts(int64_t B, int64_t ld, int r) {
     if (B < 1 || ld < 1 || ld > kSplitMaxN || r > kSplitMaxR) return 0;
     const int64_t parts = (ld + kSplitKeys - 1) / kSplitKeys;
     return B * parts <= kSplitMaxBlocks ? static_cast<int>(parts) : 0;
+}
+
+int select_wide_parts(int64_t B, int64_t ld, int r, int64_t tiles_per_set) {
+    if (B < 1 || ld <= kSplitMaxN || r > kWideMaxR || tiles_per_set < 2 * static_cast<int64_t>(r)) return 0;
+    int64_t parts = (kWideBlocks + B - 1) / B;  // about kWideBlocks workgroups
+    const int64_t by_len = ld / kWideStep;      // at least one step of keys per part
+    if (parts > by_len) parts = by_len;
+    if (parts > kWave) parts = kWave;           // the finish scans the counts with one wave
+    return parts < 1 ? 1 : static_cast<int>(parts);
 }
 
 int select_capacity(int r) {

@@ -409,3 +409,50 @@ def test_matrix_core_exact_integers(dtype):
     oids, odists = oracle.select(qh, kh, dt, np.array([0, n]), np.array([0, B]), r)
     np.testing.assert_array_equal(ids.cpu().numpy(), oids)
     np.testing.assert_array_equal(dists.cpu().numpy().astype(np.float64), odists)
+
+
+# ------------------------------------------------ wide select (long rows, fine tiles)
+
+@pytest.mark.parametrize("case", ["threshold", "all-equal-fallback", "masked-nest-step"])
+def test_wide_select_exact_integers(case):
+    """Rows of 600,000 fp32 keys of width 1024 (256-row distance tiles: 2,344
+    tiles, at least 2 r), two queries: the select is cut into parts with a
+    threshold from the tile minima.  Integer keys (a, b, c, 0, ...) give exact
+    distances, so ids and distances must equal the oracle's bit for bit.  With
+    every key equal the threshold keeps the whole row and the finish falls
+    back to the streamed select (ties by index); with a third of the keys
+    masked (a NEST step) the masked tiles' minima stay out of the threshold."""
+    _say(f"wide select: {case}")
+    n, d, B, r = 600000, 1024, 2, 1024
+    rng = np.random.default_rng(95)
+    k = np.zeros((n, d), np.float32)
+    if case != "all-equal-fallback":
+        k[:, :3] = rng.integers(-6, 7, (n, 3))
+    q = np.zeros((B, d), np.float32)
+    q[:, 3] = [1, 4]
+    vals = rng.integers(0, 300, n).astype(np.int32)
+    p_lm = rng.dirichlet(np.ones(300), B).astype(np.float32)
+    ko, qo = np.array([0, n]), np.array([0, B])
+    tq, tk, tv, tko, tqo, tp = _tensor_inputs(q, k, vals, p_lm, ko, qo, torch.float32)
+    if case == "masked-nest-step":
+        masked = rng.choice(n, n // 3, replace=False)
+        words = np.zeros((n + 31) // 32, np.uint32)
+        np.bitwise_or.at(words, masked >> 5, (np.uint32(1) << (masked & 31).astype(np.uint32)))
+        prob = knn.MixtureProblem(tq, tk, tv, tko, tqo, tp, r, 0.05, key_offsets_host=ko, query_offsets_host=qo)
+        out = prob.run_nest(0.3, 0.1, 0.5, key_mask=knn.mask_words(masked, n, "cuda"))
+        torch.cuda.synchronize()
+        p_m, ids, dists = out["p_m"], out["ids"], out["dists"]
+        o_ids, o_d = oracle.select(q, k, "f32", ko, qo, r, key_mask=words)
+        lam = oracle.rrc_lambda(o_d, 0.3, 0.1)
+        np.testing.assert_allclose(out["lambdas"].cpu().numpy().astype(np.float64), lam, rtol=0, atol=1e-6)
+    else:
+        p_m, ids, dists = knn.mixture(tq, tk, tv, tko, tqo, tp, r, 0.05, 0.5)
+        torch.cuda.synchronize()
+        o_ids, o_d = oracle.select(q, k, "f32", ko, qo, r)
+        lam = 0.5
+    np.testing.assert_array_equal(ids.cpu().numpy(), o_ids)
+    np.testing.assert_array_equal(dists.cpu().numpy().astype(np.float64), o_d)
+    ref = oracle.mix(o_ids, o_d, vals, ko, qo, p_lm, 0.05, lam)
+    np.testing.assert_allclose(p_m.cpu().numpy(), ref, rtol=0, atol=1e-5)
+    del tk
+    _free()
