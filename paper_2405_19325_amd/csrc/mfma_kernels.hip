@@ -87,18 +87,20 @@ constexpr int kChunks = kSpan * 2 / 16;          // 16-byte chunks per row and s
 // Slot of chunk c of row n in a swizzled LDS span buffer.
 __device__ __forceinline__ int swz(int n, int c) { return n * kChunks + (c ^ (n & 15)); }
 
-// MQ: 16-query blocks per workgroup; QW: groups of waves that split the
-// query blocks (4 * QW waves: each wave takes MQ / QW query blocks and two of
-// the pass's eight key blocks); NS: register sets of prefetched spans (NS
-// spans in flight); NORMS: ||k||^2 comes precomputed.
-template <knn_dtype DT, int MQ, int QW, int NS, bool NORMS>
-__global__ __launch_bounds__(4 * QW * kWave, 1) void k_dist_mfma(DistArgs a, int64_t n_tiles, int64_t groups) {
-    constexpr int kThreads = 4 * QW * kWave;
+// MQ: 16-query blocks per workgroup; WK x WQ waves: WK groups split the
+// pass's eight key blocks (8 / WK each), WQ groups split the query blocks
+// (MQ / WQ each); NS: register sets of prefetched spans (NS spans in
+// flight); NORMS: ||k||^2 comes precomputed.
+template <knn_dtype DT, int MQ, int WK, int WQ, int NS, bool NORMS>
+__global__ __launch_bounds__(WK * WQ * kWave, 1) void k_dist_mfma(DistArgs a, int64_t n_tiles, int64_t groups) {
+    constexpr int QW = WQ;
+    constexpr int KBW = 8 / WK;                          // key blocks per wave
+    constexpr int kThreads = WK * WQ * kWave;
     constexpr int QB = MQ * 16;
     constexpr int MQW = MQ / QW;                         // query blocks per wave
     constexpr int KCH = kPassKeys * kChunks / kThreads;  // key chunks per thread and step
     constexpr int QCH = QB * kChunks / kThreads;         // query chunks per thread and step
-    static_assert(MQ % QW == 0 && KCH >= 1 && QCH >= 1, "whole blocks and chunks");
+    static_assert(MQ % QW == 0 && 8 % WK == 0 && KCH >= 1 && QCH >= 1, "whole blocks and chunks");
     // native 4 x u32 vectors throughout, so that every 16-byte LDS access is
     // one ds_read_b128 / ds_write_b128 (a struct is split by the compiler)
     __shared__ __align__(16) u32x4_t klds[2][kPassKeys * kChunks];
@@ -127,7 +129,7 @@ __global__ __launch_bounds__(4 * QW * kWave, 1) void k_dist_mfma(DistArgs a, int
 
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
-    const int wave = (tid / kWave) / QW;  // this wave's pair of key blocks
+    const int wave = (tid / kWave) / QW;  // this wave's group of key blocks
     const int jq = ((tid / kWave) % QW) * MQW;  // its first query block
     const int g = lane >> 4, lr = lane & 15;
     const int64_t row_bytes = a.d * 2;
@@ -186,8 +188,8 @@ __global__ __launch_bounds__(4 * QW * kWave, 1) void k_dist_mfma(DistArgs a, int
         for (int i = 0; i < QCH; ++i) qlds[buf][i * kRowsPerChunk * kChunks + slot0] = qr_[set][i];
     };
 
-    f32x4_t acc[MQW][2];
-    float kkp[2], qqp[MQW];
+    f32x4_t acc[MQW][KBW];
+    float kkp[KBW], qqp[MQW];
     // per lane: the smallest and largest distance of each of its queries over
     // the tile (reduced across lanes once, at the end)
     float tmn[MQW][4], tmx[MQW][4];
@@ -202,34 +204,33 @@ __global__ __launch_bounds__(4 * QW * kWave, 1) void k_dist_mfma(DistArgs a, int
     }
     auto clear = [&]() __attribute__((always_inline)) {
 #pragma unroll
-        for (int j = 0; j < MQW; ++j) {
-            acc[j][0] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
-            acc[j][1] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
-        }
-        kkp[0] = kkp[1] = 0.0f;
+        for (int j = 0; j < MQW; ++j)
+#pragma unroll
+            for (int kb = 0; kb < KBW; ++kb) acc[j][kb] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int kb = 0; kb < KBW; ++kb) kkp[kb] = 0.0f;
     };
     clear();
 
-    // The matrix cores over one span in LDS buffer buf (with QN, also the
-    // query norms).
+    // The matrix cores over one span in LDS buffer buf (with qn_pass, also
+    // the query norms); the four MFMA steps unrolled, so that the next
+    // step's fragment reads overlap this step's MFMAs.
     auto compute = [&](int buf, bool qn_pass) __attribute__((always_inline)) {
-        // one MFMA step at a time for wide query batches, so that only one
-        // step's fragments are live
-#pragma unroll(MQW >= 4 ? 1 : 4)
+#pragma unroll
         for (int c = 0; c < 4; ++c) {
             const int ch = (4 * c + g) ^ lr;
-            u32x4_t bk[2], af[MQW];
+            u32x4_t bk[KBW], af[MQW];
 #pragma unroll
-            for (int kb = 0; kb < 2; ++kb) bk[kb] = klds[buf][((wave * 2 + kb) * 16 + lr) * kChunks + ch];
+            for (int kb = 0; kb < KBW; ++kb) bk[kb] = klds[buf][((wave * KBW + kb) * 16 + lr) * kChunks + ch];
 #pragma unroll
             for (int j = 0; j < MQW; ++j) af[j] = qlds[buf][((jq + j) * 16 + lr) * kChunks + ch];
 #pragma unroll
             for (int j = 0; j < MQW; ++j)
 #pragma unroll
-                for (int kb = 0; kb < 2; ++kb) acc[j][kb] = mfma16<DT>(af[j], bk[kb], acc[j][kb]);
+                for (int kb = 0; kb < KBW; ++kb) acc[j][kb] = mfma16<DT>(af[j], bk[kb], acc[j][kb]);
             if constexpr (!NORMS) {
 #pragma unroll
-                for (int kb = 0; kb < 2; ++kb) kkp[kb] = dot_vec<DT>(bk[kb], kkp[kb]);
+                for (int kb = 0; kb < KBW; ++kb) kkp[kb] = dot_vec<DT>(bk[kb], kkp[kb]);
             }
             if (qn_pass) {
 #pragma unroll
@@ -239,14 +240,14 @@ __global__ __launch_bounds__(4 * QW * kWave, 1) void k_dist_mfma(DistArgs a, int
     };
 
     // Distances of pass p: lane (g, lr) holds dot(query (jq + j)*16 + 4g + i,
-    // key c0 + (wave*2 + kb)*16 + lr) in acc[j][kb][i].
+    // key c0 + (wave*KBW + kb)*16 + lr) in acc[j][kb][i].
     auto epilogue = [&](int64_t p) __attribute__((always_inline)) {
         const int64_t c0 = r0 + p * kPassKeys;
-        float kk[2];
-        bool mk[2];  // masked key rows (Section 3.4): distance +infinity, no part in the extrema
+        float kk[KBW];
+        bool mk[KBW];  // masked key rows (Section 3.4): distance +infinity, no part in the extrema
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-            const int64_t row = c0 + (wave * 2 + kb) * 16 + lr;
+        for (int kb = 0; kb < KBW; ++kb) {
+            const int64_t row = c0 + (wave * KBW + kb) * 16 + lr;
             kk[kb] = NORMS ? (row < r1 ? a.key_sqnorms[k0 + row] : 0.0f) : group4_sum(kkp[kb]);
             mk[kb] = a.key_mask != nullptr && row < r1 && key_masked(a.key_mask, k0 + row);
         }
@@ -258,8 +259,8 @@ __global__ __launch_bounds__(4 * QW * kWave, 1) void k_dist_mfma(DistArgs a, int
                 const int q = (jq + j) * 16 + g * 4 + i;
                 const float qn = __shfl(qsum, g * 4 + i);
 #pragma unroll
-                for (int kb = 0; kb < 2; ++kb) {
-                    const int64_t row = c0 + (wave * 2 + kb) * 16 + lr;
+                for (int kb = 0; kb < KBW; ++kb) {
+                    const int64_t row = c0 + (wave * KBW + kb) * 16 + lr;
                     const float dist = mk[kb] ? __uint_as_float(kMaskedBits)
                                               : clamp_nonneg(fmaf(-2.0f, acc[j][kb][i], qn + kk[kb]));
                     const bool ok = q < nq && row < r1;
@@ -332,10 +333,10 @@ template <knn_dtype DT, bool NORMS>
 hipError_t launch_mq(int mq, const DistArgs &a, int64_t n_tiles, int64_t groups, dim3 grid, hipStream_t st) {
     const dim3 b4(4 * kWave), b8(8 * kWave);
     switch (mq) {
-    case 1: hipLaunchKernelGGL((k_dist_mfma<DT, 1, 1, 3, NORMS>), grid, b4, 0, st, a, n_tiles, groups); break;
-    case 2: hipLaunchKernelGGL((k_dist_mfma<DT, 2, 1, 3, NORMS>), grid, b4, 0, st, a, n_tiles, groups); break;
-    case 4: hipLaunchKernelGGL((k_dist_mfma<DT, 4, 1, 3, NORMS>), grid, b4, 0, st, a, n_tiles, groups); break;
-    case 8: hipLaunchKernelGGL((k_dist_mfma<DT, 8, 2, 2, NORMS>), grid, b8, 0, st, a, n_tiles, groups); break;
+    case 1: hipLaunchKernelGGL((k_dist_mfma<DT, 1, 4, 1, 3, NORMS>), grid, b4, 0, st, a, n_tiles, groups); break;
+    case 2: hipLaunchKernelGGL((k_dist_mfma<DT, 2, 4, 1, 3, NORMS>), grid, b4, 0, st, a, n_tiles, groups); break;
+    case 4: hipLaunchKernelGGL((k_dist_mfma<DT, 4, 4, 1, 3, NORMS>), grid, b4, 0, st, a, n_tiles, groups); break;
+    case 8: hipLaunchKernelGGL((k_dist_mfma<DT, 8, 4, 2, 2, NORMS>), grid, b8, 0, st, a, n_tiles, groups); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
