@@ -1288,6 +1288,7 @@ constexpr int64_t kWideStep = static_cast<int64_t>(kT) * 4 * kWideU;  // keys pe
 
 __global__ __launch_bounds__(kT) void k_select_wide_parts(SelectArgs a, int parts) {
     __shared__ __align__(16) uint32_t hist[kSelectBins];
+    __shared__ uint32_t qtile[kT];  // tiles of the current chunk with keys below the threshold
     __shared__ Shared sh;
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
@@ -1332,31 +1333,55 @@ __global__ __launch_bounds__(kT) void k_select_wide_parts(SelectArgs a, int part
         thr = sh.hi;
     }
 
-    // This part's slice: a multiple of kWideStep keys.
-    const int64_t slice = ((N + parts - 1) / parts + kWideStep - 1) / kWideStep * kWideStep;
-    const int64_t kb = static_cast<int64_t>(part) * slice;
-    const int64_t ke = kb + slice < N ? kb + slice : N;
+    // This part's tiles, kT at a time: those whose minimum is below the
+    // threshold are listed in LDS (a tile whose minimum is not below it holds
+    // no key below it), and only their rows are streamed, as one run of
+    // nq * R rows, 16 keys per thread per step with the next step's loads in
+    // flight.  R is a multiple of 8, so a 16-byte load stays in one tile.
+    const int64_t R = a.rows_per_tile;
+    const int64_t tpp = (ntiles + parts - 1) / parts;
+    const int64_t tb = static_cast<int64_t>(part) * tpp;
+    const int64_t te = tb + tpp < ntiles ? tb + tpp : ntiles;
+    const uint32_t R32 = static_cast<uint32_t>(R);
     uint64_t *list = a.cand + (b * parts + part) * static_cast<int64_t>(kWideCap);
-    auto load = [&](int64_t base, uint4 (&v)[kWideU]) {
+    for (int64_t c0 = tb; c0 < te; c0 += kT) {
+        __syncthreads();  // the previous chunk's reads of sh.total and qtile are done
+        if (tid == 0) sh.total = 0u;
+        __syncthreads();
+        const int64_t tt = c0 + tid;
+        const uint32_t qual = (tt < te && __float_as_uint(tmin[tt]) < thr) ? 1u : 0u;
+        const uint32_t qincl = wave_incl_scan_u32(qual, lane);
+        const uint32_t qtot = readlane_u32(qincl, kWave - 1);
+        uint32_t qbase = 0u;
+        if (lane == 0 && qtot > 0) qbase = atomicAdd(&sh.total, qtot);
+        if (qual) qtile[readlane_u32(qbase, 0) + qincl - 1u] = static_cast<uint32_t>(tt);
+        __syncthreads();
+        const uint32_t nrows = sh.total * R32;  // <= kT * 4096
+        // virtual row v of the run: row (v % R) of listed tile v / R; past the run, or past the row's
+        // end in its last tile, a lane reads the row's first keys and counts nothing
+        auto row_of = [&](uint32_t v) __attribute__((always_inline)) -> int64_t {
+            const uint32_t slot = v / R32;
+            return v < nrows ? static_cast<int64_t>(qtile[slot < static_cast<uint32_t>(kT) ? slot : 0u]) * R + (v - slot * R32)
+                             : N;
+        };
+        auto load = [&](uint32_t base, int64_t (&ri)[kWideU], uint4 (&v)[kWideU]) __attribute__((always_inline)) {
 #pragma unroll
-        for (int u = 0; u < kWideU; ++u) {
-            const int64_t i = base + (static_cast<int64_t>(u) * kT + tid) * 4;
-            v[u] = *reinterpret_cast<const uint4 *>(drow + (i < ke ? i : kb));  // past the slice: read its start, unused
-        }
-    };
-    if (kb < ke) {
+            for (int u = 0; u < kWideU; ++u) {
+                ri[u] = row_of(base + (static_cast<uint32_t>(u) * kT + tid) * 4u);
+                v[u] = *reinterpret_cast<const uint4 *>(drow + (ri[u] < N ? ri[u] : 0));
+            }
+        };
+        if (nrows == 0u) continue;
+        int64_t ri[kWideU], rn[kWideU];
         uint4 v[kWideU], nx[kWideU];
-        load(kb, v);
-        for (int64_t base = kb; base < ke; base += kWideStep) {
-            load(base + kWideStep < ke ? base + kWideStep : kb, nx);
+        load(0u, ri, v);
+        for (uint32_t base = 0u; base < nrows; base += static_cast<uint32_t>(kWideStep)) {
+            load(base + static_cast<uint32_t>(kWideStep), rn, nx);
             uint32_t c = 0;
 #pragma unroll
             for (int u = 0; u < kWideU; ++u)
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int64_t i = base + (static_cast<int64_t>(u) * kT + tid) * 4 + e;
-                    c += (i < ke && lane_word(v[u], e) < thr) ? 1u : 0u;
-                }
+                for (int e = 0; e < 4; ++e) c += (ri[u] + e < N && lane_word(v[u], e) < thr) ? 1u : 0u;
             const uint32_t incl = wave_incl_scan_u32(c, lane);
             const uint32_t wtot = readlane_u32(incl, kWave - 1);
             uint32_t wbase = 0u;
@@ -1366,15 +1391,18 @@ __global__ __launch_bounds__(kT) void k_select_wide_parts(SelectArgs a, int part
             for (int u = 0; u < kWideU; ++u)
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    const int64_t i = base + (static_cast<int64_t>(u) * kT + tid) * 4 + e;
                     const uint32_t bits = lane_word(v[u], e);
-                    if (i < ke && bits < thr) {
-                        if (pos < static_cast<uint32_t>(kWideCap)) list[pos] = sort_key(bits, static_cast<uint32_t>(i));
+                    if (ri[u] + e < N && bits < thr) {
+                        if (pos < static_cast<uint32_t>(kWideCap))
+                            list[pos] = sort_key(bits, static_cast<uint32_t>(ri[u] + e));
                         ++pos;
                     }
                 }
 #pragma unroll
-            for (int u = 0; u < kWideU; ++u) v[u] = nx[u];
+            for (int u = 0; u < kWideU; ++u) {
+                v[u] = nx[u];
+                ri[u] = rn[u];
+            }
         }
     }
     __syncthreads();

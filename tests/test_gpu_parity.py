@@ -456,3 +456,36 @@ def test_wide_select_exact_integers(case):
     np.testing.assert_allclose(p_m.cpu().numpy(), ref, rtol=0, atol=1e-5)
     del tk
     _free()
+
+
+def test_wide_select_many_queries_chunked_tile_scan():
+    """1,024 queries over one set of 600,000 fp32 keys of width 1024: 2,344
+    distance tiles of 256 rows and two select parts per query, so a part lists
+    its tiles with keys below the threshold in two chunks of at most 1,024
+    tiles and streams only those.  Keys (a, b, c, 0, ...) with a, b, c in
+    [-6, 6] and queries (0, 0, 0, c, 0, ...) give exact integer distances;
+    the oracle runs on the four leading columns, which give the same values."""
+    _say("wide select: 1024 queries, chunked tile scan")
+    n, d, B, r = 600000, 1024, 1024, 1024
+    rng = np.random.default_rng(96)
+    k4 = np.zeros((n, 4), np.float32)
+    k4[:, :3] = rng.integers(-6, 7, (n, 3))
+    q4 = np.zeros((B, 4), np.float32)
+    q4[:, 3] = np.arange(B) % 5
+    vals = rng.integers(0, 300, n).astype(np.int32)
+    p_lm = rng.dirichlet(np.ones(300), B).astype(np.float32)
+    ko, qo = np.array([0, n]), np.array([0, B])
+    tk = torch.zeros((n, d), dtype=torch.float32, device="cuda")
+    tk[:, :4] = torch.as_tensor(k4, device="cuda")
+    tq = torch.zeros((B, d), dtype=torch.float32, device="cuda")
+    tq[:, :4] = torch.as_tensor(q4, device="cuda")
+    _, _, tv, tko, tqo, tp = _tensor_inputs(q4, k4[:1], vals, p_lm, ko, qo, torch.float32)
+    p_m, ids, dists = knn.mixture(tq, tk, tv, tko, tqo, tp, r, 0.05, 0.5)
+    torch.cuda.synchronize()
+    o_ids, o_d = oracle.select(q4, k4, "f32", ko, qo, r)
+    np.testing.assert_array_equal(ids.cpu().numpy(), o_ids)
+    np.testing.assert_array_equal(dists.cpu().numpy().astype(np.float64), o_d)
+    ref = oracle.mix(o_ids, o_d, vals, ko, qo, p_lm, 0.05, 0.5)
+    np.testing.assert_allclose(p_m.cpu().numpy(), ref, rtol=0, atol=1e-5)
+    del tk, tq, p_m
+    _free()
