@@ -27,6 +27,10 @@ namespace knnlm {
 namespace {
 
 constexpr int kWavesPerDistBlock = kDistThreads / kWave;
+
+// Where the streaming kernel stores the (discarded) distances of the sets it
+// loads past its tile's end: one word per device, written, never read.
+__device__ float g_dist_sink;
 constexpr int kQueryRegChunks = 16;  // 16-byte query chunks a lane may hold in registers
 
 // ---------------------------------------------------------------- vector path
@@ -86,12 +90,36 @@ __device__ __forceinline__ void write_tile_extrema(const DistArgs &a, const Tile
 }
 
 // 16-byte loads: d % VEC == 0, 16-byte aligned rows, at most CPL chunks per lane.
-// Queries stay packed in registers (NQ x CPL chunks per lane); ROWS key rows per
-// wave are loaded before any of them is used.  MASK: a.key_mask is given.
-template <knn_dtype DT, int CPL, int NQ, int ROWS, bool MASK>
+// Queries stay packed in registers (NQ x CPL chunks per lane).  A wave takes
+// the tile's rows wave, wave + 4, ... in sets of at most 8 chunks per lane
+// (8 KiB per wave: a whole row, or half of a 16-chunk row) and keeps two rows
+// in flight in register sets used in turn (the loop is unrolled over the sets,
+// so no set is ever copied); a set is reloaded as soon as it is consumed.  A
+// row's halves add into the same partial sums in chunk order, so the sums are
+// those of a whole-row pass.  (Measured against deeper pipelines and
+// whole-row sets: this keeps HBM busiest at 8 and 16 KiB rows.)
+//
+// The loop body has no branch: a branch around a load makes the compiler wait
+// for every load in flight at the join, which would drain the pipeline once
+// per set.  So every load is issued unconditionally --
+//   * a set past the tile's end reads the group's first query row (in cache,
+//     so the pipeline's tail costs no HBM traffic) and its distance goes to a
+//     sink word, outside the tile's extrema;
+//   * query slots past the group's last query repeat that query, so their
+//     distances and stores repeat its own;
+//   * ||k||^2 reads the given norms, or a valid dummy word that is ignored;
+//   * every lane stores the (wave-uniform) distance to the same address.
+// MASK: a.key_mask is given.
+template <knn_dtype DT, int CPL, int NQ, bool MASK>
 __global__ __launch_bounds__(kDistThreads) void k_dist_vec(DistArgs a) {
-    constexpr int EB = Elem<DT>::BYTES;
     constexpr int NW = kWavesPerDistBlock;
+    constexpr int CPS = CPL > 8 ? 8 : CPL;  // chunks per set
+    constexpr int SPR = CPL / CPS;          // sets per row
+    constexpr int D = 2 * SPR;              // sets in flight: two rows
+    constexpr int RPI = D / SPR;            // rows per loop iteration
+    static_assert(CPL % CPS == 0 && D % SPR == 0, "whole sets per row, whole rows per iteration");
+    constexpr int EB = Elem<DT>::BYTES;
+    clear_arrivals(a, kDistThreads);
     TileWork t;
     if (!tile_work<NQ>(a, t)) return;
 
@@ -99,16 +127,18 @@ __global__ __launch_bounds__(kDistThreads) void k_dist_vec(DistArgs a) {
     const int wave = threadIdx.x / kWave;
     const int nchunks = static_cast<int>(a.d * EB / 16);
     const int64_t row_bytes = a.d * EB;
-    const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
+    const u32x4_t zero = {0u, 0u, 0u, 0u};
 
-    uint4 qv[NQ][CPL];
+    u32x4_t qv[NQ][CPL];
 #pragma unroll
     for (int j = 0; j < NQ; ++j) {
-        const uint4 *qrow = reinterpret_cast<const uint4 *>(static_cast<const char *>(a.queries) + (t.qb + j) * row_bytes);
+        const int jj = j < t.nq ? j : t.nq - 1;
+        const char *qrow = static_cast<const char *>(a.queries) + (t.qb + jj) * row_bytes;
 #pragma unroll
         for (int c = 0; c < CPL; ++c) {
             const int ch = lane + kWave * c;
-            qv[j][c] = (j < t.nq && ch < nchunks) ? qrow[ch] : zero;
+            const u32x4_t v = *reinterpret_cast<const u32x4_t *>(qrow + 16 * (ch < nchunks ? ch : 0));
+            qv[j][c] = ch < nchunks ? v : zero;
         }
     }
     float mn[NQ], mx[NQ];
@@ -118,84 +148,105 @@ __global__ __launch_bounds__(kDistThreads) void k_dist_vec(DistArgs a) {
         mx[j] = 0.0f;
     }
     const bool have_norms = a.key_sqnorms != nullptr;
+    const float *knorm = have_norms ? a.key_sqnorms + t.k0 : a.dist;  // a.dist: a valid word, never used
     const char *kset = static_cast<const char *>(a.keys) + t.k0 * row_bytes;
+    // the group's first query row: what the sets past the tile's end read (it is in cache)
+    const char *qrow0 = static_cast<const char *>(a.queries) + t.qb * row_bytes;
+    float *dq[NQ];  // this group's distance rows (repeated past the last query)
+#pragma unroll
+    for (int j = 0; j < NQ; ++j) dq[j] = a.dist + (t.qb + (j < t.nq ? j : t.nq - 1)) * a.ld;
 
-    // Software pipeline: the loads of a wave's next ROWS rows are in flight
-    // while the current rows are reduced.
-    constexpr int64_t kStep = static_cast<int64_t>(NW) * ROWS;
-    uint4 kv[ROWS][CPL];
-    bool mk[ROWS];  // the rows' mask bits (MASK)
-    int64_t row = t.r0 + wave * ROWS;
+    float qq[NQ];  // ||q||^2, computed once the first key loads are in flight
+    u32x4_t kv[D][CPS];
+    float kn[D];    // ||k||^2 of the set's row (sets that end a row)
+    uint32_t mw[D], mb[D];  // its mask word and bit (MASK; sets that end a row)
+    int64_t rc[D];  // the row each set holds (clamped into the tile)
+    bool in[D];     // the set's row is in the tile
+    float acc_k, acc_q[NQ];  // the current row's partial sums
+    // set s holds part s % SPR of row rw
+    auto load = [&](int s, int64_t rw) __attribute__((always_inline)) {
+        const int part = s % SPR;
+        const bool inside = rw < t.r1;
+        const int64_t r = inside ? rw : t.r0;
+        rc[s] = r;
+        in[s] = inside;
+        const char *krow = inside ? kset + r * row_bytes : qrow0;
 #pragma unroll
-    for (int rr = 0; rr < ROWS; ++rr) {
-        const int64_t rw = row + rr;
-        const uint4 *krow = reinterpret_cast<const uint4 *>(kset + rw * row_bytes);
-#pragma unroll
-        for (int c = 0; c < CPL; ++c) {
-            const int ch = lane + kWave * c;
-            kv[rr][c] = (rw < t.r1 && ch < nchunks) ? load_stream(krow + ch) : zero;
+        for (int c = 0; c < CPS; ++c) {
+            const int ch = lane + kWave * (part * CPS + c);
+            kv[s][c] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(krow + 16 * (ch < nchunks ? ch : 0)));
         }
-        if constexpr (MASK) mk[rr] = key_masked(a.key_mask, t.k0 + (rw < t.r1 ? rw : t.r0)) & (rw < t.r1);
-    }
+        if (part == SPR - 1) {  // with the row's last set: it is reloaded only after the row is done
+            kn[s] = knorm[have_norms ? r : 0];
+            if constexpr (MASK) {  // the word now, its bit where it is used (a test here would wait for the load)
+                mw[s] = a.key_mask[(t.k0 + r) >> 5];
+                mb[s] = static_cast<uint32_t>((t.k0 + r) & 31);
+            }
+        }
+    };
+    auto consume = [&](int s) __attribute__((always_inline)) {
+        const int part = s % SPR;
+        if (part == 0) {
+            acc_k = 0.0f;
+#pragma unroll
+            for (int j = 0; j < NQ; ++j) acc_q[j] = 0.0f;
+        }
+#pragma unroll
+        for (int c = 0; c < CPS; ++c) {
+            const int cc = part * CPS + c;
+            // chunks past the row read its first chunk: zeroed here, where the data is used
+            // (a select at the load would wait for the load)
+            const u32x4_t kc = lane + kWave * cc < nchunks ? kv[s][c] : zero;
+            const uint4 k4 = make_uint4(kc.x, kc.y, kc.z, kc.w);
+            acc_k = dot_chunk<DT>(k4, k4, acc_k);
+#pragma unroll
+            for (int j = 0; j < NQ; ++j)
+                acc_q[j] = dot_chunk<DT>(make_uint4(qv[j][cc].x, qv[j][cc].y, qv[j][cc].z, qv[j][cc].w), k4, acc_q[j]);
+        }
+        if (part != SPR - 1) return;
+        const float kk_sum = wave_allsum(acc_k);
+        const float kk = have_norms ? kn[s] : kk_sum;
+#pragma unroll
+        for (int j = 0; j < NQ; ++j) {
+            const float dot = wave_allsum(acc_q[j]);
+            float dist = clamp_nonneg(fmaf(-2.0f, dot, qq[j] + kk));
+            bool counted = in[s];
+            if constexpr (MASK) {
+                const bool masked = ((mw[s] >> mb[s]) & 1u) != 0u;
+                dist = masked ? __uint_as_float(kMaskedBits) : dist;
+                counted = counted && !masked;
+            }
+            *(in[s] ? dq[j] + rc[s] : &g_dist_sink) = dist;
+            mn[j] = counted ? fminf(mn[j], dist) : mn[j];
+            mx[j] = counted ? fmaxf(mx[j], dist) : mx[j];
+        }
+    };
+
+    int64_t row = t.r0 + wave;
+#pragma unroll
+    for (int s = 0; s < D; ++s) load(s, row + static_cast<int64_t>(s / SPR) * NW);
     // ||q||^2 after the first key loads are issued, so they overlap the query's latency.
-    float qq[NQ];
 #pragma unroll
     for (int j = 0; j < NQ; ++j) {
         float acc = 0.0f;
 #pragma unroll
-        for (int c = 0; c < CPL; ++c) acc = dot_chunk<DT>(qv[j][c], qv[j][c], acc);
+        for (int c = 0; c < CPL; ++c) {
+            const uint4 q4 = make_uint4(qv[j][c].x, qv[j][c].y, qv[j][c].z, qv[j][c].w);
+            acc = dot_chunk<DT>(q4, q4, acc);
+        }
         qq[j] = wave_allsum(acc);
     }
-    for (; row < t.r1; row += kStep) {
-        uint4 kn[ROWS][CPL];
-        bool mkn[ROWS];
+    for (; row < t.r1; row += static_cast<int64_t>(RPI) * NW) {
 #pragma unroll
-        for (int rr = 0; rr < ROWS; ++rr) {
-            const int64_t rw = row + kStep + rr;
-            const uint4 *krow = reinterpret_cast<const uint4 *>(kset + rw * row_bytes);
-#pragma unroll
-            for (int c = 0; c < CPL; ++c) {
-                const int ch = lane + kWave * c;
-                kn[rr][c] = (rw < t.r1 && ch < nchunks) ? load_stream(krow + ch) : zero;
-            }
-            // the word of a row past the tile is read from the tile's first row: no branch around the load
-            if constexpr (MASK) mkn[rr] = key_masked(a.key_mask, t.k0 + (rw < t.r1 ? rw : t.r0)) & (rw < t.r1);
-        }
-#pragma unroll
-        for (int rr = 0; rr < ROWS; ++rr) {
-            const int64_t rw = row + rr;
-            float acc_k = 0.0f;
-            float acc_q[NQ];
-#pragma unroll
-            for (int j = 0; j < NQ; ++j) acc_q[j] = 0.0f;
-#pragma unroll
-            for (int c = 0; c < CPL; ++c) {
-                if (!have_norms) acc_k = dot_chunk<DT>(kv[rr][c], kv[rr][c], acc_k);
-#pragma unroll
-                for (int j = 0; j < NQ; ++j) acc_q[j] = dot_chunk<DT>(qv[j][c], kv[rr][c], acc_q[j]);
-            }
-            const float kk = have_norms ? ((rw < t.r1) ? a.key_sqnorms[t.k0 + rw] : 0.0f) : wave_allsum(acc_k);
-#pragma unroll
-            for (int j = 0; j < NQ; ++j) {
-                const float dot = wave_allsum(acc_q[j]);
-                float dist = clamp_nonneg(fmaf(-2.0f, dot, qq[j] + kk));
-                if constexpr (MASK) dist = mk[rr] ? __uint_as_float(kMaskedBits) : dist;
-                if (rw < t.r1) {
-                    if (lane == j && j < t.nq) a.dist[(t.qb + j) * a.ld + rw] = dist;
-                    if (!MASK || !mk[rr]) {
-                        mn[j] = fminf(mn[j], dist);
-                        mx[j] = fmaxf(mx[j], dist);
-                    }
-                }
-            }
-        }
-#pragma unroll
-        for (int rr = 0; rr < ROWS; ++rr) {
-#pragma unroll
-            for (int c = 0; c < CPL; ++c) kv[rr][c] = kn[rr][c];
-            if constexpr (MASK) mk[rr] = mkn[rr];
+        for (int s = 0; s < D; ++s) {
+            // the scheduler may not mix the sets' work: mixing them needs every set's
+            // data at once, that is a wait for every load in flight
+            __builtin_amdgcn_sched_barrier(0);
+            consume(s);
+            load(s, row + static_cast<int64_t>(s / SPR + RPI) * NW);
         }
     }
+    __builtin_amdgcn_sched_barrier(0);
     if (a.tile_min != nullptr) write_tile_extrema<NQ>(a, t, mn, mx);
 }
 
@@ -210,6 +261,7 @@ __global__ __launch_bounds__(kDistThreads) void k_dist_elem(DistArgs a) {
     constexpr int EB = Elem<DT>::BYTES;
     constexpr int PW = Elem<DT>::PER_WORD;
     constexpr int NW = kWavesPerDistBlock;
+    clear_arrivals(a, kDistThreads);
     TileWork t;
     if (!tile_work<NQ>(a, t)) return;
 
@@ -331,31 +383,26 @@ __global__ __launch_bounds__(kDistThreads) void k_sqnorm_elem(const void *keys, 
 
 // ------------------------------------------------------------ dispatch
 
-template <knn_dtype DT, int CPL, int NQ, int ROWS>
+template <knn_dtype DT, int CPL, int NQ>
 hipError_t launch_vec(const DistArgs &a, dim3 grid, hipStream_t st) {
-    if constexpr (NQ * CPL <= kQueryRegChunks && ROWS * CPL <= kMaxCplVec) {
+    if constexpr (NQ * CPL <= kQueryRegChunks && CPL <= kMaxCplVec) {
         if (a.key_mask != nullptr)
-            hipLaunchKernelGGL((k_dist_vec<DT, CPL, NQ, ROWS, true>), grid, dim3(kDistThreads), 0, st, a);
+            hipLaunchKernelGGL((k_dist_vec<DT, CPL, NQ, true>), grid, dim3(kDistThreads), 0, st, a);
         else
-            hipLaunchKernelGGL((k_dist_vec<DT, CPL, NQ, ROWS, false>), grid, dim3(kDistThreads), 0, st, a);
+            hipLaunchKernelGGL((k_dist_vec<DT, CPL, NQ, false>), grid, dim3(kDistThreads), 0, st, a);
         return hipGetLastError();
     } else {
         return hipErrorInvalidValue;
     }
 }
 
-template <knn_dtype DT, int CPL, int NQ>
-hipError_t launch_vec_rows(int rows, const DistArgs &a, dim3 grid, hipStream_t st) {
-    return rows == 2 ? launch_vec<DT, CPL, NQ, 2>(a, grid, st) : launch_vec<DT, CPL, NQ, 1>(a, grid, st);
-}
-
 template <knn_dtype DT, int CPL>
-hipError_t launch_vec_nq(int nq, int rows, const DistArgs &a, dim3 grid, hipStream_t st) {
+hipError_t launch_vec_nq(int nq, const DistArgs &a, dim3 grid, hipStream_t st) {
     switch (nq) {
-    case 1: return launch_vec_rows<DT, CPL, 1>(rows, a, grid, st);
-    case 2: return launch_vec_rows<DT, CPL, 2>(rows, a, grid, st);
-    case 4: return launch_vec_rows<DT, CPL, 4>(rows, a, grid, st);
-    case 8: return launch_vec_rows<DT, CPL, 8>(rows, a, grid, st);
+    case 1: return launch_vec<DT, CPL, 1>(a, grid, st);
+    case 2: return launch_vec<DT, CPL, 2>(a, grid, st);
+    case 4: return launch_vec<DT, CPL, 4>(a, grid, st);
+    case 8: return launch_vec<DT, CPL, 8>(a, grid, st);
     default: return hipErrorInvalidValue;
     }
 }
@@ -373,11 +420,11 @@ hipError_t launch_dist_dt(const DistPlan &p, const DistArgs &a, dim3 grid, hipSt
         return hipGetLastError();
     }
     switch (p.cpl) {
-    case 1: return launch_vec_nq<DT, 1>(p.nq, p.rows, a, grid, st);
-    case 2: return launch_vec_nq<DT, 2>(p.nq, p.rows, a, grid, st);
-    case 4: return launch_vec_nq<DT, 4>(p.nq, p.rows, a, grid, st);
-    case 8: return launch_vec_nq<DT, 8>(p.nq, p.rows, a, grid, st);
-    case 16: return launch_vec_nq<DT, 16>(p.nq, p.rows, a, grid, st);
+    case 1: return launch_vec_nq<DT, 1>(p.nq, a, grid, st);
+    case 2: return launch_vec_nq<DT, 2>(p.nq, a, grid, st);
+    case 4: return launch_vec_nq<DT, 4>(p.nq, a, grid, st);
+    case 8: return launch_vec_nq<DT, 8>(p.nq, a, grid, st);
+    case 16: return launch_vec_nq<DT, 16>(p.nq, a, grid, st);
     default: return hipErrorInvalidValue;
     }
 }
@@ -434,7 +481,6 @@ DistPlan plan_distances(int64_t d, knn_dtype dtype, int64_t max_queries, const v
         p.mq = blocks;
         p.cpl = 0;
         p.nq = blocks * 16;
-        p.rows = 1;
         p.groups = (mq + p.nq - 1) / p.nq;
         return p;
     }
@@ -443,13 +489,11 @@ DistPlan plan_distances(int64_t d, knn_dtype dtype, int64_t max_queries, const v
         int nq = 8;
         while (nq > 1 && (nq * p.cpl > kQueryRegChunks || nq / 2 >= mq)) nq >>= 1;
         p.nq = nq;
-        p.rows = 1;  // one row per wave iteration, the next one already loading (measured best)
     } else {
         p.cpl = 0;
         int nq = 8;
         while (nq > 1 && nq / 2 >= mq) nq >>= 1;
         p.nq = nq;
-        p.rows = 1;
     }
     p.rows_per_tile = 0;  // set by the caller from the workspace layout
     p.tiles_per_set = 0;

@@ -209,6 +209,51 @@ def test_precomputed_norms_give_identical_results():
     torch.testing.assert_close(norms, ref, rtol=1e-5, atol=1e-5)
 
 
+# Rows of 16 chunks per lane (d = 8192 for 16-bit keys, d = 4096 for fp32) stream in two halves that add
+# into one sum; d = 4096 bf16 streams whole rows.  Integer coordinates in both halves of every row make every
+# distance an exact integer, so ids and distances must equal the oracle's bit for bit, with the key norms
+# computed on the fly or given, and with a third of the keys masked (a NEST step).
+HALF_ROWS = [("bf16-d8192", torch.bfloat16, 8192), ("f32-d4096", torch.float32, 4096), ("bf16-d4096", torch.bfloat16, 4096)]
+
+
+@pytest.mark.parametrize("masked", [False, True], ids=["unmasked", "masked"])
+@pytest.mark.parametrize("norms", [False, True], ids=["norms-on-the-fly", "norms-given"])
+@pytest.mark.parametrize("name,dtype,d", HALF_ROWS, ids=[h[0] for h in HALF_ROWS])
+def test_streamed_row_halves_exact_integers(name, dtype, d, norms, masked):
+    _say(f"row halves: {name} norms={norms} masked={masked}")
+    n, B, r = 5000, 3, 64
+    rng = np.random.default_rng(97 + d)
+    cols = [0, 1, 2, d // 2 + 3, d - 1000, d - 1]  # both halves of the row (and the last chunk)
+    k = np.zeros((n, d), np.float32)
+    k[:, cols] = rng.integers(-3, 4, (n, len(cols)))
+    q = np.zeros((B, d), np.float32)
+    q[:, cols] = rng.integers(-3, 4, (B, len(cols)))
+    vals = rng.integers(0, 500, n).astype(np.int32)
+    p_lm = rng.dirichlet(np.ones(500), B).astype(np.float32)
+    ko, qo = np.array([0, n]), np.array([0, B])
+    tq, tk, tv, tko, tqo, tp = _tensor_inputs(q, k, vals, p_lm, ko, qo, dtype)
+    kn = knn.key_sqnorms(tk) if norms else None
+    prob = knn.MixtureProblem(tq, tk, tv, tko, tqo, tp, r, 0.05, 0.5, key_sqnorms=kn, key_offsets_host=ko,
+                              query_offsets_host=qo)
+    words = None
+    if masked:
+        rows = rng.choice(n, n // 3, replace=False)
+        words = np.zeros((n + 31) // 32, np.uint32)
+        np.bitwise_or.at(words, rows >> 5, (np.uint32(1) << (rows & 31).astype(np.uint32)))
+        out = prob.run_nest(0.3, 0.1, 0.5, key_mask=knn.mask_words(rows, n, "cuda"))
+        ids, dists = out["ids"], out["dists"]
+    else:
+        _, ids, dists = prob.run()
+    torch.cuda.synchronize()
+    o_ids, o_d = oracle.select(q, k, "f32", ko, qo, r, key_mask=words)
+    np.testing.assert_array_equal(ids.cpu().numpy(), o_ids)
+    np.testing.assert_array_equal(dists.cpu().numpy().astype(np.float64), o_d)
+    if norms:
+        np.testing.assert_array_equal(kn.cpu().numpy().astype(np.float64), (k.astype(np.float64) ** 2).sum(1))
+    del tk, prob
+    _free()
+
+
 def test_element_path_matches_vector_path_bitwise():
     """A key matrix that is not 16-byte aligned takes the element-load path; the
     accumulation order is the same, so every output bit is the same."""
