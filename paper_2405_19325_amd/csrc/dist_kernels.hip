@@ -119,7 +119,6 @@ __global__ __launch_bounds__(kDistThreads) void k_dist_vec(DistArgs a) {
     constexpr int RPI = D / SPR;            // rows per loop iteration
     static_assert(CPL % CPS == 0 && D % SPR == 0, "whole sets per row, whole rows per iteration");
     constexpr int EB = Elem<DT>::BYTES;
-    clear_arrivals(a, kDistThreads);
     TileWork t;
     if (!tile_work<NQ>(a, t)) return;
 
@@ -261,7 +260,6 @@ __global__ __launch_bounds__(kDistThreads) void k_dist_elem(DistArgs a) {
     constexpr int EB = Elem<DT>::BYTES;
     constexpr int PW = Elem<DT>::PER_WORD;
     constexpr int NW = kWavesPerDistBlock;
-    clear_arrivals(a, kDistThreads);
     TileWork t;
     if (!tile_work<NQ>(a, t)) return;
 

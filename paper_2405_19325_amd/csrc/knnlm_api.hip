@@ -40,8 +40,7 @@ Layout layout(int64_t B, int64_t d, int64_t S, int64_t max_keys, int64_t max_que
     const size_t np = static_cast<size_t>(L.split_parts) * static_cast<size_t>(B);  // 0 unless split or wide
     L.off_count = align_up(L.off_cand + sizeof(uint64_t) * kSplitKeys * np);
     L.off_thr = align_up(L.off_count + 2 * sizeof(uint32_t) * np);  // counts, then minima
-    // thresholds, then the split select's arrival counters
-    L.total = align_up(L.off_thr + (L.split_parts > 0 ? 2 * sizeof(uint32_t) * static_cast<size_t>(B) : 0));
+    L.total = align_up(L.off_thr + (L.split_parts > 0 ? sizeof(uint32_t) * static_cast<size_t>(B) : 0));
     return L;
 }
 
@@ -192,10 +191,6 @@ knn_status run_part(const Call &c, int part, hipStream_t stream) {
         a.tiles_per_set = L.tiles_per_set;
         a.rows_per_tile = L.rows_per_tile;
         a.key_mask = c.key_mask;
-        if (part_thr != nullptr && select_split_parts(c.B, L.ld, c.r) > 0) {
-            a.arrive = part_thr + c.B;
-            a.n_arrive = c.B;
-        }
         return status_of(launch_distances(p, c.dtype, a, c.S, stream));
     }
     if (part == KNN_PART_SELECT || part == KNN_PART_SELECT_MIX) {
@@ -216,7 +211,6 @@ knn_status run_part(const Call &c, int part, hipStream_t stream) {
         a.part_count = part_count;
         a.part_min = part_count ? part_count + L.split_parts * c.B : nullptr;
         a.part_thr = part_thr;
-        a.arrive = part_thr ? part_thr + c.B : nullptr;
         if (part == KNN_PART_SELECT) return status_of(launch_select(a, c.B, stream));
         return status_of(launch_select_mix(a, mix_args(c), c.B, stream));
     }

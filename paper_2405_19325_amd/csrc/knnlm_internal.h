@@ -46,17 +46,7 @@ struct DistArgs {
     int64_t tiles_per_set;
     int rows_per_tile;
     const uint32_t *key_mask;    // bit (i & 31) of word i >> 5 set: global key row i is masked; or null
-    uint32_t *arrive;            // [n_arrive] words the first workgroup sets to 0 (the split select's counters), or null
-    int64_t n_arrive;
 };
-
-// Sets the split select's per-query counters to 0: run by the first
-// workgroup of every distance kernel, before anything else, so that the
-// select that follows on the stream starts from 0.
-__device__ __forceinline__ void clear_arrivals(const DistArgs &a, int nthreads) {
-    if (a.arrive != nullptr && blockIdx.x == 0 && blockIdx.y == 0)
-        for (int64_t i = threadIdx.x; i < a.n_arrive; i += nthreads) a.arrive[i] = 0u;
-}
 
 // A masked key row is at distance +infinity (bits kMaskedBits), above every
 // real distance, and stays out of the per-tile extrema.

@@ -110,7 +110,6 @@ __global__ __launch_bounds__(WK * WQ * kWave, 1) void k_dist_mfma(DistArgs a, in
     // Consecutive workgroups land on different XCDs (round robin over 8).  The
     // query groups of one key tile are numbered 8 apart, so they run on one XCD
     // at about the same time and all but the first read the tile from its L2.
-    clear_arrivals(a, kThreads);
     const int64_t L = blockIdx.x;
     const int64_t grp = (L >> 3) % groups;
     const int64_t tl = ((L >> 3) / groups) * 8 + (L & 7);

@@ -22,7 +22,6 @@ struct SelectArgs {
     uint32_t *part_count;        // split select: [B, parts] candidates per part
     uint32_t *part_min;          // split select: [B, parts] smallest candidate distance bits per part
     uint32_t *part_thr;          // split select: [B] threshold on the distance bits
-    uint32_t *arrive;            // split select (short rows): [B] parts of each query done so far, 0 between calls
 };
 
 struct MixArgs {

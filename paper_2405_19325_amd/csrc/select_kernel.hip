@@ -879,10 +879,10 @@ __global__ __launch_bounds__(kT) void k_select_fast(SelectArgs a, MixArgs m) {
 
 // Split path: rows of at most kSplitMaxN keys, r <= kSplitMaxR, few queries.
 // Query b's row is cut into `parts` parts of kSplitKeys keys so that one query
-// keeps many CUs busy; one kernel (k_select_split below): a parts step in every
-// workgroup, then a finish step in the last of each query's parts.
+// keeps many CUs busy; two kernels, and no atomics or fences between
+// workgroups (the kernel boundary orders them).
 //
-// Parts step: every part of query b reads
+// Parts kernel (blockIdx.x = b * parts + part): every part of query b reads
 // the same kSplitSamples keys sampled across the row (1024 runs of 4
 // consecutive keys, one run every N / 1024) and takes as threshold the end of the histogram bin, over the
 // samples' own range, that holds the ks-th smallest of them, ks aiming at
@@ -896,11 +896,14 @@ __global__ __launch_bounds__(kT) void k_select_fast(SelectArgs a, MixArgs m) {
 constexpr int kSplitSamples = 4 * kT;
 
 template <int MODE>
-__device__ __forceinline__ void split_part(const SelectArgs &a, const MixArgs &m, int parts, int64_t b, int part,
-                                           uint32_t *hist, Shared &sh) {
+__global__ __launch_bounds__(kT) void k_select_parts(SelectArgs a, MixArgs m, int parts) {
     constexpr bool DENSE = MODE == kMixFixed;  // the dense term lambda * p_LM is known here
+    __shared__ __align__(16) uint32_t hist[kSelectBins];
+    __shared__ Shared sh;
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
+    const int64_t b = blockIdx.x / parts;
+    const int part = static_cast<int>(blockIdx.x - b * parts);
     const float *drow = a.dist + b * a.ld;
     const int64_t ld = a.ld < kSplitMaxN ? a.ld : kSplitMaxN;  // the host launches this kernel only when ld <= kSplitMaxN
     if (tid == 0) {
@@ -1022,7 +1025,7 @@ __device__ __forceinline__ void split_part(const SelectArgs &a, const MixArgs &m
     }
 }
 
-// Finish step (one workgroup per query).  It loads the part counts together
+// Finish kernel (one workgroup per query).  It loads the part counts together
 // with the first kSplitCap / parts entries of every list, gathers the
 // candidates into LDS (the rest of a longer list afterwards), and bucket-sorts
 // them on their distance bits while their tokens load.  Then it writes pi;
@@ -1042,27 +1045,25 @@ __device__ __forceinline__ void finish_sort(uint64_t *cand, uint32_t total, uint
                                              NoHook(), keep);
 }
 
-constexpr int kSplitSortBytes = 2 * kSplitCap * 8 + (8 << kFinishBinsLog2);
 template <int MODE>
-constexpr int split_smem_bytes() {  // + tokens, + room for the vocabulary tile
-    return MODE != kNoMix ? kSplitSortBytes + kSplitCap * 4 + 16384 : kSplitSortBytes;
-}
-
-template <int MODE>
-__device__ __forceinline__ void split_finish(const SelectArgs &a, const MixArgs &m, int parts, int64_t b,
-                                             unsigned char *smem, Shared &sh, uint32_t *part_off) {
+__global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, int parts) {
     constexpr bool MIX = MODE != kNoMix;
     constexpr int PER = kSplitCap / kT;
-    constexpr int kSortBytes = kSplitSortBytes;
-    static_assert(!MIX || kVocabTileFast * 4 <= split_smem_bytes<MODE>(), "the vocabulary tile fits over the sort buffers");
+    constexpr int kSortBytes = 2 * kSplitCap * 8 + (8 << kFinishBinsLog2);
+    constexpr int kSmem = MIX ? kSortBytes + kSplitCap * 4 + 16384 : kSortBytes;  // + tokens, + room for the tile
+    static_assert(!MIX || kVocabTileFast * 4 <= kSmem, "the vocabulary tile fits over the sort buffers");
+    __shared__ __align__(16) unsigned char smem[kSmem];
     uint64_t *cand = reinterpret_cast<uint64_t *>(smem);                          // [kSplitCap]
     uint64_t *tmp = cand + kSplitCap;                                              // [kSplitCap]
     uint32_t *hist = reinterpret_cast<uint32_t *>(tmp + kSplitCap);                // [2 << kFinishBinsLog2]: counts, starts
     int32_t *tok_of = reinterpret_cast<int32_t *>(smem + kSortBytes);              // [kSplitCap]
     float *acc = reinterpret_cast<float *>(smem);  // mixture: a vocabulary tile, over everything above
+    __shared__ Shared sh;
+    __shared__ uint32_t part_off[kWave + 1];
 
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
+    const int64_t b = blockIdx.x;
     const uint64_t *lists = a.cand + b * parts * kSplitKeys;
 
     // Counts, threshold and the first `win` entries of every list, all in flight together.
@@ -1210,38 +1211,6 @@ __device__ __forceinline__ void split_finish(const SelectArgs &a, const MixArgs 
             if (in) m.p_m[b * m.V + tok] = fmaf(lam, plm_t, acc[tok - t0] * scale);
         }
     }
-}
-
-// Split select kernel (blockIdx.x = b * parts + part): every workgroup runs
-// the parts step for its part of query b; the last of query b's parts to
-// finish it runs the finish step.  A part publishes its list, count and
-// minimum with an agent-scope release before it counts itself in
-// arrive[b] (an agent-scope atomic); the part that takes the count to
-// `parts` acquires at agent scope, so that it sees every part's list (the
-// L2 caches of the XCDs are not coherent with each other), and sets
-// arrive[b] back to 0 for the next call (the distance stage also clears it).
-// No workgroup waits for another.
-template <int MODE>
-__global__ __launch_bounds__(kT) void k_select_split(SelectArgs a, MixArgs m, int parts) {
-    __shared__ __align__(16) unsigned char smem[split_smem_bytes<MODE>()];
-    static_assert(kSelectBins * 4 <= split_smem_bytes<MODE>(), "the parts histogram fits in the finish's buffers");
-    __shared__ Shared sh;
-    __shared__ uint32_t part_off[kWave + 1];
-    __shared__ uint32_t last;
-    const int64_t b = blockIdx.x / parts;
-    const int part = static_cast<int>(blockIdx.x - b * parts);
-    split_part<MODE>(a, m, parts, b, part, reinterpret_cast<uint32_t *>(smem), sh);  // ends with thread 0's stores
-    if (threadIdx.x == 0) {
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-        const uint32_t before = __hip_atomic_fetch_add(a.arrive + b, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        const bool fin = before == static_cast<uint32_t>(parts - 1);
-        if (fin) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-        last = fin ? 1u : 0u;
-    }
-    __syncthreads();
-    if (last == 0u) return;
-    split_finish<MODE>(a, m, parts, b, smem, sh, part_off);
-    if (threadIdx.x == 0) a.arrive[b] = 0u;
 }
 
 // Standalone mixture on caller-given neighbours (any order): one workgroup per query.
@@ -1543,9 +1512,11 @@ hipError_t launch_sel(const SelectArgs &a, const MixArgs &m, int64_t B, hipStrea
     const dim3 grid(static_cast<unsigned>(B)), block(kT);
     const int parts = select_split_parts(B, a.ld, a.r);
     if (parts > 0) {
-        if (a.cand == nullptr || a.part_count == nullptr || a.part_thr == nullptr || a.arrive == nullptr)
-            return hipErrorInvalidValue;
-        hipLaunchKernelGGL((k_select_split<MODE>), dim3(static_cast<unsigned>(B * parts)), block, 0, st, a, m, parts);
+        if (a.cand == nullptr || a.part_count == nullptr || a.part_thr == nullptr) return hipErrorInvalidValue;
+        hipLaunchKernelGGL((k_select_parts<MODE>), dim3(static_cast<unsigned>(B * parts)), block, 0, st, a, m, parts);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL((k_select_finish<MODE>), grid, block, 0, st, a, m, parts);
         return hipGetLastError();
     }
     const int wparts = select_wide_parts(B, a.ld, a.r, a.tiles_per_set);
