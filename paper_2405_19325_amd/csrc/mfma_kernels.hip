@@ -37,7 +37,11 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
-constexpr int kPassKeys = 128;  // keys per pass: 8 blocks of 16, two per wave
+constexpr int kTileQuantum = 256;  // tile rows are multiples of the largest pass (256 keys)
+
+// Where the epilogue stores the (discarded) distances of rows past the tile or
+// query slots past the group: one word per device, written, never read.
+__device__ float g_mfma_sink;
 
 template <knn_dtype DT>
 __device__ __forceinline__ f32x4_t mfma16(const u32x4_t a, const u32x4_t b, f32x4_t c) {
@@ -81,29 +85,36 @@ __device__ __forceinline__ float group4_sum(float v) {
     return v;
 }
 
-constexpr int kSpan = kMfmaSpan;                 // elements of d per pipeline step (256 bytes of a row)
-constexpr int kChunks = kSpan * 2 / 16;          // 16-byte chunks per row and span
+constexpr int kSpan = kMfmaSpan;  // d is a multiple of this (the largest span)
 
-// Slot of chunk c of row n in a swizzled LDS span buffer.
-__device__ __forceinline__ int swz(int n, int c) { return n * kChunks + (c ^ (n & 15)); }
+// Slot of chunk c of row n in a swizzled LDS span buffer of CH 16-byte chunks per row.
+template <int CH>
+__device__ __forceinline__ int swz(int n, int c) { return n * CH + (c ^ (n & (CH - 1))); }
 
 // MQ: 16-query blocks per workgroup; WK x WQ waves: WK groups split the
-// pass's eight key blocks (8 / WK each), WQ groups split the query blocks
-// (MQ / WQ each); NS: register sets of prefetched spans (NS spans in
-// flight); NORMS: ||k||^2 comes precomputed.
-template <knn_dtype DT, int MQ, int WK, int WQ, int NS, bool NORMS>
+// pass's PK / 16 key blocks, WQ groups split the query blocks (MQ / WQ each);
+// NS: register sets of prefetched spans (NS spans in flight); NORMS: ||k||^2
+// comes precomputed; PK keys per pass and SPAN elements of d per pipeline
+// step.  A wide query block re-stages its span in LDS once per pass, so
+// 128-query workgroups take 256-key passes of 64-element spans (the same
+// matrix-core work per step as 128 keys x 128 elements, with a quarter less
+// loaded and written to LDS per step, a third less read from it).
+template <knn_dtype DT, int MQ, int WK, int WQ, int NS, bool NORMS, int PK, int SPAN>
 __global__ __launch_bounds__(WK * WQ * kWave, 1) void k_dist_mfma(DistArgs a, int64_t n_tiles, int64_t groups) {
     constexpr int QW = WQ;
-    constexpr int KBW = 8 / WK;                          // key blocks per wave
+    constexpr int kChunks = SPAN * 2 / 16;               // 16-byte chunks per row and span
+    constexpr int KSTEPS = SPAN / 32;                    // MFMA steps per span
+    constexpr int KBW = PK / 16 / WK;                    // key blocks per wave
     constexpr int kThreads = WK * WQ * kWave;
     constexpr int QB = MQ * 16;
     constexpr int MQW = MQ / QW;                         // query blocks per wave
-    constexpr int KCH = kPassKeys * kChunks / kThreads;  // key chunks per thread and step
+    constexpr int KCH = PK * kChunks / kThreads;         // key chunks per thread and step
     constexpr int QCH = QB * kChunks / kThreads;         // query chunks per thread and step
-    static_assert(MQ % QW == 0 && 8 % WK == 0 && KCH >= 1 && QCH >= 1, "whole blocks and chunks");
+    static_assert(MQ % QW == 0 && (PK / 16) % WK == 0 && KCH >= 1 && QCH >= 1, "whole blocks and chunks");
+    static_assert(SPAN % 32 == 0 && kSpan % SPAN == 0 && kChunks <= 16, "whole MFMA steps, spans dividing d");
     // native 4 x u32 vectors throughout, so that every 16-byte LDS access is
     // one ds_read_b128 / ds_write_b128 (a struct is split by the compiler)
-    __shared__ __align__(16) u32x4_t klds[2][kPassKeys * kChunks];
+    __shared__ __align__(16) u32x4_t klds[2][PK * kChunks];
     __shared__ __align__(16) u32x4_t qlds[2][QB * kChunks];
     __shared__ uint32_t smin[QB], smax[QB];
 
@@ -133,8 +144,8 @@ __global__ __launch_bounds__(WK * WQ * kWave, 1) void k_dist_mfma(DistArgs a, in
     const int jq = ((tid / kWave) % QW) * MQW;  // its first query block
     const int g = lane >> 4, lr = lane & 15;
     const int64_t row_bytes = a.d * 2;
-    const int64_t nspan = a.d / kSpan;
-    const int64_t npass = (r1 - r0 + kPassKeys - 1) / kPassKeys;
+    const int64_t nspan = a.d / SPAN;
+    const int64_t npass = (r1 - r0 + PK - 1) / PK;
     const int64_t T = npass * nspan;  // pipeline steps of this tile
     const char *qbase = static_cast<const char *>(a.queries) + qb * row_bytes;
     const char *kset = static_cast<const char *>(a.keys) + k0 * row_bytes;
@@ -144,13 +155,15 @@ __global__ __launch_bounds__(WK * WQ * kWave, 1) void k_dist_mfma(DistArgs a, in
         smax[q] = 0u;
     }
 
-    // Loads: chunk i of this thread is row i * 16 + tid / 16 of the pass (keys)
-    // or of the query block, 16-byte column tid % 16 of the span; its LDS slot
-    // swz(i * 16 + rsub, col) is i * 256 + slot0.
+    // Loads: chunk i of this thread is row i * R + tid / kChunks of the pass
+    // (keys) or of the query block, 16-byte column tid % kChunks of the span
+    // (R = kThreads / kChunks rows per chunk index, a multiple of 16, so its
+    // LDS slot swz(i * R + rsub, col) is i * R * kChunks + slot0).
     const int col = tid & (kChunks - 1);
     const int rsub = tid / kChunks;
-    const int slot0 = swz(rsub, col);
-    constexpr int kRowsPerChunk = kThreads / kChunks;  // 16 rows per chunk index
+    const int slot0 = swz<kChunks>(rsub, col);
+    constexpr int kRowsPerChunk = kThreads / kChunks;
+    static_assert(kRowsPerChunk % 16 == 0, "the swizzle repeats every 16 rows");
 
     // Addresses: a uniform base per step plus a 32-bit offset per chunk (a
     // tile is at most 4096 rows of at most 128 KiB).
@@ -169,9 +182,9 @@ __global__ __launch_bounds__(WK * WQ * kWave, 1) void k_dist_mfma(DistArgs a, in
     const uint32_t ns = static_cast<uint32_t>(nspan);  // steps fit 32 bits: at most 32 passes of 512 spans
     auto load = [&](int set, int64_t t) __attribute__((always_inline)) {
         const uint32_t p = static_cast<uint32_t>(t) / ns, sp = static_cast<uint32_t>(t) - p * ns;
-        const char *kspan = ktile + static_cast<int64_t>(sp) * (2 * kSpan);
-        const char *qspan = qbase + static_cast<int64_t>(sp) * (2 * kSpan);
-        const uint32_t prow = p * kPassKeys + static_cast<uint32_t>(rsub);
+        const char *kspan = ktile + static_cast<int64_t>(sp) * (2 * SPAN);
+        const char *qspan = qbase + static_cast<int64_t>(sp) * (2 * SPAN);
+        const uint32_t prow = p * PK + static_cast<uint32_t>(rsub);
 #pragma unroll
         for (int i = 0; i < KCH; ++i) {
             const uint32_t rr = prow + static_cast<uint32_t>(i * kRowsPerChunk);
@@ -190,18 +203,8 @@ __global__ __launch_bounds__(WK * WQ * kWave, 1) void k_dist_mfma(DistArgs a, in
 
     f32x4_t acc[MQW][KBW];
     float kkp[KBW], qqp[MQW];
-    // per lane: the smallest and largest distance of each of its queries over
-    // the tile (reduced across lanes once, at the end)
-    float tmn[MQW][4], tmx[MQW][4];
 #pragma unroll
-    for (int j = 0; j < MQW; ++j) {
-        qqp[j] = 0.0f;  // ||q||^2 partials: the first pass adds them up, later passes reuse them
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            tmn[j][i] = __builtin_huge_valf();
-            tmx[j][i] = 0.0f;
-        }
-    }
+    for (int j = 0; j < MQW; ++j) qqp[j] = 0.0f;  // ||q||^2 partials: the first pass adds them up, later passes reuse them
     auto clear = [&]() __attribute__((always_inline)) {
 #pragma unroll
         for (int j = 0; j < MQW; ++j)
@@ -213,12 +216,12 @@ __global__ __launch_bounds__(WK * WQ * kWave, 1) void k_dist_mfma(DistArgs a, in
     clear();
 
     // The matrix cores over one span in LDS buffer buf (with qn_pass, also
-    // the query norms); the four MFMA steps unrolled, so that the next
+    // the query norms); the span's MFMA steps unrolled, so that the next
     // step's fragment reads overlap this step's MFMAs.
     auto compute = [&](int buf, bool qn_pass) __attribute__((always_inline)) {
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            const int ch = (4 * c + g) ^ lr;
+        for (int c = 0; c < KSTEPS; ++c) {
+            const int ch = (4 * c + g) ^ (lr & (kChunks - 1));
             u32x4_t bk[KBW], af[MQW];
 #pragma unroll
             for (int kb = 0; kb < KBW; ++kb) bk[kb] = klds[buf][((wave * KBW + kb) * 16 + lr) * kChunks + ch];
@@ -242,7 +245,7 @@ __global__ __launch_bounds__(WK * WQ * kWave, 1) void k_dist_mfma(DistArgs a, in
     // Distances of pass p: lane (g, lr) holds dot(query (jq + j)*16 + 4g + i,
     // key c0 + (wave*KBW + kb)*16 + lr) in acc[j][kb][i].
     auto epilogue = [&](int64_t p) __attribute__((always_inline)) {
-        const int64_t c0 = r0 + p * kPassKeys;
+        const int64_t c0 = r0 + p * PK;
         float kk[KBW];
         bool mk[KBW];  // masked key rows (Section 3.4): distance +infinity, no part in the extrema
 #pragma unroll
@@ -251,6 +254,8 @@ __global__ __launch_bounds__(WK * WQ * kWave, 1) void k_dist_mfma(DistArgs a, in
             kk[kb] = NORMS ? (row < r1 ? a.key_sqnorms[k0 + row] : 0.0f) : group4_sum(kkp[kb]);
             mk[kb] = a.key_mask != nullptr && row < r1 && key_masked(a.key_mask, k0 + row);
         }
+        // the pass's extrema of each query fold into the tile's (LDS atomics) here,
+        // so that no per-lane extrema stay live through the main loop
 #pragma unroll
         for (int j = 0; j < MQW; ++j) {
             const float qsum = group4_sum(qqp[j]);  // ||q||^2 of query (jq + j)*16 + lr
@@ -258,17 +263,23 @@ __global__ __launch_bounds__(WK * WQ * kWave, 1) void k_dist_mfma(DistArgs a, in
             for (int i = 0; i < 4; ++i) {
                 const int q = (jq + j) * 16 + g * 4 + i;
                 const float qn = __shfl(qsum, g * 4 + i);
+                float tmn = __builtin_huge_valf(), tmx = 0.0f;
 #pragma unroll
                 for (int kb = 0; kb < KBW; ++kb) {
                     const int64_t row = c0 + (wave * KBW + kb) * 16 + lr;
                     const float dist = mk[kb] ? __uint_as_float(kMaskedBits)
                                               : clamp_nonneg(fmaf(-2.0f, acc[j][kb][i], qn + kk[kb]));
                     const bool ok = q < nq && row < r1;
-                    if (ok) a.dist[(qb + q) * a.ld + row] = dist;
-                    if (ok && !mk[kb]) {
-                        tmn[j][i] = fminf(tmn[j][i], dist);
-                        tmx[j][i] = fmaxf(tmx[j][i], dist);
-                    }
+                    // no branch around the store (nor any other memory operation in the loop)
+                    *(ok ? a.dist + (qb + q) * a.ld + row : &g_mfma_sink) = dist;
+                    tmn = ok && !mk[kb] ? fminf(tmn, dist) : tmn;
+                    tmx = ok && !mk[kb] ? fmaxf(tmx, dist) : tmx;
+                }
+                tmn = row16_min(tmn);
+                tmx = row16_max(tmx);
+                if (lr == 0 && q < nq) {
+                    atomicMin(&smin[q], __float_as_uint(tmn));
+                    atomicMax(&smax[q], __float_as_uint(tmx));
                 }
             }
         }
@@ -307,19 +318,7 @@ __global__ __launch_bounds__(WK * WQ * kWave, 1) void k_dist_mfma(DistArgs a, in
         }
     }
 
-    // the tile's extrema of each query: over the 16 keys of a lane row, then
-    // over the lanes and waves with LDS atomics
-#pragma unroll
-    for (int j = 0; j < MQW; ++j)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int q = (jq + j) * 16 + g * 4 + i;
-            const float mn = row16_min(tmn[j][i]), mx = row16_max(tmx[j][i]);
-            if (lr == 0 && q < nq) {
-                atomicMin(&smin[q], __float_as_uint(mn));
-                atomicMax(&smax[q], __float_as_uint(mx));
-            }
-        }
+    // the tile's extrema of each query (folded in by every pass's epilogue)
     if (a.tile_min != nullptr) {
         __syncthreads();
         for (int q = tid; q < nq; q += kThreads) {
@@ -333,10 +332,10 @@ template <knn_dtype DT, bool NORMS>
 hipError_t launch_mq(int mq, const DistArgs &a, int64_t n_tiles, int64_t groups, dim3 grid, hipStream_t st) {
     const dim3 b4(4 * kWave), b8(8 * kWave);
     switch (mq) {
-    case 1: hipLaunchKernelGGL((k_dist_mfma<DT, 1, 4, 1, 3, NORMS>), grid, b4, 0, st, a, n_tiles, groups); break;
-    case 2: hipLaunchKernelGGL((k_dist_mfma<DT, 2, 4, 1, 3, NORMS>), grid, b4, 0, st, a, n_tiles, groups); break;
-    case 4: hipLaunchKernelGGL((k_dist_mfma<DT, 4, 4, 1, 3, NORMS>), grid, b4, 0, st, a, n_tiles, groups); break;
-    case 8: hipLaunchKernelGGL((k_dist_mfma<DT, 8, 4, 2, 2, NORMS>), grid, b8, 0, st, a, n_tiles, groups); break;
+    case 1: hipLaunchKernelGGL((k_dist_mfma<DT, 1, 4, 1, 3, NORMS, 128, 128>), grid, b4, 0, st, a, n_tiles, groups); break;
+    case 2: hipLaunchKernelGGL((k_dist_mfma<DT, 2, 4, 1, 3, NORMS, 128, 128>), grid, b4, 0, st, a, n_tiles, groups); break;
+    case 4: hipLaunchKernelGGL((k_dist_mfma<DT, 4, 4, 1, 3, NORMS, 128, 128>), grid, b4, 0, st, a, n_tiles, groups); break;
+    case 8: hipLaunchKernelGGL((k_dist_mfma<DT, 8, 4, 2, 2, NORMS, 256, 64>), grid, b8, 0, st, a, n_tiles, groups); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -350,20 +349,22 @@ hipError_t launch_dt(int mq, const DistArgs &a, int64_t n_tiles, int64_t groups,
 
 }  // namespace
 
-// Key rows per workgroup: at least two passes, and enough passes that a tile
-// runs at least 64 pipeline steps (spans), at most 32 passes.
+// Key rows per workgroup: at least 256, and enough that a tile runs at least
+// 64 pipeline steps of 128 keys x 128 elements, at most 4096 rows; always a
+// multiple of 256, so that both pass sizes divide it.
 int mfma_tile_rows(int64_t d) {
     const int64_t nspan = d / kSpan > 0 ? d / kSpan : 1;
-    int64_t passes = (64 + nspan - 1) / nspan;
-    if (passes < 2) passes = 2;
-    if (passes > 32) passes = 32;
-    return static_cast<int>(passes * kPassKeys);
+    int64_t rows = (64 + nspan - 1) / nspan * 128;
+    rows = (rows + kTileQuantum - 1) / kTileQuantum * kTileQuantum;
+    if (rows < kTileQuantum) rows = kTileQuantum;
+    if (rows > 4096) rows = 4096;
+    return static_cast<int>(rows);
 }
 
 hipError_t launch_distances_mfma(int mq, knn_dtype dtype, const DistArgs &args, int64_t S, int64_t groups,
                                  hipStream_t stream) {
     const int64_t n_tiles = S * args.tiles_per_set;
-    if (groups < 1 || args.rows_per_tile % kPassKeys != 0 || args.d % kSpan != 0) return hipErrorInvalidConfiguration;
+    if (groups < 1 || args.rows_per_tile % kTileQuantum != 0 || args.d % kSpan != 0) return hipErrorInvalidConfiguration;
     const int64_t nblocks = (n_tiles + 7) / 8 * 8 * groups;
     if (nblocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
     const dim3 grid(static_cast<unsigned>(nblocks));
