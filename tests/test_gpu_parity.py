@@ -437,11 +437,20 @@ def test_matrix_core_workloads(name, spec, seed):
     assert rep2.ok(), rep2.failures[:5]
 
 
+# (queries, d): 37 queries take one 64-query group of 128-key passes of 128-element spans; 130 queries take
+# two 128-query groups (the second holding 2) of 256-key passes of 64-element spans, and d = 640 gives tiles
+# of 1792 rows (7 such passes), the last tile of the row partial.
+MFMA_EXACT = [(37, 256), (130, 640)]
+
+
+@pytest.mark.parametrize("B,d", MFMA_EXACT, ids=[f"{b}q-d{d}" for b, d in MFMA_EXACT])
 @pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float16])
-def test_matrix_core_exact_integers(dtype):
-    _say(f"matrix-core exact integers {dtype}")
-    rng = np.random.default_rng(41)
-    B, n, d, r = 37, 3000, 64, 300
+def test_matrix_core_exact_integers(dtype, B, d):
+    """Integer queries and keys in [-4, 4]: every dot product and norm is exact in fp32, so the matrix-core
+    path must give the oracle's ids and distances bit for bit."""
+    _say(f"matrix-core exact integers {dtype} B={B} d={d}")
+    rng = np.random.default_rng(41 + d)
+    n, r = 3000, 300
     q = rng.integers(-4, 5, (B, d)).astype(np.float32)
     k = rng.integers(-4, 5, (n, d)).astype(np.float32)
     vals = rng.integers(0, 500, n).astype(np.int32)
