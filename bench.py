@@ -205,6 +205,25 @@ def main():
     nest_step = {"ms_per_step": round(nest_ms, 5), "queries_per_s": round(B / (nest_ms / 1e3), 1), "steps": n_nest,
                  "alpha": 0.3, "tau": 0.1, "delta": 0.5, "gamma": 0.05, "masked_keys": int(len(masked))}
 
+    # The key-norm pre-pass (knn_key_sqnorms, row (a1)): run once per datastore
+    # before the decode loop, so it is reported apart from the step.
+    # Algorithmic bytes: every key once, plus 4 bytes written per key.
+    n_norm = min(a.steps, 50)
+    norm_out = torch.empty(total_keys, dtype=torch.float32, device=dev)
+    for i in range(2):
+        knn.key_sqnorms(probs[i % 2].keys, out=norm_out)
+    torch.cuda.synchronize()
+    k_start, k_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    k_start.record(stream)
+    for i in range(n_norm):
+        knn.key_sqnorms(probs[i % 2].keys, out=norm_out)
+    k_end.record(stream)
+    torch.cuda.synchronize()
+    norm_ms = k_start.elapsed_time(k_end) / n_norm
+    norm_bytes = total_keys * (spec.d * w.keys.element_size() + 4)
+    key_norms = {"ms_per_launch": round(norm_ms, 5), "alg_bytes": int(norm_bytes), "launches": n_norm,
+                 "hbm_frac": round(norm_bytes / (norm_ms / 1e3) / 1e9 / PEAK_HBM_GBS, 4)}
+
     max_q = int(np.diff(w.query_offsets_host).max())
     matrix_core = spec.dtype in ("bf16", "f16") and spec.d % 8 == 0 and max_q >= 16
     achieved = dist_alg_bytes / (dist_launch_ms / 1e3) / 1e9
@@ -239,7 +258,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": spec.dtype,
         "data": "synthetic (seeded N(0,1)*8/sqrt(d) keys and queries, Zipf(1.1) values, softmax N(0,2) p_LM)",
         "config": {
             "workload": (f"{spec.name}: B={B} queries, d={spec.d}, {spec.S} key set(s), N={total_keys} "
@@ -257,6 +276,7 @@ def main():
         "distance_topr": topr,
         "rrc_step": rrc,
         "nest_step": nest_step,
+        "key_norms_prepass": key_norms,
         "host_wall_s": round(wall, 3),
         "roofline": roofline,
         "cpu_baseline": cpu,

@@ -205,10 +205,14 @@ def distances(queries, keys, key_offsets, query_offsets, key_sqnorms=None, key_o
     return out
 
 
-def key_sqnorms(keys: torch.Tensor) -> torch.Tensor:
-    """knn_key_sqnorms: ||k||^2 per row, fp32, with the summation order knn_lm_mixture uses."""
+def key_sqnorms(keys: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """knn_key_sqnorms: ||k||^2 per row, fp32, with the summation order knn_lm_mixture uses (into `out`
+    when given: a contiguous [rows] fp32 device tensor)."""
     _need(keys.is_cuda and keys.is_contiguous() and keys.dim() == 2, "keys: contiguous 2-D device tensor")
-    out = torch.empty(keys.shape[0], dtype=torch.float32, device=keys.device)
+    if out is None:
+        out = torch.empty(keys.shape[0], dtype=torch.float32, device=keys.device)
+    _need(out.is_cuda and out.dtype == torch.float32 and out.is_contiguous() and out.numel() == keys.shape[0],
+          "out: contiguous [rows] fp32 device tensor")
     st = load().knn_key_sqnorms(_ptr(keys), keys.shape[0], keys.shape[1], _dtype_code(keys), _ptr(out),
                                 _stream(None))
     _lib.check("knn_key_sqnorms", st)

@@ -333,25 +333,65 @@ __global__ __launch_bounds__(kDistThreads) void k_dist_elem(DistArgs a) {
 
 // ------------------------------------------------------------ key norms
 
+// ||k||^2 per row: the wave-per-row layout and word order of the distance
+// kernel (so the values equal its on-the-fly norms bit for bit), over a fixed
+// grid whose waves stride over the rows, two rows in flight per wave in
+// register sets used in turn (half-row sets for 16-chunk rows), every load
+// unconditional: rows past the end read row 0 and store into a sink word.
 template <knn_dtype DT, int CPL>
 __global__ __launch_bounds__(kDistThreads) void k_sqnorm_vec(const void *keys, int64_t n, int64_t d, float *out) {
     constexpr int EB = Elem<DT>::BYTES;
+    constexpr int CPS = CPL > 8 ? 8 : CPL;  // chunks per set
+    constexpr int SPR = CPL / CPS;          // sets per row
+    constexpr int D = 2 * SPR;              // sets in flight: two rows
     const int lane = threadIdx.x & (kWave - 1);
     const int64_t wave_global = (static_cast<int64_t>(blockIdx.x) * kDistThreads + threadIdx.x) / kWave;
     const int64_t nwaves = static_cast<int64_t>(gridDim.x) * (kDistThreads / kWave);
     const int nchunks = static_cast<int>(d * EB / 16);
-    for (int64_t row = wave_global; row < n; row += nwaves) {
-        const uint4 *krow = reinterpret_cast<const uint4 *>(static_cast<const char *>(keys) + row * d * EB);
-        float acc = 0.0f;
+    const int64_t row_bytes = d * EB;
+    const char *base = static_cast<const char *>(keys);
+    const u32x4_t zero = {0u, 0u, 0u, 0u};
+    u32x4_t kv[D][CPS];
+    int64_t rc[D];
+    bool in[D];
+    float acc = 0.0f;
+    auto load = [&](int s, int64_t rw) __attribute__((always_inline)) {
+        const int part = s % SPR;
+        const bool inside = rw < n;
+        rc[s] = inside ? rw : 0;
+        in[s] = inside;
+        const char *krow = base + rc[s] * row_bytes;
 #pragma unroll
-        for (int c = 0; c < CPL; ++c) {
-            const int ch = lane + kWave * c;
-            const uint4 v = (ch < nchunks) ? krow[ch] : make_uint4(0u, 0u, 0u, 0u);
-            acc = dot_chunk<DT>(v, v, acc);
+        for (int c = 0; c < CPS; ++c) {
+            const int ch = lane + kWave * (part * CPS + c);
+            kv[s][c] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(krow + 16 * (ch < nchunks ? ch : 0)));
         }
-        acc = wave_allsum(acc);
-        if (lane == 0) out[row] = acc;
+    };
+    auto consume = [&](int s) __attribute__((always_inline)) {
+        const int part = s % SPR;
+        if (part == 0) acc = 0.0f;
+#pragma unroll
+        for (int c = 0; c < CPS; ++c) {
+            const u32x4_t kc = lane + kWave * (part * CPS + c) < nchunks ? kv[s][c] : zero;
+            const uint4 k4 = make_uint4(kc.x, kc.y, kc.z, kc.w);
+            acc = dot_chunk<DT>(k4, k4, acc);
+        }
+        if (part != SPR - 1) return;
+        const float v = wave_allsum(acc);
+        *(in[s] ? out + rc[s] : &g_dist_sink) = v;
+    };
+    int64_t row = wave_global;
+#pragma unroll
+    for (int s = 0; s < D; ++s) load(s, row + static_cast<int64_t>(s / SPR) * nwaves);
+    for (; row < n; row += 2 * nwaves) {
+#pragma unroll
+        for (int s = 0; s < D; ++s) {
+            __builtin_amdgcn_sched_barrier(0);  // keep the sets' work apart (see the distance kernel)
+            consume(s);
+            load(s, row + static_cast<int64_t>(s / SPR + 2) * nwaves);
+        }
     }
+    __builtin_amdgcn_sched_barrier(0);
 }
 
 template <knn_dtype DT>
@@ -519,7 +559,9 @@ hipError_t launch_key_sqnorms(const void *keys, int64_t n, int64_t d, knn_dtype 
     if (n == 0) return hipSuccess;
     const int64_t waves_needed = n;
     int64_t blocks = (waves_needed + kWavesPerDistBlock - 1) / kWavesPerDistBlock;
-    if (blocks > 65536) blocks = 65536;
+    // the vector kernel: enough rows per wave for its pipeline (at most 1024 workgroups, four per CU)
+    const int64_t max_blocks = vector_path_ok(d, dtype, keys, keys) ? 1024 : 65536;
+    if (blocks > max_blocks) blocks = max_blocks;
     const dim3 grid(static_cast<unsigned>(blocks));
     const bool vec = vector_path_ok(d, dtype, keys, keys);
     const int cpl = vec ? pow2_at_least((d / vec_elems(dtype) + kWave - 1) / kWave) : 0;
