@@ -488,10 +488,13 @@ bool mfma_shape(int64_t d, knn_dtype dtype, int64_t max_queries) {
            max_queries >= kMfmaMinQueries;
 }
 
-// Key rows per distance workgroup.  Streaming path: about 1 MiB of keys, fewer
-// when the launch would otherwise have under 512 workgroups (two per CU,
-// measured best).  Matrix-core path: whole 128-key passes, enough of them for
-// a deep pipeline.  A multiple of 8 rows.
+// Key rows per distance workgroup.  Streaming path: about 1 MiB of keys,
+// fewer (down to 16 rows) when the launch would otherwise have under 2048
+// workgroups: with more workgroups than fit at once, each XCD's dispatcher
+// hands the later ones to the CUs that finish first, which evens out the
+// tail (measured at 64Ki x 4096 bf16: 77 us at 2048 workgroups against
+// 80.5 us at 512).  Matrix-core path: whole passes, enough of them for a deep
+// pipeline.  A multiple of 8 rows.
 // Depends on sizes only, so the workspace size does not depend on pointers.
 int dist_tile_rows(int64_t d, knn_dtype dtype, int64_t S, int64_t max_keys, int64_t max_queries) {
     if (mfma_shape(d, dtype, max_queries)) return mfma_tile_rows(d);
@@ -501,7 +504,7 @@ int dist_tile_rows(int64_t d, knn_dtype dtype, int64_t S, int64_t max_keys, int6
     if (rpt > 4096) rpt = 4096;
     rpt = (rpt + step - 1) / step * step;
     if (rpt < step) rpt = step;
-    while (rpt > step && S * ((max_keys + rpt - 1) / rpt) < 512) rpt = (rpt / 2 + step - 1) / step * step;
+    while (rpt > 2 * step && S * ((max_keys + rpt - 1) / rpt) < 2048) rpt = (rpt / 2 + step - 1) / step * step;
     return static_cast<int>(rpt);
 }
 

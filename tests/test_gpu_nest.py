@@ -83,10 +83,12 @@ def _check_decisions(out, vals, ko, qo, draft=None):
 
 
 # (path, n keys per set, queries, r, d): the split select needs B * ceil(n / 4096)
-# <= 256, the one-workgroup select n <= 65536 and r <= 1024, the general one the
-# rest; 16 or more bf16 queries of a set with d % 128 == 0 take the matrix cores.
+# <= 256, the one-workgroup select n <= 65536 and r <= 1024, the wide one rows of
+# more than 65536 keys in at least 2 r distance tiles with r <= 2048, the general
+# one the rest; 16 or more bf16 queries of a set with d % 128 == 0 take the matrix cores.
 PATHS = [("split", 40000, 6, 1024, 4), ("one-workgroup", 40000, 40, 1024, 4),
-         ("general-long-row", 70000, 6, 1024, 4), ("general-r2048", 40000, 3, 2048, 4),
+         ("wide-long-row", 70000, 6, 1024, 4), ("general-long-row", 70000, 6, 2500, 4),
+         ("general-r2048", 40000, 3, 2048, 4),
          ("matrix-core", 20000, 32, 1024, 128)]
 
 

@@ -2,7 +2,8 @@
 knn_lm_mixture_rrc and knn_mix_rrc against the oracle's rrc_lambda and its
 mixture with one lambda per query, through every select path (split over
 workgroups for few queries, one workgroup per query for rows of at most 64K
-keys, and the general path for longer rows or r > 1024)."""
+keys, the wide path for longer rows in fine tiles, and the general path for
+the rest: longer rows with r > 2048, or r > 1024)."""
 import math
 
 import numpy as np
@@ -50,9 +51,11 @@ def _integer_case(n, B, seed):
 
 
 # (path, n keys, queries, r): the split select needs B * ceil(n / 4096) <= 256,
-# the one-workgroup select n <= 65536 and r <= 1024, the general one the rest.
-PATHS = [("split", 40000, 6, 1024), ("one-workgroup", 40000, 40, 1024), ("general-long-row", 70000, 6, 1024),
-         ("general-r2048", 40000, 3, 2048), ("split-r1", 5000, 4, 1)]
+# the one-workgroup select n <= 65536 and r <= 1024, the wide one rows of more
+# than 65536 keys in at least 2 r distance tiles with r <= 2048 (16-row tiles
+# here), the general one the rest.
+PATHS = [("split", 40000, 6, 1024), ("one-workgroup", 40000, 40, 1024), ("wide-long-row", 70000, 6, 1024),
+         ("general-long-row", 70000, 6, 2500), ("general-r2048", 40000, 3, 2048), ("split-r1", 5000, 4, 1)]
 
 
 @pytest.mark.parametrize("path,n,B,r", PATHS, ids=[p[0] for p in PATHS])
