@@ -22,7 +22,7 @@ struct Layout {
     int64_t tiles_per_set;
     int64_t ld;  // distance row stride = tiles_per_set * rows_per_tile
     int split_parts;  // > 0: the select runs split over parts, short rows or long (candidate lists and counts below)
-    size_t off_dist, off_tmin, off_tmax, off_cand, off_count, off_thr, total;
+    size_t off_dist, off_tmin, off_tmax, off_cand, off_count, off_thr, off_best, off_ticket, total;
 };
 
 Layout layout(int64_t B, int64_t d, int64_t S, int64_t max_keys, int64_t max_queries, knn_dtype dtype, int32_t r) {
@@ -40,7 +40,10 @@ Layout layout(int64_t B, int64_t d, int64_t S, int64_t max_keys, int64_t max_que
     const size_t np = static_cast<size_t>(L.split_parts) * static_cast<size_t>(B);  // 0 unless split or wide
     L.off_count = align_up(L.off_cand + sizeof(uint64_t) * kSplitKeys * np);
     L.off_thr = align_up(L.off_count + 2 * sizeof(uint32_t) * np);  // counts, then minima
-    L.total = align_up(L.off_thr + (L.split_parts > 0 ? sizeof(uint32_t) * static_cast<size_t>(B) : 0));
+    const size_t per_row = L.split_parts > 0 ? static_cast<size_t>(B) : 0;  // split or wide: thresholds, NEST words
+    L.off_best = align_up(L.off_thr + sizeof(uint32_t) * per_row);
+    L.off_ticket = align_up(L.off_best + sizeof(uint64_t) * per_row);
+    L.total = align_up(L.off_ticket + sizeof(uint32_t) * per_row);
     return L;
 }
 
@@ -212,7 +215,12 @@ knn_status run_part(const Call &c, int part, hipStream_t stream) {
         a.part_min = part_count ? part_count + L.split_parts * c.B : nullptr;
         a.part_thr = part_thr;
         if (part == KNN_PART_SELECT) return status_of(launch_select(a, c.B, stream));
-        return status_of(launch_select_mix(a, mix_args(c), c.B, stream));
+        MixArgs mx = mix_args(c);
+        if (ws && L.split_parts > 0) {
+            mx.best = reinterpret_cast<uint64_t *>(ws + L.off_best);
+            mx.ticket = reinterpret_cast<uint32_t *>(ws + L.off_ticket);
+        }
+        return status_of(launch_select_mix(a, mx, c.B, stream));
     }
     if (part == KNN_PART_MIX) return status_of(launch_mix(mix_args(c), c.B, stream));
     return KNN_ERR_INVALID_ARG;

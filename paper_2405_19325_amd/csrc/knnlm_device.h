@@ -132,6 +132,13 @@ __device__ __forceinline__ float wave_allmin(float v) {
     return fminf(fminf(r0, r1), fminf(r2, r3));
 }
 
+// A value every lane of the wave reads at the same address, read through the
+// scalar data cache (a read only): it is waited for on its own counter, so
+// that using it does not wait for the vector loads and stores in flight.
+__device__ __forceinline__ int32_t load_scalar_i32(const int32_t *p) {
+    return *reinterpret_cast<const __attribute__((address_space(4))) int32_t *>(reinterpret_cast<uintptr_t>(p));
+}
+
 __device__ __forceinline__ float wave_allmax(float v) {
     v = fmaxf(v, dpp_f32<0xB1>(v));
     v = fmaxf(v, dpp_f32<0x4E>(v));

@@ -49,6 +49,11 @@ struct MixArgs {
     int32_t *span_key;           // [B] the nearest neighbour in pi whose value is next_token, or -1
     int32_t *use_span;           // [B] 1 if lambda_t <= delta and span_key >= 0
     float delta;
+    // Split select whose finish writes each row in slices (NEST outputs):
+    // [B] each, the row's largest entry key and its workgroup count, cleared
+    // by the parts kernel; or null.
+    uint64_t *best;
+    uint32_t *ticket;
 };
 
 hipError_t launch_spec_verify(const float *p_max, const float *p_draft, const int32_t *next_token,

@@ -58,6 +58,11 @@ constexpr int64_t kFastMaxN = static_cast<int64_t>(kT) * 4 * kFastU;  // 65536
 constexpr int kFastCap = 4096;                              // candidates the fast path keeps in LDS
 constexpr int kVocabTile = 8192;                            // mixture tile, general path
 constexpr int kVocabTileFast = 32768;                       // mixture tile, fast path (128 KiB)
+constexpr int kVocabSlice = 4 * kT;                         // p_M entries per workgroup, sliced split finish
+constexpr int64_t kSliceMaxBlocks = 256;                    // workgroups a sliced split finish may take
+
+// Target of the mixture's 16-byte stores from lanes past the end of a row.
+__device__ float4 g_mix_sink;
 
 // What a select launch does after pi: nothing, the mixture with one lambda,
 // the mixture with lambda_t from relative retrieval confidence, or that and
@@ -78,15 +83,16 @@ struct Shared {
 // The weight of p_LM for one query from its nearest (d_first) and r-th nearest
 // (d_last) distance: m.lambda, or with RRC (eq. rrc, |s| = the distance)
 // sigmoid((d_first / d_last - alpha) / tau), a row of zero distances having
-// ratio 1.  Thread 0 records it in m.lambda_out.
+// ratio 1.  Thread 0 records it in m.lambda_out (when `record`).
 template <int MODE>
-__device__ __forceinline__ float query_lambda(const MixArgs &m, int64_t b, float d_first, float d_last) {
+__device__ __forceinline__ float query_lambda(const MixArgs &m, int64_t b, float d_first, float d_last,
+                                              bool record = true) {
     if constexpr (!rrc_mode(MODE)) {
         return m.lambda;
     } else {
         const float ratio = d_last > 0.0f ? d_first / d_last : 1.0f;
         const float lam = 1.0f / (1.0f + expf(-(ratio - m.alpha) / m.tau));
-        if (threadIdx.x == 0 && m.lambda_out != nullptr) m.lambda_out[b] = lam;
+        if (record && threadIdx.x == 0 && m.lambda_out != nullptr) m.lambda_out[b] = lam;
         return lam;
     }
 }
@@ -483,17 +489,31 @@ __device__ __forceinline__ bool mix_vec4(const MixArgs &m, int64_t b) {
            ((reinterpret_cast<uintptr_t>(m.p_lm + b * m.V) | reinterpret_cast<uintptr_t>(m.p_m + b * m.V)) & 15u) == 0;
 }
 
-// This thread's float4s of the p_LM tile starting at v0 (16-byte path only).
+// This thread's float4s of the p_LM tile starting at v0 (16-byte path only):
+// unconditional loads, lanes past the row reading its last float4 (or, off the
+// 16-byte path, the sink), so that no branch sits around them; those lanes'
+// values are never used.
 template <int NV4>
 __device__ __forceinline__ void mix_prefetch(const MixArgs &m, int64_t b, int64_t v0, float4 (&pre)[NV4]) {
     const int64_t nv = (m.V - v0 < static_cast<int64_t>(NV4) * 4 * kT) ? m.V - v0 : static_cast<int64_t>(NV4) * 4 * kT;
-    const bool vec4 = mix_vec4(m, b);
-    const float4 *src = reinterpret_cast<const float4 *>(m.p_lm + b * m.V + v0);
+    const bool row = mix_vec4(m, b) && nv >= 4;
+    const float4 *src = row ? reinterpret_cast<const float4 *>(m.p_lm + b * m.V + v0) : &g_mix_sink;
+    const int64_t last = row ? nv / 4 - 1 : 0;  // the sink has one element
 #pragma unroll
     for (int q = 0; q < NV4; ++q) {
         const int64_t i = static_cast<int64_t>(q) * kT + threadIdx.x;
-        pre[q] = (vec4 && i < nv / 4) ? src[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+        pre[q] = src[i < last ? i : last];
     }
+}
+
+// Waits for the loads of a prefetch that a path does not use, so that no code
+// after that path and another one meet waits for the other path's stores.
+template <int NV4>
+__device__ __forceinline__ void consume_loads(const float4 (&pre)[NV4]) {
+    float t = 0.0f;
+#pragma unroll
+    for (int q = 0; q < NV4; ++q) t += (pre[q].x + pre[q].y) + (pre[q].z + pre[q].w);
+    asm volatile("" ::"v"(t));
 }
 
 // p_M row b with weight lam of p_LM: weights wj (unnormalised softmax terms, sum z) are scatter-added
@@ -508,22 +528,17 @@ __device__ __forceinline__ void block_argmax(float &v, uint32_t &i, uint32_t *re
     const float m = wave_allmax(v);
     const uint32_t j = wave_allmin_u32(v == m ? i : ~0u);
     const int wave = threadIdx.x / kWave;
-    if ((threadIdx.x & (kWave - 1)) == 0) {
+    const int lane = threadIdx.x & (kWave - 1);
+    if (lane == 0) {
         red[wave] = __float_as_uint(m);
         red[kNumWaves + wave] = j;
     }
     __syncthreads();
-    float bm = __uint_as_float(red[0]);
-    uint32_t bj = red[kNumWaves];
-#pragma unroll
-    for (int w = 1; w < kNumWaves; ++w) {
-        const float x = __uint_as_float(red[w]);
-        const uint32_t y = red[kNumWaves + w];
-        if (x > bm || (x == bm && y < bj)) {
-            bm = x;
-            bj = y;
-        }
-    }
+    // the waves' results, one a lane, reduced the same way again
+    const float x = lane < kNumWaves ? __uint_as_float(red[lane]) : -__builtin_huge_valf();
+    const uint32_t y = lane < kNumWaves ? red[kNumWaves + lane] : ~0u;
+    const float bm = wave_allmax(x);
+    const uint32_t bj = wave_allmin_u32(x == bm ? y : ~0u);
     __syncthreads();
     v = bm;
     i = bj;
@@ -583,8 +598,8 @@ __device__ __forceinline__ void note_entry(float v, int64_t w, int32_t dtok, uin
 
 // p_M row b with weight lam of p_LM: weights wj (unnormalised softmax terms, sum z) are scatter-added
 // onto their tokens tok (-1: none) one vocabulary tile of TILE entries at a
-// time in LDS; each tile's p_LM slice sits in registers (prefetched by the
-// caller for the first tile when `first` is given) and is mixed with 16-byte
+// time in LDS; each tile's p_LM slice sits in registers in pre (the first
+// tile's loaded by the caller when PREFETCHED) and is mixed with 16-byte
 // accesses.  With no neighbour (z = 0) p_kNN is 0.
 //
 // NEST: the decoding outputs of the row from the values just written (Algorithm
@@ -592,69 +607,107 @@ __device__ __forceinline__ void note_entry(float v, int64_t w, int32_t dtok, uin
 // value, p_M at the row's draft token, and the span start -- the nearest
 // neighbour carrying w_t, from nkey = (distance bits << 32 | key id) of each
 // neighbour (~0 for none) -- with the span flag lambda <= delta.
-template <int PER, int TILE, bool NEST = false>
+//
+// A workgroup writes entries [c0, c1) of the row (c1 < 0: to the end), c0 a
+// multiple of 4 kT.  When `slices` workgroups share the row, the one with
+// first_slice set writes what belongs to the row as a whole but not to an
+// entry, and the NEST outputs come from the last of them to finish, through
+// m.best[b] and m.ticket[b] (both zero before the first one starts).
+template <int PER, int TILE, bool NEST, bool PREFETCHED>
 __device__ __forceinline__ void mix_row(const float (&wj)[PER], const int32_t (&tok)[PER], const uint64_t (&nkey)[PER],
                                         float z, float lam, const MixArgs &m, int64_t b, float *acc,
-                                        const float4 (*first)[TILE / 4 / kT] = nullptr) {
+                                        float4 (&pre)[TILE / 4 / kT], int64_t c0 = 0, int64_t c1 = -1,
+                                        int slices = 1, bool first_slice = true) {
+    const int64_t end = c1 < 0 ? m.V : c1;  // this workgroup writes entries [c0, end)
     constexpr int kV4 = TILE / 4 / kT;  // float4 per thread per tile
     const int tid = threadIdx.x;
     const float scale = z > 0.0f ? (1.0f - lam) / z : 0.0f;
     const float *plm = m.p_lm + b * m.V;
     float *pm = m.p_m + b * m.V;
     const bool vec4 = mix_vec4(m, b);
-    const int32_t dtok = (NEST && m.draft != nullptr) ? m.draft[b] : -1;
+    const int32_t dtok = (NEST && m.draft != nullptr) ? load_scalar_i32(m.draft + b) : -1;
     float bv = -1.0f;  // this thread's largest entry and its token
     int32_t bw = 0;
     float pd = 0.0f;   // p_M(dtok), held by the thread that writes it
-    for (int64_t v0 = 0; v0 < m.V; v0 += TILE) {
-        const int64_t nv = (m.V - v0 < TILE) ? m.V - v0 : TILE;
-        float4 pre[kV4];
-        if (v0 == 0 && first != nullptr) {
+    if constexpr (!PREFETCHED) mix_prefetch(m, b, c0, pre);
+    int64_t v0 = c0;
+    do {  // at least once, so that pre is used on every path
+        const int64_t nv = (end - v0 < TILE) ? end - v0 : TILE;
+        const bool more = v0 + TILE < end;
+        if (v0 != c0) mix_prefetch(m, b, v0, pre);
 #pragma unroll
-            for (int q = 0; q < kV4; ++q) pre[q] = (*first)[q];
-        } else {
-            mix_prefetch(m, b, v0, pre);
-        }
-        for (int i = tid; i < TILE / 4; i += kT) reinterpret_cast<float4 *>(acc)[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int q = 0; q < kV4; ++q) reinterpret_cast<float4 *>(acc)[q * kT + tid] = make_float4(0.f, 0.f, 0.f, 0.f);
         __syncthreads();
 #pragma unroll
         for (int q = 0; q < PER; ++q)
             if (tok[q] >= v0 && tok[q] < v0 + nv) atomicAdd(&acc[tok[q] - v0], wj[q]);
         __syncthreads();
         if (vec4) {
+            // Stores with no branch around them (lanes past the row store to a
+            // sink), so that no store waits for the one before it.
             float4 *dst = reinterpret_cast<float4 *>(pm + v0);
 #pragma unroll
             for (int q = 0; q < kV4; ++q) {
                 const int64_t i = static_cast<int64_t>(q) * kT + tid;
-                if (i < nv / 4) {
-                    const float4 a4 = reinterpret_cast<const float4 *>(acc)[i];
-                    float4 o;
-                    o.x = fmaf(lam, pre[q].x, a4.x * scale);
-                    o.y = fmaf(lam, pre[q].y, a4.y * scale);
-                    o.z = fmaf(lam, pre[q].z, a4.z * scale);
-                    o.w = fmaf(lam, pre[q].w, a4.w * scale);
-                    dst[i] = o;
+                const bool in = i < nv / 4;
+                const float4 a4 = reinterpret_cast<const float4 *>(acc)[i];
+                float4 o;
+                o.x = fmaf(lam, pre[q].x, a4.x * scale);
+                o.y = fmaf(lam, pre[q].y, a4.y * scale);
+                o.z = fmaf(lam, pre[q].z, a4.z * scale);
+                o.w = fmaf(lam, pre[q].w, a4.w * scale);
+                *(in ? dst + i : &g_mix_sink) = o;
+                if constexpr (NEST) {
                     const int32_t w = static_cast<int32_t>(v0 + 4 * i);
-                    note_entry<NEST>(o.x, w, dtok, bv, bw, pd);
-                    note_entry<NEST>(o.y, w + 1, dtok, bv, bw, pd);
-                    note_entry<NEST>(o.z, w + 2, dtok, bv, bw, pd);
-                    note_entry<NEST>(o.w, w + 3, dtok, bv, bw, pd);
+                    note_entry<NEST>(in ? o.x : -1.0f, w, dtok, bv, bw, pd);
+                    note_entry<NEST>(in ? o.y : -1.0f, w + 1, dtok, bv, bw, pd);
+                    note_entry<NEST>(in ? o.z : -1.0f, w + 2, dtok, bv, bw, pd);
+                    note_entry<NEST>(in ? o.w : -1.0f, w + 3, dtok, bv, bw, pd);
                 }
             }
         } else {
+            consume_loads(pre);  // unused on this path
             for (int64_t i = tid; i < nv; i += kT) {
                 const float o = fmaf(lam, plm[v0 + i], acc[i] * scale);
                 pm[v0 + i] = o;
                 note_entry<NEST>(o, static_cast<int32_t>(v0 + i), dtok, bv, bw, pd);
             }
         }
-        __syncthreads();
-    }
+        if (more) __syncthreads();  // acc is cleared again next
+        v0 += TILE;
+    } while (v0 < end);
     if constexpr (NEST) {
-        uint32_t *red = reinterpret_cast<uint32_t *>(acc);  // free after the last tile
+        __shared__ uint32_t red[2 * kNumWaves];
+        __shared__ uint64_t row_best;  // sliced rows: the row's largest entry key, seen by the last workgroup
+        __shared__ uint32_t is_last;
         float top = bv;
         uint32_t wtu = static_cast<uint32_t>(bw);
         block_argmax(top, wtu, red);
+        if (m.p_draft != nullptr) {
+            // entry w was written by thread (w / 4) % kT on the 16-byte path, w % kT otherwise
+            const bool valid = dtok >= 0 && dtok < m.V;
+            const bool mine = valid && dtok >= c0 && dtok < end &&
+                              (vec4 ? ((dtok / 4) % kT == tid) : (dtok % kT == tid));
+            if (mine) m.p_draft[b] = pd;
+            if (tid == 0 && first_slice && !valid) m.p_draft[b] = 0.0f;
+        }
+        if (slices > 1) {
+            // The row's workgroups each add their largest entry to the row's
+            // 64-bit maximum (largest value, then lowest token; 0 for none) and
+            // count themselves; the last one to count goes on with the row's.
+            if (tid == 0) {
+                atomicMax(reinterpret_cast<unsigned long long *>(m.best + b),
+                          static_cast<unsigned long long>(top >= 0.0f ? best_key(top, wtu) : 0ull));
+                const uint32_t t = __hip_atomic_fetch_add(m.ticket + b, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+                is_last = t == static_cast<uint32_t>(slices - 1) ? 1u : 0u;
+                row_best = is_last ? __hip_atomic_load(m.best + b, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0ull;
+            }
+            __syncthreads();
+            if (is_last == 0u) return;
+            const uint64_t k = row_best;
+            top = k == 0ull ? -1.0f : __uint_as_float(static_cast<uint32_t>(k >> 32));
+            wtu = k == 0ull ? 0u : 0xffffffffu - static_cast<uint32_t>(k);
+        }
         const int32_t wt = static_cast<int32_t>(wtu);
         // the nearest neighbour carrying wt: smallest (distance bits, id)
         uint32_t nd = ~0u, ni = ~0u;
@@ -670,13 +723,6 @@ __device__ __forceinline__ void mix_row(const float (&wj)[PER], const int32_t (&
         float nearness = nd == ~0u ? -1.0f : __uint_as_float(kMaskedBits - nd);
         block_argmax(nearness, ni, red);
         const uint64_t near = nearness < 0.0f ? ~0ull : static_cast<uint64_t>(ni);
-        if (m.p_draft != nullptr) {
-            // entry w was written by thread (w / 4) % kT on the 16-byte path, w % kT otherwise
-            const bool mine = dtok >= 0 && dtok < m.V &&
-                              (vec4 ? ((dtok / 4) % kT == tid) : (dtok % kT == tid));
-            if (mine) m.p_draft[b] = pd;
-            if (tid == 0 && !(dtok >= 0 && dtok < m.V)) m.p_draft[b] = 0.0f;
-        }
         if (tid == 0) {
             const int32_t span = near == ~0ull ? -1 : static_cast<int32_t>(static_cast<uint32_t>(near));
             m.next_token[b] = wt;
@@ -745,7 +791,8 @@ __global__ __launch_bounds__(kT) void k_select(SelectArgs a, MixArgs m) {
             }
         }
         const float z = block_sum(zpart, sh.red_f);
-        mix_row<kPer, kVocabTile, MODE == kMixNest>(wj, tok, nkey, z, lam, m, b, acc);
+        float4 pre[kVocabTile / 4 / kT];
+        mix_row<kPer, kVocabTile, MODE == kMixNest, false>(wj, tok, nkey, z, lam, m, b, acc, pre);
     }
 }
 
@@ -873,7 +920,7 @@ __global__ __launch_bounds__(kT) void k_select_fast(SelectArgs a, MixArgs m) {
         const float lam = query_lambda<MODE>(m, b, sh.dmin, sh.dlast);
         float wj[1] = {ok ? expf(-m.mu * (dj - sh.dmin)) : 0.0f};
         const float z = block_sum(wj[0], sh.red_f);
-        mix_row<1, kVocabTileFast, MODE == kMixNest>(wj, tok, nkey, z, lam, m, b, acc, &pre);
+        mix_row<1, kVocabTileFast, MODE == kMixNest, true>(wj, tok, nkey, z, lam, m, b, acc, pre);
     }
 }
 
@@ -888,16 +935,18 @@ __global__ __launch_bounds__(kT) void k_select_fast(SelectArgs a, MixArgs m) {
 // samples' own range, that holds the ks-th smallest of them, ks aiming at
 // about r + 4 sd + 4 samples' worth of keys; it writes its keys below the
 // threshold to its own list (distance bits << 32 | key index << 12) and their
-// count, and part 0 records the threshold.  With mixing, each part also
-// writes its slice of the dense term of p_M: lambda * p_LM is what
-// fmaf(lambda, p_LM, acc * scale) gives wherever no neighbour carries the
-// token.  The part's keys and samples are requested before the row length is
+// count, and part 0 records the threshold.  With a fixed lambda and a finish
+// that writes only the neighbours' entries, each part also writes its slice of
+// the dense term of p_M: lambda * p_LM is what fmaf(lambda, p_LM, acc * scale)
+// gives wherever no neighbour carries the token.  The part's keys and samples are requested before the row length is
 // known (as if the row filled the stride) and corrected after.
 constexpr int kSplitSamples = 4 * kT;
 
-template <int MODE>
+template <int MODE, bool DENSE_TERM>
 __global__ __launch_bounds__(kT) void k_select_parts(SelectArgs a, MixArgs m, int parts) {
-    constexpr bool DENSE = MODE == kMixFixed;  // the dense term lambda * p_LM is known here
+    // the dense term lambda * p_LM is known here; written here unless the
+    // finish writes whole slices of the row
+    constexpr bool DENSE = MODE == kMixFixed && DENSE_TERM;
     __shared__ __align__(16) uint32_t hist[kSelectBins];
     __shared__ Shared sh;
     const int tid = threadIdx.x;
@@ -1022,6 +1071,10 @@ __global__ __launch_bounds__(kT) void k_select_parts(SelectArgs a, MixArgs m, in
         a.part_count[bp] = sh.ccount;
         a.part_min[bp] = sh.cmin;
         if (part == 0) a.part_thr[b] = thr;
+        if (MODE == kMixNest && part == 0 && m.best != nullptr) {  // the sliced finish's row maximum and count
+            m.best[b] = 0ull;
+            m.ticket[b] = 0u;
+        }
     }
 }
 
@@ -1045,9 +1098,10 @@ __device__ __forceinline__ void finish_sort(uint64_t *cand, uint32_t total, uint
                                              NoHook(), keep);
 }
 
-template <int MODE>
-__global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, int parts) {
+template <int MODE, bool SLICED>
+__global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, int parts, int slices) {
     constexpr bool MIX = MODE != kNoMix;
+    static_assert(!SLICED || MIX, "slices are of the p_M row");
     constexpr int PER = kSplitCap / kT;
     constexpr int kSortBytes = 2 * kSplitCap * 8 + (8 << kFinishBinsLog2);
     constexpr int kSmem = MIX ? kSortBytes + kSplitCap * 4 + 16384 : kSortBytes;  // + tokens, + room for the tile
@@ -1063,7 +1117,8 @@ __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, i
 
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
-    const int64_t b = blockIdx.x;
+    const int64_t b = SLICED ? blockIdx.x / slices : blockIdx.x;
+    const int g = SLICED ? static_cast<int>(blockIdx.x - b * slices) : 0;  // the row's slice
     const uint64_t *lists = a.cand + b * parts * kSplitKeys;
 
     // Counts, threshold and the first `win` entries of every list, all in flight together.
@@ -1078,6 +1133,10 @@ __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, i
         const uint32_t p = e / win;
         key[q] = p < static_cast<uint32_t>(parts) ? lists[p * kSplitKeys + (e - p * win)] : ~0ull;
     }
+    // The p_LM entries this workgroup mixes: its slice, or the row's first tile
+    // (loaded during the write-out below).
+    float4 pre[SLICED ? kVocabSlice / 4 / kT : kVocabTileFast / 4 / kT];
+    if constexpr (SLICED) mix_prefetch(m, b, static_cast<int64_t>(g) * kVocabSlice, pre);
     const int64_t s = set_of_query(a.query_offsets, a.S, b);
     const int64_t k0 = a.key_offsets[s];
     int64_t N = a.key_offsets[s + 1] - k0;
@@ -1166,13 +1225,12 @@ __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, i
         if (MIX && ok) tok = m.values[k0 + id];
     }
     if (tok < 0 || tok >= m.V) tok = -1;  // tokens outside [0, V) carry no mass
-    if (MODE == kMixFixed && tok >= 0) plm_t = plm_row[tok];  // needed only at the end
+    if (MODE == kMixFixed && !SLICED && tok >= 0) plm_t = plm_row[tok];  // needed only at the end
     // the nearest and (RRC) the r-th nearest distance: the ends of pi, in LDS in both branches above
     const float d0 = nvalid > 0 ? __uint_as_float(static_cast<uint32_t>(cand[0] >> 32)) : 0.0f;
     const float dlast = nvalid > 0 ? __uint_as_float(static_cast<uint32_t>(cand[nvalid - 1] >> 32)) : 0.0f;
-    float4 pre[kVocabTileFast / 4 / kT];
-    if constexpr (rrc_mode(MODE)) mix_prefetch(m, b, 0, pre);  // the first p_LM tile, during the write-out
-    if (tid < a.r) {
+    if constexpr (rrc_mode(MODE) && !SLICED) mix_prefetch(m, b, 0, pre);  // during the write-out
+    if (g == 0 && tid < a.r) {
         a.ids[b * a.r + tid] = ok ? static_cast<int32_t>(id) : -1;
         a.dists[b * a.r + tid] = ok ? __uint_as_float(static_cast<uint32_t>(x >> 32)) : __builtin_huge_valf();
     }
@@ -1187,13 +1245,19 @@ __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, i
         float z = 0.0f;
 #pragma unroll
         for (int w = 0; w < kNumWaves; ++w) z += sh.red_f[w];
-        const float lam = query_lambda<MODE>(m, b, d0, dlast);
-        if constexpr (rrc_mode(MODE)) {
+        const float lam = query_lambda<MODE>(m, b, d0, dlast, g == 0);
+        const float w1[1] = {wj};
+        const int32_t t1[1] = {tok};
+        const uint64_t k1[1] = {ok ? ((x >> 32) << 32) | id : ~0ull};
+        if constexpr (SLICED) {
+            // this workgroup's slice of the row, with any lambda
+            const int64_t c0 = static_cast<int64_t>(g) * kVocabSlice;
+            const int64_t c1 = m.V - c0 < kVocabSlice ? m.V : c0 + kVocabSlice;
+            mix_row<1, kVocabSlice, MODE == kMixNest, true>(w1, t1, k1, z, lam, m, b, acc, pre, c0, c1, slices, g == 0);
+            return;
+        } else if constexpr (rrc_mode(MODE)) {
             // lambda_t is known only now: the whole row, tile by tile
-            const float w1[1] = {wj};
-            const int32_t t1[1] = {tok};
-            const uint64_t k1[1] = {ok ? ((x >> 32) << 32) | id : ~0ull};
-            mix_row<1, kVocabTileFast, MODE == kMixNest>(w1, t1, k1, z, lam, m, b, acc, &pre);
+            mix_row<1, kVocabTileFast, MODE == kMixNest, true>(w1, t1, k1, z, lam, m, b, acc, pre);
             return;
         }
         const float scale = z > 0.0f ? (1.0f - lam) / z : 0.0f;
@@ -1258,7 +1322,8 @@ __global__ __launch_bounds__(kT) void k_mix(MixArgs m) {
                              : ~0ull;
     }
     const float z = block_sum(zpart, red_f);
-    mix_row<kPer, kVocabTile, MODE == kMixNest>(wj, tok, nkey, z, lam, m, b, acc);
+    float4 pre[kVocabTile / 4 / kT];
+    mix_row<kPer, kVocabTile, MODE == kMixNest, false>(wj, tok, nkey, z, lam, m, b, acc, pre);
 }
 
 // Wide path: rows longer than the split path's (ld > kSplitMaxN), r <= kWideMaxR,
@@ -1500,7 +1565,8 @@ __global__ __launch_bounds__(kT) void k_select_wide_finish(SelectArgs a, MixArgs
             }
         }
         const float z = block_sum(zpart, sh.red_f);  // its barrier also ends the sort scratch's use
-        mix_row<kPer, kVocabTile, MODE == kMixNest>(wj, tok, nkey, z, lam, m, b, acc);
+        float4 pre[kVocabTile / 4 / kT];
+        mix_row<kPer, kVocabTile, MODE == kMixNest, false>(wj, tok, nkey, z, lam, m, b, acc, pre);
     }
 }
 
@@ -1513,10 +1579,30 @@ hipError_t launch_sel(const SelectArgs &a, const MixArgs &m, int64_t B, hipStrea
     const int parts = select_split_parts(B, a.ld, a.r);
     if (parts > 0) {
         if (a.cand == nullptr || a.part_count == nullptr || a.part_thr == nullptr) return hipErrorInvalidValue;
-        hipLaunchKernelGGL((k_select_parts<MODE>), dim3(static_cast<unsigned>(B * parts)), block, 0, st, a, m, parts);
+        // With mixing and few rows, the finish runs once per vocabulary slice
+        // of each row, every one of those workgroups selecting pi again, so
+        // that the row is written by many CUs.
+        constexpr bool MIX = MODE != kNoMix;
+        const int64_t slices = MIX ? (m.V + kVocabSlice - 1) / kVocabSlice : 1;
+        const bool sliced = MIX && B * slices <= kSliceMaxBlocks &&
+                            (MODE != kMixNest || (m.best != nullptr && m.ticket != nullptr));
+        if (sliced) {
+            hipLaunchKernelGGL((k_select_parts<MODE, false>), dim3(static_cast<unsigned>(B * parts)), block, 0, st, a,
+                               m, parts);
+        } else {
+            hipLaunchKernelGGL((k_select_parts<MODE, true>), dim3(static_cast<unsigned>(B * parts)), block, 0, st, a,
+                               m, parts);
+        }
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
-        hipLaunchKernelGGL((k_select_finish<MODE>), grid, block, 0, st, a, m, parts);
+        if constexpr (MIX) {
+            if (sliced) {
+                hipLaunchKernelGGL((k_select_finish<MODE, true>), dim3(static_cast<unsigned>(B * slices)), block, 0,
+                                   st, a, m, parts, static_cast<int>(slices));
+                return hipGetLastError();
+            }
+        }
+        hipLaunchKernelGGL((k_select_finish<MODE, false>), grid, block, 0, st, a, m, parts, 1);
         return hipGetLastError();
     }
     const int wparts = select_wide_parts(B, a.ld, a.r, a.tiles_per_set);

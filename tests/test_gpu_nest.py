@@ -145,6 +145,55 @@ def test_fewer_unmasked_keys_than_r(path, B, r):
     _check_decisions(out, vals, ko, qo)
 
 
+@pytest.mark.parametrize("V", [10001, 12288])
+def test_rows_written_in_vocabulary_slices(V):
+    """The split select's finish writes each row in slices of 4096 entries, one
+    workgroup each (here 3), and combines the NEST outputs across them: the
+    greedy token lies in a different slice per query, drafts in the first and
+    last slice and outside [0, V).  V = 10001 takes the 4-byte mixture, 12288
+    the 16-byte one.  Two NEST steps in a row (the row maximum and count start
+    again from zero), the RRC step and the fixed-lambda step all match the
+    oracle."""
+    _say(f"rows in vocabulary slices: V={V}")
+    n, B, r, d = 20000, 3, 256, 4
+    rng = np.random.default_rng(V)
+    k = np.zeros((n, d), np.float32)
+    k[:, :3] = rng.integers(-6, 7, (n, 3))
+    q = np.zeros((B, d), np.float32)
+    q[:, 3] = np.arange(B)
+    vals = rng.integers(0, V, n).astype(np.int32)
+    p_lm = rng.dirichlet(np.ones(V), B).astype(np.float32)
+    for b, w in enumerate([V - 3, 4100, 17]):  # a p_LM peak in the last, middle and first slice
+        p_lm[b, w] += 2.0
+    p_lm /= p_lm.sum(1, keepdims=True)
+    ko, qo = np.array([0, n]), np.array([0, B])
+    prob = _problem(q, k, vals, p_lm, ko, qo, r, 0.05, torch.float32)
+    o_ids, o_d = oracle.select(q, k, "f32", ko, qo, r)
+    o_lam = oracle.rrc_lambda(o_d, ALPHA, TAU)
+    for drafts in ([V - 1, 0, -1], [4096, V, V - 4]):
+        draft = torch.as_tensor(np.array(drafts, np.int32), device="cuda")
+        for rep in range(2):
+            out = prob.run_nest(ALPHA, TAU, DELTA, draft_tokens=draft)
+            torch.cuda.synchronize()
+            np.testing.assert_array_equal(out["ids"].cpu().numpy(), o_ids)
+            np.testing.assert_array_equal(out["dists"].cpu().numpy().astype(np.float64), o_d)
+            np.testing.assert_allclose(out["lambdas"].cpu().numpy().astype(np.float64), o_lam, rtol=0, atol=1e-6)
+            ref = oracle.mix(o_ids, o_d, vals, ko, qo, p_lm, 0.05, o_lam)
+            np.testing.assert_allclose(out["p_m"].cpu().numpy(), ref, rtol=0, atol=1e-5)
+            want = _check_decisions(out, vals, ko, qo, draft)
+            assert sorted(set((want["next_token"] // 4096).tolist())) == [0, 1, 2], want["next_token"]
+    p_m, ids, dists, lam = prob.run_rrc(ALPHA, TAU)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(ids.cpu().numpy(), o_ids)
+    np.testing.assert_allclose(p_m.cpu().numpy(), oracle.mix(o_ids, o_d, vals, ko, qo, p_lm, 0.05, o_lam),
+                               rtol=0, atol=1e-5)
+    p_m, ids, dists = prob.run()
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(ids.cpu().numpy(), o_ids)
+    np.testing.assert_allclose(p_m.cpu().numpy(), oracle.mix(o_ids, o_d, vals, ko, qo, p_lm, 0.05, prob.lam),
+                               rtol=0, atol=1e-5)
+
+
 SYNTH = [
     ("decode-bf16-split", gen.scaled(gen.config("decode_7b"), n_keys=30000, B=2), 81),
     ("ragged-bf16", gen.scaled(gen.config("ragged_batch"), B=12, S=4, n_keys=(1100, 5000, 3333, 2048), r=1024), 82),
