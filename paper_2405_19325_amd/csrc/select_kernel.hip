@@ -489,6 +489,13 @@ __device__ __forceinline__ bool mix_vec4(const MixArgs &m, int64_t b) {
            ((reinterpret_cast<uintptr_t>(m.p_lm + b * m.V) | reinterpret_cast<uintptr_t>(m.p_m + b * m.V)) & 15u) == 0;
 }
 
+// The draft token row b checks (NEST; -1 for none), read at a kernel's start
+// through the scalar cache so that only its use waits for it.
+template <int MODE>
+__device__ __forceinline__ int32_t draft_token(const MixArgs &m, int64_t b) {
+    return (MODE == kMixNest && m.draft != nullptr) ? load_scalar_i32(m.draft + b) : -1;
+}
+
 // This thread's float4s of the p_LM tile starting at v0 (16-byte path only):
 // unconditional loads, lanes past the row reading its last float4 (or, off the
 // 16-byte path, the sink), so that no branch sits around them; those lanes'
@@ -608,16 +615,18 @@ __device__ __forceinline__ void note_entry(float v, int64_t w, int32_t dtok, uin
 // neighbour carrying w_t, from nkey = (distance bits << 32 | key id) of each
 // neighbour (~0 for none) -- with the span flag lambda <= delta.
 //
-// A workgroup writes entries [c0, c1) of the row (c1 < 0: to the end), c0 a
-// multiple of 4 kT.  When `slices` workgroups share the row, the one with
+// dtok is the draft token of the row (NEST; -1 for none), read by the caller
+// at its start.  A workgroup writes entries [c0, c1) of the row (c1 < 0: to
+// the end), c0 a multiple of 4 kT; ONE_TILE: they fit one tile, and pre holds
+// it.  When `slices` workgroups share the row, the one with
 // first_slice set writes what belongs to the row as a whole but not to an
 // entry, and the NEST outputs come from the last of them to finish, through
 // m.best[b] and m.ticket[b] (both zero before the first one starts).
-template <int PER, int TILE, bool NEST, bool PREFETCHED>
+template <int PER, int TILE, bool NEST, bool PREFETCHED, bool ONE_TILE = false>
 __device__ __forceinline__ void mix_row(const float (&wj)[PER], const int32_t (&tok)[PER], const uint64_t (&nkey)[PER],
                                         float z, float lam, const MixArgs &m, int64_t b, float *acc,
-                                        float4 (&pre)[TILE / 4 / kT], int64_t c0 = 0, int64_t c1 = -1,
-                                        int slices = 1, bool first_slice = true) {
+                                        float4 (&pre)[TILE / 4 / kT], int32_t dtok, int64_t c0 = 0,
+                                        int64_t c1 = -1, int slices = 1, bool first_slice = true) {
     const int64_t end = c1 < 0 ? m.V : c1;  // this workgroup writes entries [c0, end)
     constexpr int kV4 = TILE / 4 / kT;  // float4 per thread per tile
     const int tid = threadIdx.x;
@@ -625,7 +634,6 @@ __device__ __forceinline__ void mix_row(const float (&wj)[PER], const int32_t (&
     const float *plm = m.p_lm + b * m.V;
     float *pm = m.p_m + b * m.V;
     const bool vec4 = mix_vec4(m, b);
-    const int32_t dtok = (NEST && m.draft != nullptr) ? load_scalar_i32(m.draft + b) : -1;
     float bv = -1.0f;  // this thread's largest entry and its token
     int32_t bw = 0;
     float pd = 0.0f;   // p_M(dtok), held by the thread that writes it
@@ -634,7 +642,7 @@ __device__ __forceinline__ void mix_row(const float (&wj)[PER], const int32_t (&
     do {  // at least once, so that pre is used on every path
         const int64_t nv = (end - v0 < TILE) ? end - v0 : TILE;
         const bool more = v0 + TILE < end;
-        if (v0 != c0) mix_prefetch(m, b, v0, pre);
+        if (!ONE_TILE && v0 != c0) mix_prefetch(m, b, v0, pre);
 #pragma unroll
         for (int q = 0; q < kV4; ++q) reinterpret_cast<float4 *>(acc)[q * kT + tid] = make_float4(0.f, 0.f, 0.f, 0.f);
         __syncthreads();
@@ -673,9 +681,9 @@ __device__ __forceinline__ void mix_row(const float (&wj)[PER], const int32_t (&
                 note_entry<NEST>(o, static_cast<int32_t>(v0 + i), dtok, bv, bw, pd);
             }
         }
-        if (more) __syncthreads();  // acc is cleared again next
+        if (!ONE_TILE && more) __syncthreads();  // acc is cleared again next
         v0 += TILE;
-    } while (v0 < end);
+    } while (!ONE_TILE && v0 < end);
     if constexpr (NEST) {
         __shared__ uint32_t red[2 * kNumWaves];
         __shared__ uint64_t row_best;  // sliced rows: the row's largest entry key, seen by the last workgroup
@@ -746,6 +754,7 @@ __global__ __launch_bounds__(kT) void k_select(SelectArgs a, MixArgs m) {
 
     const int tid = threadIdx.x;
     const int64_t b = blockIdx.x;
+    const int32_t dtok = draft_token<MODE>(m, b);
     const int64_t s = set_of_query(a.query_offsets, a.S, b);
     const int64_t k0 = a.key_offsets[s];
     int64_t N = a.key_offsets[s + 1] - k0;
@@ -792,7 +801,7 @@ __global__ __launch_bounds__(kT) void k_select(SelectArgs a, MixArgs m) {
         }
         const float z = block_sum(zpart, sh.red_f);
         float4 pre[kVocabTile / 4 / kT];
-        mix_row<kPer, kVocabTile, MODE == kMixNest, false>(wj, tok, nkey, z, lam, m, b, acc, pre);
+        mix_row<kPer, kVocabTile, MODE == kMixNest, false>(wj, tok, nkey, z, lam, m, b, acc, pre, dtok);
     }
 }
 
@@ -812,6 +821,7 @@ __global__ __launch_bounds__(kT) void k_select_fast(SelectArgs a, MixArgs m) {
 
     const int tid = threadIdx.x;
     const int64_t b = blockIdx.x;
+    const int32_t dtok = draft_token<MODE>(m, b);
     const int64_t s = set_of_query(a.query_offsets, a.S, b);
     const int64_t k0 = a.key_offsets[s];
     int64_t N = a.key_offsets[s + 1] - k0;
@@ -920,7 +930,7 @@ __global__ __launch_bounds__(kT) void k_select_fast(SelectArgs a, MixArgs m) {
         const float lam = query_lambda<MODE>(m, b, sh.dmin, sh.dlast);
         float wj[1] = {ok ? expf(-m.mu * (dj - sh.dmin)) : 0.0f};
         const float z = block_sum(wj[0], sh.red_f);
-        mix_row<1, kVocabTileFast, MODE == kMixNest, true>(wj, tok, nkey, z, lam, m, b, acc, pre);
+        mix_row<1, kVocabTileFast, MODE == kMixNest, true>(wj, tok, nkey, z, lam, m, b, acc, pre, dtok);
     }
 }
 
@@ -1119,6 +1129,7 @@ __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, i
     const int lane = tid & (kWave - 1);
     const int64_t b = SLICED ? blockIdx.x / slices : blockIdx.x;
     const int g = SLICED ? static_cast<int>(blockIdx.x - b * slices) : 0;  // the row's slice
+    const int32_t dtok = draft_token<MODE>(m, b);
     const uint64_t *lists = a.cand + b * parts * kSplitKeys;
 
     // Counts, threshold and the first `win` entries of every list, all in flight together.
@@ -1253,11 +1264,12 @@ __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, i
             // this workgroup's slice of the row, with any lambda
             const int64_t c0 = static_cast<int64_t>(g) * kVocabSlice;
             const int64_t c1 = m.V - c0 < kVocabSlice ? m.V : c0 + kVocabSlice;
-            mix_row<1, kVocabSlice, MODE == kMixNest, true>(w1, t1, k1, z, lam, m, b, acc, pre, c0, c1, slices, g == 0);
+            mix_row<1, kVocabSlice, MODE == kMixNest, true, true>(w1, t1, k1, z, lam, m, b, acc, pre, dtok, c0, c1,
+                                                                  slices, g == 0);
             return;
         } else if constexpr (rrc_mode(MODE)) {
             // lambda_t is known only now: the whole row, tile by tile
-            mix_row<1, kVocabTileFast, MODE == kMixNest, true>(w1, t1, k1, z, lam, m, b, acc, pre);
+            mix_row<1, kVocabTileFast, MODE == kMixNest, true>(w1, t1, k1, z, lam, m, b, acc, pre, dtok);
             return;
         }
         const float scale = z > 0.0f ? (1.0f - lam) / z : 0.0f;
@@ -1284,6 +1296,7 @@ __global__ __launch_bounds__(kT) void k_mix(MixArgs m) {
     __shared__ float red_f[kNumWaves];
     const int tid = threadIdx.x;
     const int64_t b = blockIdx.x;
+    const int32_t dtok = draft_token<MODE>(m, b);
     const int64_t s = set_of_query(m.query_offsets, m.S, b);
     const int64_t k0 = m.key_offsets[s];
     const int64_t N = m.key_offsets[s + 1] - k0;
@@ -1323,7 +1336,7 @@ __global__ __launch_bounds__(kT) void k_mix(MixArgs m) {
     }
     const float z = block_sum(zpart, red_f);
     float4 pre[kVocabTile / 4 / kT];
-    mix_row<kPer, kVocabTile, MODE == kMixNest, false>(wj, tok, nkey, z, lam, m, b, acc, pre);
+    mix_row<kPer, kVocabTile, MODE == kMixNest, false>(wj, tok, nkey, z, lam, m, b, acc, pre, dtok);
 }
 
 // Wide path: rows longer than the split path's (ld > kSplitMaxN), r <= kWideMaxR,
@@ -1492,6 +1505,7 @@ __global__ __launch_bounds__(kT) void k_select_wide_finish(SelectArgs a, MixArgs
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
     const int64_t b = blockIdx.x;
+    const int32_t dtok = draft_token<MODE>(m, b);
     const int64_t s = set_of_query(a.query_offsets, a.S, b);
     const int64_t k0 = a.key_offsets[s];
     int64_t N = a.key_offsets[s + 1] - k0;
@@ -1566,7 +1580,7 @@ __global__ __launch_bounds__(kT) void k_select_wide_finish(SelectArgs a, MixArgs
         }
         const float z = block_sum(zpart, sh.red_f);  // its barrier also ends the sort scratch's use
         float4 pre[kVocabTile / 4 / kT];
-        mix_row<kPer, kVocabTile, MODE == kMixNest, false>(wj, tok, nkey, z, lam, m, b, acc, pre);
+        mix_row<kPer, kVocabTile, MODE == kMixNest, false>(wj, tok, nkey, z, lam, m, b, acc, pre, dtok);
     }
 }
 
