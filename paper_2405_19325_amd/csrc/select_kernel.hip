@@ -618,11 +618,12 @@ __device__ __forceinline__ void note_entry(float v, int64_t w, int32_t dtok, uin
 // dtok is the draft token of the row (NEST; -1 for none), read by the caller
 // at its start.  A workgroup writes entries [c0, c1) of the row (c1 < 0: to
 // the end), c0 a multiple of 4 kT; ONE_TILE: they fit one tile, and pre holds
-// it.  When `slices` workgroups share the row, the one with
+// it; SCATTERED (with ONE_TILE): the caller has already added the weights
+// into acc and ordered that with a barrier.  When `slices` workgroups share the row, the one with
 // first_slice set writes what belongs to the row as a whole but not to an
 // entry, and the NEST outputs come from the last of them to finish, through
 // m.best[b] and m.ticket[b] (both zero before the first one starts).
-template <int PER, int TILE, bool NEST, bool PREFETCHED, bool ONE_TILE = false>
+template <int PER, int TILE, bool NEST, bool PREFETCHED, bool ONE_TILE = false, bool SCATTERED = false>
 __device__ __forceinline__ void mix_row(const float (&wj)[PER], const int32_t (&tok)[PER], const uint64_t (&nkey)[PER],
                                         float z, float lam, const MixArgs &m, int64_t b, float *acc,
                                         float4 (&pre)[TILE / 4 / kT], int32_t dtok, int64_t c0 = 0,
@@ -643,13 +644,15 @@ __device__ __forceinline__ void mix_row(const float (&wj)[PER], const int32_t (&
         const int64_t nv = (end - v0 < TILE) ? end - v0 : TILE;
         const bool more = v0 + TILE < end;
         if (!ONE_TILE && v0 != c0) mix_prefetch(m, b, v0, pre);
+        if constexpr (!SCATTERED) {
 #pragma unroll
-        for (int q = 0; q < kV4; ++q) reinterpret_cast<float4 *>(acc)[q * kT + tid] = make_float4(0.f, 0.f, 0.f, 0.f);
-        __syncthreads();
+            for (int q = 0; q < kV4; ++q) reinterpret_cast<float4 *>(acc)[q * kT + tid] = make_float4(0.f, 0.f, 0.f, 0.f);
+            __syncthreads();
 #pragma unroll
-        for (int q = 0; q < PER; ++q)
-            if (tok[q] >= v0 && tok[q] < v0 + nv) atomicAdd(&acc[tok[q] - v0], wj[q]);
-        __syncthreads();
+            for (int q = 0; q < PER; ++q)
+                if (tok[q] >= v0 && tok[q] < v0 + nv) atomicAdd(&acc[tok[q] - v0], wj[q]);
+            __syncthreads();
+        }
         if (vec4) {
             // Stores with no branch around them (lanes past the row store to a
             // sink), so that no store waits for the one before it.
@@ -1122,6 +1125,9 @@ __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, i
     uint32_t *hist = reinterpret_cast<uint32_t *>(tmp + kSplitCap);                // [2 << kFinishBinsLog2]: counts, starts
     int32_t *tok_of = reinterpret_cast<int32_t *>(smem + kSortBytes);              // [kSplitCap]
     float *acc = reinterpret_cast<float *>(smem);  // mixture: a vocabulary tile, over everything above
+    // sliced: the slice's tile, over the sort's scratch (dead once the sort returns)
+    float *acc_s = reinterpret_cast<float *>(tmp);
+    static_assert(kVocabSlice * 4 <= kSplitCap * 8, "the slice's tile fits over the sort scratch");
     __shared__ Shared sh;
     __shared__ uint32_t part_off[kWave + 1];
 
@@ -1219,6 +1225,7 @@ __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, i
 #pragma unroll
             for (int q = 0; q < PER; ++q)
                 if (valid[q]) tok_of[slot[q]] = tv[q];
+            if constexpr (SLICED) reinterpret_cast<float4 *>(acc_s)[tid] = make_float4(0.f, 0.f, 0.f, 0.f);
             __syncthreads();
         }
         x = ok ? cand[tid] : ~0ull;
@@ -1234,6 +1241,10 @@ __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, i
         x = ok ? cand[tid] : ~0ull;
         id = static_cast<uint32_t>(x);
         if (MIX && ok) tok = m.values[k0 + id];
+        if constexpr (SLICED) {
+            reinterpret_cast<float4 *>(acc_s)[tid] = make_float4(0.f, 0.f, 0.f, 0.f);
+            __syncthreads();
+        }
     }
     if (tok < 0 || tok >= m.V) tok = -1;  // tokens outside [0, V) carry no mass
     if (MODE == kMixFixed && !SLICED && tok >= 0) plm_t = plm_row[tok];  // needed only at the end
@@ -1248,6 +1259,10 @@ __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, i
     if constexpr (MIX) {
         const float dj = __uint_as_float(static_cast<uint32_t>(x >> 32));
         const float wj = ok ? expf(-m.mu * (dj - d0)) : 0.0f;
+        const int64_t c0 = static_cast<int64_t>(g) * kVocabSlice;  // sliced: this workgroup's entries
+        if constexpr (SLICED) {
+            if (tok >= c0 && tok < c0 + kVocabSlice) atomicAdd(&acc_s[tok - c0], wj);  // ordered by Z's barrier
+        }
         // Z; the barrier also ends every use of the sort buffers, which the
         // vocabulary tile then takes over.
         const float wsum = wave_allsum(wj);
@@ -1262,10 +1277,9 @@ __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, i
         const uint64_t k1[1] = {ok ? ((x >> 32) << 32) | id : ~0ull};
         if constexpr (SLICED) {
             // this workgroup's slice of the row, with any lambda
-            const int64_t c0 = static_cast<int64_t>(g) * kVocabSlice;
             const int64_t c1 = m.V - c0 < kVocabSlice ? m.V : c0 + kVocabSlice;
-            mix_row<1, kVocabSlice, MODE == kMixNest, true, true>(w1, t1, k1, z, lam, m, b, acc, pre, dtok, c0, c1,
-                                                                  slices, g == 0);
+            mix_row<1, kVocabSlice, MODE == kMixNest, true, true, true>(w1, t1, k1, z, lam, m, b, acc_s, pre, dtok,
+                                                                        c0, c1, slices, g == 0);
             return;
         } else if constexpr (rrc_mode(MODE)) {
             // lambda_t is known only now: the whole row, tile by tile
