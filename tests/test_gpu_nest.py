@@ -194,6 +194,34 @@ def test_rows_written_in_vocabulary_slices(V):
                                rtol=0, atol=1e-5)
 
 
+@pytest.mark.parametrize("B", [32, 33])
+def test_split_finish_on_both_sides_of_slicing(B):
+    """B queries, each on its own set of 4096 keys (split select, one part a
+    row): with 32 the finish takes 8 vocabulary slices a row (256 workgroups),
+    with 33 one workgroup a row, the parts kernel writing the fixed-lambda
+    dense term.  The fixed-lambda, RRC and NEST steps all match the oracle."""
+    _say(f"split finish, B={B}")
+    spec = gen.scaled(gen.config("ragged_batch"), B=B, S=B, n_keys=4096, d=256, mu=1 / 16, r=256)
+    w = gen.make(spec, 90 + B, device="cuda")
+    prob = knn.MixtureProblem(w.queries, w.keys, w.values, w.key_offsets, w.query_offsets, w.p_lm, w.r, w.mu,
+                              w.lam, key_offsets_host=w.key_offsets_host, query_offsets_host=w.query_offsets_host)
+    p_m, ids, dists = prob.run()
+    torch.cuda.synchronize()
+    rep = parity.check_workload(w, p_m, ids, dists)
+    assert rep.ok(), rep.failures[:5]
+    alpha = _median_ratio(w)
+    p_m, ids, dists, lam = prob.run_rrc(alpha, TAU)
+    torch.cuda.synchronize()
+    rep = parity.check_workload(w, p_m, ids, dists, rrc=(alpha, TAU), lambdas=lam)
+    assert rep.ok(), rep.failures[:5]
+    draft = _drafts(w, B)
+    out = prob.run_nest(alpha, TAU, DELTA, draft_tokens=draft)
+    torch.cuda.synchronize()
+    rep = parity.check_workload(w, out["p_m"], out["ids"], out["dists"], rrc=(alpha, TAU), lambdas=out["lambdas"])
+    assert rep.ok(), rep.failures[:5]
+    _check_decisions(out, w.values.cpu().numpy(), w.key_offsets_host, w.query_offsets_host, draft)
+
+
 SYNTH = [
     ("decode-bf16-split", gen.scaled(gen.config("decode_7b"), n_keys=30000, B=2), 81),
     ("ragged-bf16", gen.scaled(gen.config("ragged_batch"), B=12, S=4, n_keys=(1100, 5000, 3333, 2048), r=1024), 82),
