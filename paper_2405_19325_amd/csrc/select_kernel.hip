@@ -617,12 +617,13 @@ __device__ __forceinline__ void note_entry(float v, int64_t w, int32_t dtok, uin
 //
 // dtok is the draft token of the row (NEST; -1 for none), read by the caller
 // at its start.  A workgroup writes entries [c0, c1) of the row (c1 < 0: to
-// the end), c0 a multiple of 4 kT; ONE_TILE: they fit one tile, and pre holds
-// it; SCATTERED (with ONE_TILE): the caller has already added the weights
-// into acc and ordered that with a barrier.  When `slices` workgroups share the row, the one with
-// first_slice set writes what belongs to the row as a whole but not to an
-// entry, and the NEST outputs come from the last of them to finish, through
-// m.best[b] and m.ticket[b] (both zero before the first one starts).
+// the end), c0 a multiple of 4 kT.  ONE_TILE: they fit one tile, and pre
+// holds it.  SCATTERED (with ONE_TILE): the caller has already added the
+// weights into acc and ordered that with a barrier.  When `slices` workgroups
+// share the row, the one with first_slice set writes what belongs to the row
+// as a whole but not to an entry, and the NEST outputs come from the last of
+// them to finish, through m.best[b] and m.ticket[b] (both zero before the
+// first one starts).
 template <int PER, int TILE, bool NEST, bool PREFETCHED, bool ONE_TILE = false, bool SCATTERED = false>
 __device__ __forceinline__ void mix_row(const float (&wj)[PER], const int32_t (&tok)[PER], const uint64_t (&nkey)[PER],
                                         float z, float lam, const MixArgs &m, int64_t b, float *acc,
@@ -1261,10 +1262,11 @@ __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, i
         const float wj = ok ? expf(-m.mu * (dj - d0)) : 0.0f;
         const int64_t c0 = static_cast<int64_t>(g) * kVocabSlice;  // sliced: this workgroup's entries
         if constexpr (SLICED) {
-            if (tok >= c0 && tok < c0 + kVocabSlice) atomicAdd(&acc_s[tok - c0], wj);  // ordered by Z's barrier
+            if (tok >= c0 && tok < c0 + kVocabSlice) atomicAdd(&acc_s[tok - c0], wj);
         }
-        // Z; the barrier also ends every use of the sort buffers, which the
-        // vocabulary tile then takes over.
+        // Z; the barrier also ends every use of the sort buffers, which an
+        // unsliced vocabulary tile then takes over, and orders a slice's
+        // additions before its reads.
         const float wsum = wave_allsum(wj);
         if (lane == 0) sh.red_f[tid / kWave] = wsum;
         __syncthreads();
