@@ -170,6 +170,39 @@ def test_small_workloads(name, spec, seed, qps):
         assert ids[:, 0].cpu().numpy().tolist() == w.planted_ids.tolist()
 
 
+@pytest.mark.parametrize("B2", [3, 40])
+def test_empty_key_sets_without_queries(B2):
+    """Key sets of 0 keys own no query (a set that owns one needs r keys): one
+    between two sets and one at the end, whose offset is the total.  With 2 +
+    B2 queries the rows take the split (B2 = 3) or the one-workgroup select
+    (B2 = 40); ids and distances match the oracle bit for bit (integer
+    distances), p_M to the usual bound."""
+    _say(f"empty key sets, {2 + B2} queries")
+    rng = np.random.default_rng(31 + B2)
+    n0, n2, d, r = 3000, 2000, 8, 64
+    k = np.zeros((n0 + n2, d), np.float32)
+    k[:, :3] = rng.integers(-6, 7, (n0 + n2, 3))
+    q = np.zeros((2 + B2, d), np.float32)
+    q[:, 3] = np.arange(2 + B2) % 5
+    V = 1000
+    vals = rng.integers(0, V, n0 + n2).astype(np.int32)
+    p_lm = rng.dirichlet(np.ones(V), 2 + B2).astype(np.float32)
+    ko = np.array([0, n0, n0, n0 + n2, n0 + n2])
+    qo = np.array([0, 2, 2, 2 + B2, 2 + B2])
+    dev = "cuda"
+    prob = knn.MixtureProblem(torch.as_tensor(q, device=dev), torch.as_tensor(k, device=dev),
+                              torch.as_tensor(vals, device=dev), torch.as_tensor(ko, device=dev),
+                              torch.as_tensor(qo, device=dev), torch.as_tensor(p_lm, device=dev), r, 0.1, 0.4,
+                              key_offsets_host=ko, query_offsets_host=qo)
+    p_m, ids, dists = prob.run()
+    torch.cuda.synchronize()
+    o_ids, o_d = oracle.select(q, k, "f32", ko, qo, r)
+    np.testing.assert_array_equal(ids.cpu().numpy(), o_ids)
+    np.testing.assert_array_equal(dists.cpu().numpy().astype(np.float64), o_d)
+    np.testing.assert_allclose(p_m.cpu().numpy(), oracle.mix(o_ids, o_d, vals, ko, qo, p_lm, 0.1, 0.4),
+                               rtol=0, atol=1e-5)
+
+
 def test_query_equal_to_key_gives_zero_distance():
     _say("q == k")
     spec = gen.scaled(gen.config("decode_7b"), n_keys=8000, B=4)
