@@ -194,6 +194,52 @@ def test_rows_written_in_vocabulary_slices(V):
                                rtol=0, atol=1e-5)
 
 
+# (path, keys, queries, r): vocabularies larger than one mixture tile (32768
+# entries on the one-workgroup select and the unsliced split finish, 8192 on
+# the general select), so that rows are written over several tiles.
+LARGE_V_PATHS = [("split-sliced", 40000, 2, 256), ("split-unsliced", 40000, 20, 256),
+                 ("one-workgroup", 40000, 40, 256), ("general-r2048", 40000, 3, 2048)]
+
+
+@pytest.mark.parametrize("V", [50257, 65536])
+@pytest.mark.parametrize("path,n,B,r", LARGE_V_PATHS, ids=[p[0] for p in LARGE_V_PATHS])
+def test_vocabularies_over_several_tiles(path, n, B, r, V):
+    """Fixed-lambda, RRC and NEST steps with V = 50257 (4-byte mixture) and
+    65536 (16-byte mixture): ids and distances bit for bit (integer distances),
+    p_M to the usual bound, the decoding outputs on the GPU's own rows; drafts
+    in the first tile, the last one, and outside [0, V)."""
+    _say(f"large vocabulary: {path} V={V}")
+    rng = np.random.default_rng(V + B)
+    d = 4
+    k = np.zeros((n, d), np.float32)
+    k[:, :3] = rng.integers(-6, 7, (n, 3))
+    q = np.zeros((B, d), np.float32)
+    q[:, 3] = np.arange(B) % 6
+    vals = rng.integers(0, V, n).astype(np.int32)
+    p_lm = rng.dirichlet(np.ones(V), B).astype(np.float32)
+    ko, qo = np.array([0, n]), np.array([0, B])
+    prob = _problem(q, k, vals, p_lm, ko, qo, r, 0.05, torch.float32)
+    o_ids, o_d = oracle.select(q, k, "f32", ko, qo, r)
+    p_m, ids, dists = prob.run()
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(ids.cpu().numpy(), o_ids)
+    np.testing.assert_array_equal(dists.cpu().numpy().astype(np.float64), o_d)
+    np.testing.assert_allclose(p_m.cpu().numpy(), oracle.mix(o_ids, o_d, vals, ko, qo, p_lm, 0.05, prob.lam),
+                               rtol=0, atol=1e-5)
+    o_lam = oracle.rrc_lambda(o_d, ALPHA, TAU)
+    ref = oracle.mix(o_ids, o_d, vals, ko, qo, p_lm, 0.05, o_lam)
+    p_m, ids, dists, lam = prob.run_rrc(ALPHA, TAU)
+    torch.cuda.synchronize()
+    np.testing.assert_allclose(lam.cpu().numpy().astype(np.float64), o_lam, rtol=0, atol=1e-6)
+    np.testing.assert_allclose(p_m.cpu().numpy(), ref, rtol=0, atol=1e-5)
+    draft = torch.as_tensor(np.array([[3, V - 2, V, -5][i % 4] for i in range(B)], np.int32), device="cuda")
+    out = prob.run_nest(ALPHA, TAU, DELTA, draft_tokens=draft)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(out["ids"].cpu().numpy(), o_ids)
+    np.testing.assert_allclose(out["p_m"].cpu().numpy(), ref, rtol=0, atol=1e-5)
+    _check_decisions(out, vals, ko, qo, draft)
+
+
 @pytest.mark.parametrize("B", [32, 33])
 def test_split_finish_on_both_sides_of_slicing(B):
     """B queries, each on its own set of 4096 keys (split select, one part a
