@@ -326,6 +326,62 @@ def test_nest_step_synthetic_workloads(name, spec, seed):
     torch.testing.assert_close(p_m2, first["p_m"], rtol=0, atol=1e-7)
 
 
+def test_steps_replay_from_graphs():
+    """The fixed-lambda step and the NEST step (split select, finish in
+    vocabulary slices with its cross-slice maximum and count, which the parts
+    kernel clears, so no memset) captured in HIP graphs: three rounds of
+    replays, with eager steps and synchronisations between and every output
+    overwritten before each replay, each equal to the eager results: ids,
+    distances and decisions exactly, p_M and the p_M values among the outputs
+    up to the order of LDS atomics."""
+    _say("graph replays")
+    w = gen.make(gen.scaled(gen.config("decode_7b"), n_keys=20000, B=2), 87, device="cuda")
+    prob = knn.MixtureProblem(w.queries, w.keys, w.values, w.key_offsets, w.query_offsets, w.p_lm, w.r, w.mu,
+                              w.lam, key_offsets_host=w.key_offsets_host, query_offsets_host=w.query_offsets_host)
+    draft = _drafts(w, 87)
+    ref_n = {k: v.clone() for k, v in prob.run_nest(ALPHA, TAU, DELTA, draft_tokens=draft).items()}
+    ref_f = [t.clone() for t in prob.run()]
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    g_nest, g_fixed = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g_nest, stream=side):
+        prob.run_nest(ALPHA, TAU, DELTA, draft_tokens=draft)
+    with torch.cuda.graph(g_fixed, stream=side):
+        prob.run()
+    torch.cuda.synchronize()
+    exact = ("ids", "dists", "next_token", "span_key", "use_span", "lambdas")
+
+    def poison():  # every output overwritten before a replay, so each replay must write it again
+        for t in (prob.p_m, prob.dists, prob.lambdas, prob.p_max, prob.p_draft):
+            t.fill_(float("nan"))
+        for t in (prob.ids, prob.next_token, prob.span_key, prob.use_span):
+            t.fill_(-7)
+        torch.cuda.synchronize()
+
+    for rnd in range(3):
+        poison()
+        g_nest.replay()
+        torch.cuda.synchronize()
+        got = {"p_m": prob.p_m, "ids": prob.ids, "dists": prob.dists, "lambdas": prob.lambdas,
+               "next_token": prob.next_token, "p_max": prob.p_max, "span_key": prob.span_key,
+               "use_span": prob.use_span, "p_draft": prob.p_draft}
+        for key, want in ref_n.items():
+            if key in exact:
+                assert torch.equal(got[key], want), (rnd, key)
+            else:
+                torch.testing.assert_close(got[key], want, rtol=0, atol=1e-7)
+        prob.run()  # eager work between replays
+        torch.cuda.synchronize()
+        poison()
+        g_fixed.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(prob.ids, ref_f[1]) and torch.equal(prob.dists, ref_f[2]), rnd
+        torch.testing.assert_close(prob.p_m, ref_f[0], rtol=0, atol=1e-7)
+        prob.run_nest(ALPHA, TAU, DELTA, draft_tokens=draft)
+        torch.cuda.synchronize()
+
+
 def test_spec_verify_hand_cases(golden_dir):
     import json
     import os
