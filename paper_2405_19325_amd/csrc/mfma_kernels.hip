@@ -21,8 +21,9 @@
 // of the span -- the same elements for both operands, so the contraction is
 // exact up to fp32 rounding -- for v_mfma_f32_16x16x32 (bf16 or f16, fp32
 // accumulate).  Two LDS buffers alternate: while the matrix cores work on
-// span t, span t + 1 is written to the other buffer, and spans t + 2 and
-// t + 3 load into two register sets.  The loads are never guarded by a
+// span t, span t + 1 is written to the other buffer, and the next NS spans
+// load into NS register sets (NS = 2 to 4, as many as the shape's registers
+// allow at two waves per SIMD).  The loads are never guarded by a
 // branch, since a branch around loads makes the compiler wait for every load
 // in flight: rows past the data read the tile's first row, and steps past the
 // tile's end re-read its last span (from L2).
@@ -332,7 +333,7 @@ template <knn_dtype DT, bool NORMS>
 hipError_t launch_mq(int mq, const DistArgs &a, int64_t n_tiles, int64_t groups, dim3 grid, hipStream_t st) {
     const dim3 b4(4 * kWave), b8(8 * kWave);
     switch (mq) {
-    case 1: hipLaunchKernelGGL((k_dist_mfma<DT, 1, 4, 1, 3, NORMS, 128, 128>), grid, b4, 0, st, a, n_tiles, groups); break;
+    case 1: hipLaunchKernelGGL((k_dist_mfma<DT, 1, 4, 1, 4, NORMS, 128, 128>), grid, b4, 0, st, a, n_tiles, groups); break;
     case 2: hipLaunchKernelGGL((k_dist_mfma<DT, 2, 4, 1, 3, NORMS, 128, 128>), grid, b4, 0, st, a, n_tiles, groups); break;
     case 4: hipLaunchKernelGGL((k_dist_mfma<DT, 4, 4, 1, 3, NORMS, 128, 128>), grid, b4, 0, st, a, n_tiles, groups); break;
     case 8: hipLaunchKernelGGL((k_dist_mfma<DT, 8, 4, 2, 2, NORMS, 256, 64>), grid, b8, 0, st, a, n_tiles, groups); break;
