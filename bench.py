@@ -64,8 +64,8 @@ def measured_traffic(workload):
 def main():
     a = _args()
     if a.gpus != 1:
-        print(f"bench.py runs on one GPU only; --gpus {a.gpus} is not supported by this build "
-              "(the kNN-LM step has no cross-GPU path here).", file=sys.stderr)
+        print(f"bench.py runs on one GPU only; --gpus {a.gpus} is not supported "
+              "(the library's kNN-LM step has no cross-GPU path).", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np

@@ -59,7 +59,7 @@ typedef enum {
     KNN_OK = 0,
     KNN_ERR_INVALID_ARG = 1,  /* null pointer, bad size, mu/lambda out of range, bad hint */
     KNN_ERR_R_EXCEEDS_N = 2,  /* r larger than the smallest key set (min_keys_per_set) */
-    KNN_ERR_UNSUPPORTED = 3,  /* valid request this build does not serve (r > KNNLM_MAX_R, ...) */
+    KNN_ERR_UNSUPPORTED = 3,  /* valid request the library does not serve (r > KNNLM_MAX_R, ...) */
     KNN_ERR_WORKSPACE = 4,    /* workspace NULL or smaller than knn_lm_mixture_workspace_size() */
     KNN_ERR_HIP = 5           /* a HIP launch failed */
 } knn_status;
