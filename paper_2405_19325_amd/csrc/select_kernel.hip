@@ -1616,12 +1616,14 @@ hipError_t launch_sel(const SelectArgs &a, const MixArgs &m, int64_t B, hipStrea
         const int64_t slices = MIX ? (m.V + kVocabSlice - 1) / kVocabSlice : 1;
         const bool sliced = MIX && B * slices <= kSliceMaxBlocks &&
                             (MODE != kMixNest || (m.best != nullptr && m.ticket != nullptr));
-        if (sliced) {
-            hipLaunchKernelGGL((k_select_parts<MODE, false>), dim3(static_cast<unsigned>(B * parts)), block, 0, st, a,
-                               m, parts);
+        const dim3 pgrid(static_cast<unsigned>(B * parts));
+        if constexpr (MODE == kMixFixed) {  // the dense term: in the parts kernel unless the finish is sliced
+            if (sliced)
+                hipLaunchKernelGGL((k_select_parts<MODE, false>), pgrid, block, 0, st, a, m, parts);
+            else
+                hipLaunchKernelGGL((k_select_parts<MODE, true>), pgrid, block, 0, st, a, m, parts);
         } else {
-            hipLaunchKernelGGL((k_select_parts<MODE, true>), dim3(static_cast<unsigned>(B * parts)), block, 0, st, a,
-                               m, parts);
+            hipLaunchKernelGGL((k_select_parts<MODE, false>), pgrid, block, 0, st, a, m, parts);
         }
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
