@@ -12,7 +12,7 @@
  *   1. s(q, k) = -||q - k||^2: the negative squared L2 distance, computed here
  *      directly as sum_j (q_j - k_j)^2 in fp64 from the stored element bytes
  *      widened to fp64 (eq. non-parametric and the sentence after it;
- *      Appendix A "retrieve the top-1024 tokens using the squared l2 distance").
+ *      Appendix A, where r = 1024 neighbours are retrieved by squared L2 distance).
  *   2. pi = the r keys of the query's own key set with the largest s, i.e. the
  *      smallest distance; equal distances are ordered by the lower key index
  *      (the paper does not say; this is the reading used throughout).

@@ -7,8 +7,8 @@ loaded, importing the functions raises.
 from __future__ import annotations
 
 import ctypes
-import os
 import re
+import sys
 from typing import Dict
 
 from . import build as _build
@@ -61,11 +61,14 @@ def library_path() -> str:
 
 
 def load() -> ctypes.CDLL:
-    """Load libknnlm.so (building it first only if it is not there at all)."""
+    """Load libknnlm.so, rebuilding it first if it is missing or was built from
+    other sources than the ones in the tree (a failed rebuild raises)."""
     global _lib
     if _lib is not None:
         return _lib
-    if not os.path.exists(_build.LIB):
+    if _build.stale():
+        print(f"libknnlm: {_build.LIB} is missing or older than its sources; rebuilding", file=sys.stderr,
+              flush=True)
         _build.build()
     lib = ctypes.CDLL(_build.LIB)
     for name, (res, args) in SIGNATURES.items():

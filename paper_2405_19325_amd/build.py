@@ -3,6 +3,7 @@ from __future__ import annotations
 
 import concurrent.futures
 import glob
+import hashlib
 import os
 import shutil
 import subprocess
@@ -13,6 +14,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libknnlm.so")
+# Hash of the sources a library was built from, written next to it by build().
+LIB_HASH = LIB + ".srchash"
 OBJDIR = os.path.join(ROOT, "_build", "obj")
 
 HIPCC = os.environ.get("HIPCC", shutil.which("hipcc") or "/opt/rocm/bin/hipcc")
@@ -35,9 +38,25 @@ def _compile(src: str) -> str:
     return obj
 
 
+def _deps():
+    return sorted(sources() + glob.glob(os.path.join(CSRC, "*.h")) + glob.glob(os.path.join(INCLUDE, "*.h")))
+
+
+def source_hash() -> str:
+    """sha256 over the names and contents of the HIP sources and headers the library is built from."""
+    h = hashlib.sha256()
+    for p in _deps():
+        h.update(os.path.relpath(p, ROOT).encode() + b"\0")
+        with open(p, "rb") as f:
+            h.update(f.read())
+        h.update(b"\0")
+    return h.hexdigest()
+
+
 def build(verbose: bool = False) -> str:
     """Compile every csrc/*.hip and link libknnlm.so next to this file."""
     os.makedirs(OBJDIR, exist_ok=True)
+    digest = source_hash()
     srcs = sources()
     with concurrent.futures.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
         objs = list(ex.map(_compile, srcs))
@@ -47,17 +66,20 @@ def build(verbose: bool = False) -> str:
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stderr}")
     os.replace(tmp, LIB)
+    with open(LIB_HASH + ".tmp", "w") as f:
+        f.write(digest + "\n")
+    os.replace(LIB_HASH + ".tmp", LIB_HASH)
     if verbose:
         print(f"built {LIB}")
     return LIB
 
 
 def stale() -> bool:
-    if not os.path.exists(LIB):
+    """True if libknnlm.so is missing or was not built from the sources as they are now."""
+    if not os.path.exists(LIB) or not os.path.exists(LIB_HASH):
         return True
-    t = os.path.getmtime(LIB)
-    deps = sources() + glob.glob(os.path.join(CSRC, "*.h")) + glob.glob(os.path.join(INCLUDE, "*.h"))
-    return any(os.path.getmtime(p) > t for p in deps)
+    with open(LIB_HASH) as f:
+        return f.read().strip() != source_hash()
 
 
 if __name__ == "__main__":

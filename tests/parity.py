@@ -143,10 +143,43 @@ def check_query(rep: Report, b: int, q_host: np.ndarray, keys_host: np.ndarray, 
         rep.failures.append(f"{tag}: sum p_M off by {serr:.3g}")
 
 
+def host_threads() -> int:
+    """Host threads the oracle may use here: the cores this process may run on, at most 16."""
+    return max(1, min(16, oracle.default_threads()))
+
+
+def oracle_select_rows(q_rows: np.ndarray, keys_host: np.ndarray, dtype: str, r: int,
+                       threads: Optional[int] = None):
+    """The oracle's (ids, fp64 dists) of each query row against one key set.
+
+    With several rows, the rows run concurrently, each oracle call on its share
+    of the threads (ctypes releases the GIL and the oracle keeps no state
+    between calls); with one row, that row's key range is split over all of
+    them.  Neither changes the oracle's arithmetic."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    threads = threads or host_threads()
+    nq = q_rows.shape[0]
+    n = keys_host.shape[0]
+    workers = max(1, min(threads, nq))
+    per = max(1, threads // workers)
+
+    def one(i):
+        ids, d = oracle.select(q_rows[i:i + 1], keys_host, dtype, np.array([0, n]), np.array([0, 1]), r,
+                               nthreads=per)
+        return ids[0], d[0]
+
+    if workers == 1:
+        return [one(i) for i in range(nq)]
+    with ThreadPoolExecutor(max_workers=workers) as ex:
+        return list(ex.map(one, range(nq)))
+
+
 def check_workload(w, p_m, ids, dists, sample: Optional[List[int]] = None, rrc: Optional[tuple] = None,
-                   lambdas=None) -> Report:
+                   lambdas=None, host_keys=None) -> Report:
     """P2-P5 on the queries `sample` (all by default) of a workload run on the GPU; with
-    rrc = (alpha, tau) and the GPU's per-query lambdas, P6 too."""
+    rrc = (alpha, tau) and the GPU's per-query lambdas, P6 too.  host_keys(s), if
+    given, returns set s's key elements on the host (e.g. from a cache)."""
     rep = Report()
     ko, qo = w.key_offsets_host, w.query_offsets_host
     set_of = w.set_of_query()
@@ -158,12 +191,16 @@ def check_workload(w, p_m, ids, dists, sample: Optional[List[int]] = None, rrc: 
     for b in sample:
         by_set.setdefault(int(set_of[b]), []).append(b)
     for s, bs in by_set.items():
-        keys_h, dt = oracle.host_elements(w.keys[ko[s]:ko[s + 1]])
+        if host_keys is not None:
+            keys_h, dt = host_keys(s)
+        else:
+            keys_h, dt = oracle.host_elements(w.keys[ko[s]:ko[s + 1]])
         vals = w.values[ko[s]:ko[s + 1]].cpu().numpy()
-        for b in bs:
-            q_h, _ = oracle.host_elements(w.queries[b:b + 1])
-            check_query(rep, b, q_h, keys_h, dt, vals, w.p_lm[b].cpu().numpy(), w.r, w.mu, w.lam, ids_h[b],
-                        dists_h[b], p_m[b].cpu().numpy(), rrc=rrc,
+        q_rows, _ = oracle.host_elements(w.queries[bs])
+        refs = oracle_select_rows(q_rows, keys_h, dt, w.r)
+        for j, b in enumerate(bs):
+            check_query(rep, b, q_rows[j], keys_h, dt, vals, w.p_lm[b].cpu().numpy(), w.r, w.mu, w.lam, ids_h[b],
+                        dists_h[b], p_m[b].cpu().numpy(), oracle_ids=refs[j][0], oracle_dists=refs[j][1], rrc=rrc,
                         gpu_lambda=None if lam_h is None else float(lam_h[b]))
         del keys_h
     return rep

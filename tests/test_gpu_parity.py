@@ -4,8 +4,8 @@ Rules P2-P5 are in tests/parity.py.  Cases: the hand-worked cases, exact
 integer inputs (every distance exact, so ids, order and distances must match
 the oracle bit for bit), every element type and both load paths, ragged key
 sets, planted neighbours, degenerate shapes (r = 1, r = N, r = 4096, all keys
-equal, empty query groups), lambda = 1, precomputed key norms, the stage
-entry points, and the full-size workloads on sampled queries.
+equal, empty query groups), lambda = 1, precomputed key norms and the stage
+entry points.  The full-size workloads are in test_gpu_full_size.py.
 """
 import gc
 import json
@@ -354,32 +354,6 @@ def test_mix_entry_point():
     np.testing.assert_allclose(out.cpu().numpy(), ref, rtol=0, atol=1e-6)
 
 
-# -------------------------------------------------------- full-size workloads
-
-FULL = [("decode_7b", None), ("ragged_batch", [0, 17, 40, 63]), ("decode_70b", [0, 9]),
-        ("specverify_seq", [0, 31, 127]), ("specverify_static", [0, 77])]
-
-
-@pytest.mark.parametrize("name,sample", FULL, ids=[f[0] for f in FULL])
-def test_full_size_workloads(name, sample):
-    _free()
-    _say(f"full workload {name}: generating")
-    w = gen.make(gen.config(name), gen.CONFIG_SEEDS[name], device="cuda")
-    _say(f"full workload {name}: running")
-    p_m, ids, dists = _run(w)
-    _say(f"full workload {name}: oracle on {sample if sample is not None else 'all'} queries")
-    rep = parity.check_workload(w, p_m, ids, dists, sample=sample)
-    _say(f"{name}: {rep.summary()}")
-    # properties that hold for every query
-    pm64 = p_m.double()
-    torch.testing.assert_close(pm64.sum(1), w.lam * w.p_lm.double().sum(1) + (1 - w.lam), rtol=0, atol=1e-5)
-    assert torch.all(dists[:, 1:] >= dists[:, :-1])
-    assert int(ids.min()) >= 0
-    assert rep.ok(), rep.failures[:5]
-    del w, p_m, ids, dists
-    _free()
-
-
 def test_split_and_one_workgroup_select_agree():
     """The same queries through the split select (few queries: a 64K-key row
     over 16 workgroups) and the one-workgroup select (20 queries): the same
@@ -404,8 +378,9 @@ def test_split_and_one_workgroup_select_agree():
 
 def _sampled_positions(path, n):
     """Key positions whose distances the sampled threshold of each select path reads."""
-    if path == "split":  # 4096 keys, one every n / 4096
-        return (np.arange(4096) * n) >> 12
+    if path == "split":  # 1024 runs of 4 consecutive keys, a run starting every n / 1024 (at a multiple of 4)
+        starts = ((np.arange(1024, dtype=np.int64) * n) >> 10) & ~3
+        return (starts[:, None] + np.arange(4)).ravel()
     t = np.arange(1024)
     return (t & 15) * 4096 + 4 * t + ((t >> 4) & 3)  # one-workgroup path: a key per thread's registers
 
@@ -437,6 +412,38 @@ def test_adversarial_row_takes_the_streamed_path(path, B):
     counts = np.bincount(vals[expect], minlength=50).astype(np.float64)
     want = 0.5 * 0.02 + 0.5 * counts / r
     np.testing.assert_allclose(p_m.cpu().numpy(), np.broadcast_to(want, (B, 50)), rtol=0, atol=1e-6)
+
+
+@pytest.mark.parametrize("path,B", [("split", 1), ("one-workgroup", 20)])
+def test_sample_keeps_fewer_than_r_takes_the_streamed_path(path, B):
+    """The keys at the sampled positions are the nearest of the row, at many
+    different distances, and every other key is far away: the sampled
+    threshold then keeps about a hundred keys, fewer than r, and the streamed
+    select over the whole row must take over.  Small integer entries make
+    every distance exact, so ids and distances equal the oracle's bit for bit."""
+    _say(f"sample keeps fewer than r ({path})")
+    n, d, r = 65536, 16, 1000
+    sampled = _sampled_positions(path, n)
+    j = np.arange(sampled.size)
+    k = np.full((n, d), 100.0, np.float32)
+    k[sampled] = 0.0
+    k[sampled, 0] = 1 + j % 60
+    k[sampled, 1] = j // 60
+    q = np.zeros((B, d), np.float32)
+    rng = np.random.default_rng(97)
+    vals = rng.integers(0, 50, n).astype(np.int32)
+    p_lm = np.full((B, 50), 0.02, np.float32)
+    tq, tk, tv, tko, tqo, tp = _tensor_inputs(q, k, vals, p_lm, [0, n], [0, B], torch.bfloat16)
+    p_m, ids, dists = knn.mixture(tq, tk, tv, tko, tqo, tp, r, 0.1, 0.5)
+    torch.cuda.synchronize()
+    qh, dt = oracle.host_elements(tq)
+    kh, _ = oracle.host_elements(tk)
+    oids, odists = oracle.select(qh, kh, dt, np.array([0, n]), np.array([0, B]), r)
+    assert np.isin(oids, sampled).all()  # the answer lies among the samples
+    np.testing.assert_array_equal(ids.cpu().numpy(), oids)
+    np.testing.assert_array_equal(dists.cpu().numpy().astype(np.float64), odists)
+    ref = oracle.mix(oids, odists, vals, np.array([0, n]), np.array([0, B]), p_lm, 0.1, 0.5)
+    np.testing.assert_allclose(p_m.cpu().numpy(), ref, rtol=0, atol=1e-5)
 
 
 # ------------------------------------------------- matrix-core (query batch) path
