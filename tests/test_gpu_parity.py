@@ -446,6 +446,49 @@ def test_sample_keeps_fewer_than_r_takes_the_streamed_path(path, B):
     np.testing.assert_allclose(p_m.cpu().numpy(), ref, rtol=0, atol=1e-5)
 
 
+# (case, V): 40,000 keys of width 4, two queries and a mixture -- the split select (ten parts per row, each
+# keeping its keys below a threshold sampled across the row) and its finish, sliced by 4096-entry pieces of
+# p_M.  V = 10001 takes the mixture's scalar path, V = 32000 its 16-byte path.
+SPLIT_SLICED = [("threshold", 32000), ("threshold", 10001), ("all-equal-fallback", 32000)]
+
+
+@pytest.mark.parametrize("case,V", SPLIT_SLICED, ids=[f"{c}-V{v}" for c, v in SPLIT_SLICED])
+@pytest.mark.parametrize("rrc", [False, True], ids=["fixed-lambda", "rrc"])
+def test_split_select_sliced_finish_exact_integers(case, V, rrc):
+    """Integer keys (a, b, c, 0) with a, b, c in [-60, 60] give exact distances in many distinct values, so the
+    sampled threshold keeps somewhat more than r keys; with every key equal it keeps the whole row and the
+    finish falls back to the streamed select (ties by index).  ids and distances bit for bit against the
+    oracle, p_M within 1e-5 (with RRC, lambda_t within 1e-6)."""
+    _say(f"split select, sliced finish: {case}, V={V}, rrc={rrc}")
+    n, d, B, r = 40000, 4, 2, 1024
+    rng = np.random.default_rng(98)
+    k = np.zeros((n, d), np.float32)
+    if case != "all-equal-fallback":
+        k[:, :3] = rng.integers(-60, 61, (n, 3))
+    q = np.zeros((B, d), np.float32)
+    q[:, 3] = [2, 5]
+    q[1, 0] = 7
+    vals = rng.integers(0, V, n).astype(np.int32)
+    p_lm = rng.dirichlet(np.ones(V), B).astype(np.float32)
+    ko, qo = np.array([0, n]), np.array([0, B])
+    tq, tk, tv, tko, tqo, tp = _tensor_inputs(q, k, vals, p_lm, ko, qo, torch.float32)
+    prob = knn.MixtureProblem(tq, tk, tv, tko, tqo, tp, r, 0.05, 0.4, key_offsets_host=ko, query_offsets_host=qo)
+    o_ids, o_d = oracle.select(q, k, "f32", ko, qo, r)
+    if rrc:
+        p_m, ids, dists, lam_t = prob.run_rrc(0.3, 0.1)
+        torch.cuda.synchronize()
+        lam = oracle.rrc_lambda(o_d, 0.3, 0.1)
+        np.testing.assert_allclose(lam_t.cpu().numpy().astype(np.float64), lam, rtol=0, atol=1e-6)
+    else:
+        p_m, ids, dists = prob.run()
+        torch.cuda.synchronize()
+        lam = 0.4
+    np.testing.assert_array_equal(ids.cpu().numpy(), o_ids)
+    np.testing.assert_array_equal(dists.cpu().numpy().astype(np.float64), o_d)
+    ref = oracle.mix(o_ids, o_d, vals, ko, qo, p_lm, 0.05, lam)
+    np.testing.assert_allclose(p_m.cpu().numpy(), ref, rtol=0, atol=1e-5)
+
+
 # ------------------------------------------------- matrix-core (query batch) path
 
 MFMA = [
