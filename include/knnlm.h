@@ -55,6 +55,9 @@ extern "C" {
 /* Largest r accepted (the paper retrieves r = 1024, Appendix A). */
 #define KNNLM_MAX_R 4096
 
+/* Size of the per-GPU scratch array behind knn_lm_mixture_noalloc (32 MiB). */
+#define KNNLM_NOALLOC_SCRATCH_BYTES (32u << 20)
+
 typedef enum {
     KNN_OK = 0,
     KNN_ERR_INVALID_ARG = 1,  /* null pointer, bad size, mu/lambda out of range, bad hint */
@@ -110,6 +113,36 @@ knn_status knn_lm_mixture(const void *queries, const void *keys, const float *ke
                           int64_t max_keys_per_set, int64_t max_queries_per_set, knn_dtype dtype,
                           int32_t r, float mu, float lambda, float *p_m, int32_t *nbr_ids,
                           float *nbr_dists, void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * knn_lm_mixture_noalloc -- knn_lm_mixture without a workspace argument, for
+ * callers that cannot allocate device memory (code under HIP graph capture,
+ * serving loops that forbid allocation).  It computes exactly what
+ * knn_lm_mixture computes, with the same kernels, and allocates nothing: its
+ * scratch space is a static array of KNNLM_NOALLOC_SCRATCH_BYTES in device
+ * memory, one per GPU, held from the library's first use on that GPU until
+ * the process ends.  Its device address is looked up on the first call with
+ * that GPU current (make that first call outside graph capture).
+ *
+ * Arguments as knn_lm_mixture; the caller still owns every input and output.
+ * If knn_lm_mixture_workspace_size() for these sizes exceeds
+ * KNNLM_NOALLOC_SCRATCH_BYTES the call returns KNN_ERR_WORKSPACE and enqueues
+ * nothing (32 MiB serves, e.g., 64 queries on sets of up to 65,536 keys at
+ * d = 4096, or 16 queries on sets of 131,072 keys at d = 8192).
+ *
+ * Every call on one GPU shares that GPU's array, and nothing in it needs to
+ * start at any value (each call writes what it later reads): two calls that
+ * can run at the same time on one GPU (different streams without ordering)
+ * race on it and give unspecified results.  Calls on one stream are ordered
+ * and safe.
+ */
+knn_status knn_lm_mixture_noalloc(const void *queries, const void *keys, const float *key_sqnorms,
+                                  const int32_t *values, const int64_t *key_offsets,
+                                  const int64_t *query_offsets, const float *p_lm, int64_t B, int64_t d,
+                                  int64_t V, int64_t S, int64_t total_keys, int64_t min_keys_per_set,
+                                  int64_t max_keys_per_set, int64_t max_queries_per_set, knn_dtype dtype,
+                                  int32_t r, float mu, float lambda, float *p_m, int32_t *nbr_ids,
+                                  float *nbr_dists, void *stream);
 
 /*
  * knn_lm_mixture_rrc -- the whole step with a weight of p_LM per query from

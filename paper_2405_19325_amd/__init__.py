@@ -18,9 +18,8 @@ import torch
 from . import _lib
 from ._lib import DTYPES, PARTS, KnnError, load, status_string  # noqa: F401
 
-__all__ = ["MixtureProblem", "mixture", "distances", "key_sqnorms", "mix", "mix_rrc", "spec_verify", "mask_words",
-           "workspace_size", "KnnError",
-           "load", "status_string", "abi_version"]
+__all__ = ["MixtureProblem", "mixture", "mixture_noalloc", "distances", "key_sqnorms", "mix", "mix_rrc",
+           "spec_verify", "mask_words", "workspace_size", "KnnError", "load", "status_string", "abi_version"]
 
 _TORCH_DTYPES = {torch.float32: "f32", torch.bfloat16: "bf16", torch.float16: "f16"}
 
@@ -187,6 +186,30 @@ def mixture(queries, keys, values, key_offsets, query_offsets, p_lm, r, mu=None,
     prob = MixtureProblem(queries, keys, values, key_offsets, query_offsets, p_lm, r, mu, lam, key_sqnorms,
                           key_offsets_host, query_offsets_host)
     return prob.run()
+
+
+def mixture_noalloc(queries, keys, values, key_offsets, query_offsets, p_lm, r, mu, lam, p_m, ids, dists,
+                    key_offsets_host, query_offsets_host, key_sqnorms=None, stream=None):
+    """knn_lm_mixture_noalloc: the step into the caller's p_m [B, V] fp32, ids [B, r] int32 and
+    dists [B, r] fp32, with the library's static per-GPU scratch array as workspace (nothing
+    is allocated; the host offsets give the planning hints)."""
+    ko = np.asarray(key_offsets_host, np.int64)
+    qo = np.asarray(query_offsets_host, np.int64)
+    nk, nq = np.diff(ko), np.diff(qo)
+    B, d = int(queries.shape[0]), int(queries.shape[1])
+    V = int(p_lm.shape[1])
+    min_keys = int(nk[nq > 0].min()) if (nq > 0).any() else 0
+    for name, t, dt, shape in (("p_m", p_m, torch.float32, (B, V)), ("ids", ids, torch.int32, (B, r)),
+                               ("dists", dists, torch.float32, (B, r))):
+        _need(t.is_cuda and t.dtype == dt and t.is_contiguous() and tuple(t.shape) == shape,
+              f"{name}: contiguous {tuple(shape)} {dt} device tensor")
+    st = load().knn_lm_mixture_noalloc(
+        _ptr(queries), _ptr(keys), _ptr(key_sqnorms), _ptr(values), _ptr(key_offsets), _ptr(query_offsets),
+        _ptr(p_lm), B, d, V, len(ko) - 1, int(keys.shape[0]), min_keys, int(nk.max()), int(nq.max()),
+        _dtype_code(queries), int(r), float(1.0 / math.sqrt(d) if mu is None else mu), float(lam), _ptr(p_m),
+        _ptr(ids), _ptr(dists), _stream(stream))
+    _lib.check("knn_lm_mixture_noalloc", st)
+    return p_m, ids, dists
 
 
 def distances(queries, keys, key_offsets, query_offsets, key_sqnorms=None, key_offsets_host=None,

@@ -31,6 +31,7 @@ _RRC_ARGS = [P, P, P, P, P, P, P, I64, I64, I64, I64, I64, I64, I64, I64, I, I32
 
 SIGNATURES: Dict[str, tuple] = {
     "knn_lm_mixture": (I, _MIX_ARGS),
+    "knn_lm_mixture_noalloc": (I, _MIX_ARGS[:22] + [P]),
     "knn_lm_mixture_rrc": (I, _RRC_ARGS),
     "knn_lm_mixture_part": (I, [I] + _MIX_ARGS),
     "knn_nest_step": (I, [P, P, P, P, P, P, P, I64, I64, I64, I64, I64, I64, I64, I64, I, I32, F, F, F, F, P, P,

@@ -4,8 +4,16 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "knnlm.h"
 #include "select_internal.h"
+
+// The workspace of knn_lm_mixture_noalloc: one array per GPU, held from the
+// library's load until the process ends.  Host code never uses its name as an
+// address (on the host it is only a stand-in for the symbol): the device
+// address comes from hipGetSymbolAddress, once per device.
+static __device__ __align__(256) unsigned char scratch[KNNLM_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -271,6 +279,26 @@ Call make_call(const void *queries, const void *keys, const float *key_sqnorms, 
     return c;
 }
 
+// Device address of `scratch` on the current device, resolved on the first
+// call made with that device current and kept for later calls.
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mutex;
+void *g_scratch_ptr[kMaxScratchDevices];
+
+knn_status scratch_of_current_device(void **out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return KNN_ERR_HIP;
+    if (dev < 0 || dev >= kMaxScratchDevices) return KNN_ERR_UNSUPPORTED;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (g_scratch_ptr[dev] == nullptr) {
+        void *ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr) return KNN_ERR_HIP;
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = g_scratch_ptr[dev];
+    return KNN_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -291,6 +319,25 @@ knn_status knn_lm_mixture(const void *queries, const void *keys, const float *ke
     st = run_part(c, KNN_PART_DISTANCES, hs);
     if (st != KNN_OK) return st;
     return run_part(c, KNN_PART_SELECT_MIX, hs);
+}
+
+knn_status knn_lm_mixture_noalloc(const void *queries, const void *keys, const float *key_sqnorms,
+                                  const int32_t *values, const int64_t *key_offsets,
+                                  const int64_t *query_offsets, const float *p_lm, int64_t B, int64_t d,
+                                  int64_t V, int64_t S, int64_t total_keys, int64_t min_keys_per_set,
+                                  int64_t max_keys_per_set, int64_t max_queries_per_set, knn_dtype dtype,
+                                  int32_t r, float mu, float lambda, float *p_m, int32_t *nbr_ids,
+                                  float *nbr_dists, void *stream) {
+    knn_status st = check_sizes(B, d, V, S, total_keys, min_keys_per_set, max_keys_per_set, max_queries_per_set,
+                                dtype, r, true);
+    if (st != KNN_OK) return st;
+    const size_t need = layout(B, d, S, max_keys_per_set, max_queries_per_set, dtype, r).total;
+    if (need > static_cast<size_t>(KNNLM_NOALLOC_SCRATCH_BYTES)) return KNN_ERR_WORKSPACE;
+    void *ws = nullptr;
+    if ((st = scratch_of_current_device(&ws)) != KNN_OK) return st;
+    return knn_lm_mixture(queries, keys, key_sqnorms, values, key_offsets, query_offsets, p_lm, B, d, V, S,
+                          total_keys, min_keys_per_set, max_keys_per_set, max_queries_per_set, dtype, r, mu, lambda,
+                          p_m, nbr_ids, nbr_dists, ws, static_cast<size_t>(KNNLM_NOALLOC_SCRATCH_BYTES), stream);
 }
 
 knn_status knn_lm_mixture_rrc(const void *queries, const void *keys, const float *key_sqnorms,
