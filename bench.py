@@ -26,6 +26,10 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0  # MI355X HBM3E, published
+PEAK_MFMA_16BIT_TFLOPS = 2500.0  # MI355X dense bf16 / fp16 matrix cores, published
+# The workloads of the per-config block, with the timed steps of each.
+PER_CONFIG_STEPS = {"tiny": 200, "decode_7b": 200, "ragged_batch": 20, "decode_70b": 20, "specverify_seq": 10,
+                    "specverify_static": 10}
 PMC_FILE = os.path.join(ROOT, "profiles", "dist_kernel_{workload}_pmc.json")
 
 
@@ -39,6 +43,9 @@ def _args():
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle sample")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed region, run a plain 512 MiB device copy (HBM counter calibration)")
+    ap.add_argument("--per-config", dest="per_config", action="store_true", default=None,
+                    help="also time every workload (default: on for the decode_7b headline run)")
+    ap.add_argument("--no-per-config", dest="per_config", action="store_false")
     return ap.parse_args()
 
 
@@ -235,6 +242,10 @@ def main():
                 "avg_launch_ms": round(dist_launch_ms, 5), "timed_launches": n_dist,
                 "in_step_event_ms": round(avg_dist_ms, 5)}
 
+    stream_gbs = stream_read_gbs(knn, torch, dev)
+    roofline["stream_read_gbs"] = round(stream_gbs, 1)
+    roofline["frac_of_stream_read"] = round(achieved / stream_gbs, 4)
+
     if a.copy_calibration:
         src = torch.empty(256 * 1024 * 1024, dtype=torch.bfloat16, device=dev)  # 512 MiB
         src.fill_(1.0)
@@ -246,6 +257,14 @@ def main():
     cpu = None
     if not a.no_cpu_baseline:
         cpu = cpu_baseline(w, spec, seed, a.cpu_seconds)
+
+    per_config = None
+    if a.per_config if a.per_config is not None else a.workload == "decode_7b":
+        del probs, keys2, w
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        per_config = {name: time_config(name, steps, stream_gbs, not a.no_cpu_baseline)
+                      for name, steps in PER_CONFIG_STEPS.items()}
 
     line = {
         "metric": "kNN-LM mixture queries/s + achieved HBM GB/s (d=4096, N=64K keys, r=1024)",
@@ -281,7 +300,148 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
     }
+    if per_config is not None:
+        line["per_config"] = per_config
     print(json.dumps(line), flush=True)
+
+
+def stream_read_gbs(knn, torch, dev, nbytes=2 << 30, reps=10):
+    """HBM read rate of a plain read kernel (knn_stream_read) over a 2 GiB buffer, larger than the last-level
+    cache: the ceiling the distance stage's key streaming is compared with."""
+    buf = torch.ones(nbytes // 2, dtype=torch.bfloat16, device=dev)
+    sink = torch.zeros(1, dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream()
+    for _ in range(2):
+        knn.stream_read(buf, sink)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(reps):
+        knn.stream_read(buf, sink)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del buf
+    return nbytes / (ms / 1e3) / 1e9
+
+
+def _events_ms(torch, fn, n):
+    """Average ms of fn(i) over n calls on the current stream (one event pair around all of them)."""
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for i in range(n):
+        fn(i)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / n
+
+
+def time_config(name, steps, stream_gbs, with_oracle):
+    """One workload at full size: the whole step, the distance stage alone and distance + top-r, each over
+    `steps` back-to-back calls (two key buffers alternate when the keys would fit the last-level cache), the
+    fractions of 8 TB/s (and of the measured plain read) on algorithmic bytes, the matrix cores' share of
+    their dense peak on query batches, and the oracle's time for one query scaled by multiply-adds to the
+    step."""
+    import numpy as np
+    import torch
+
+    import paper_2405_19325_amd as knn
+    from workloads import gen
+
+    dev = torch.device("cuda:0")
+    spec, seed = gen.config(name), gen.CONFIG_SEEDS[name]
+    w = gen.make(spec, seed, device=dev)
+    ko, qo = w.key_offsets_host, w.query_offsets_host
+    nk, nq = np.diff(ko), np.diff(qo)
+    esize = w.keys.element_size()
+    total_keys = int(ko[-1])
+    B = int(qo[-1])
+    key_bytes = total_keys * spec.d * esize
+    dist_bytes = key_bytes + B * spec.d * esize
+    step_bytes = dist_bytes + 2 * B * spec.V * 4 + B * spec.r * 4
+    topr_bytes = dist_bytes + B * spec.r * 8
+    macs = int(np.sum(nq * nk)) * spec.d
+    bufs = [w.keys]
+    if key_bytes < 2 * 256 * 2 ** 20:
+        bufs.append(gen.second_key_copy(spec, seed, device=dev))
+    hints = dict(key_offsets_host=ko, query_offsets_host=qo)
+    probs = [knn.MixtureProblem(w.queries, k, w.values, w.key_offsets, w.query_offsets, w.p_lm, w.r, w.mu, w.lam,
+                                **hints) for k in bufs]
+    nb = len(probs)
+    for i in range(2):
+        probs[i % nb].run()
+
+    def full(i):
+        probs[i % nb].run_part("distances")
+        probs[i % nb].run_part("select_mix")
+
+    def topr(i):
+        probs[i % nb].run_part("distances")
+        probs[i % nb].run_part("select")
+
+    step_ms = _events_ms(torch, full, steps)
+    dist_ms = _events_ms(torch, lambda i: probs[i % nb].run_part("distances"), steps)
+    topr_ms = _events_ms(torch, topr, steps)
+    dist_gbs = dist_bytes / (dist_ms / 1e3) / 1e9
+    out = {
+        "workload": (f"B={B}, d={spec.d}, {spec.S} key set(s), N={total_keys} {spec.dtype} keys, r={spec.r}, "
+                     f"V={spec.V}"),
+        "steps": steps,
+        "ms_per_step": round(step_ms, 5),
+        "queries_per_s": round(B / (step_ms / 1e3), 1),
+        "step_alg_bytes": int(step_bytes),
+        "step_hbm_frac": round(step_bytes / (step_ms / 1e3) / 1e9 / PEAK_HBM_GBS, 4),
+        "distance_ms": round(dist_ms, 5),
+        "distance_gbs": round(dist_gbs, 1),
+        "distance_hbm_frac": round(dist_gbs / PEAK_HBM_GBS, 4),
+        "distance_frac_of_stream_read": round(dist_gbs / stream_gbs, 4),
+        "distance_topr_ms": round(topr_ms, 5),
+        "distance_topr_hbm_frac": round(topr_bytes / (topr_ms / 1e3) / 1e9 / PEAK_HBM_GBS, 4),
+        "key_buffers_rotated": nb,
+    }
+    if spec.dtype in ("bf16", "f16") and spec.d % 128 == 0 and int(nq.max()) >= 16:
+        tflops = 2.0 * macs / (dist_ms / 1e3) / 1e12
+        out["matrix_cores"] = {"alg_flops": 2 * macs, "tflops": round(tflops, 1),
+                               "frac_of_dense_peak": round(tflops / PEAK_MFMA_16BIT_TFLOPS, 4)}
+    del probs, bufs
+    if with_oracle:
+        out["oracle"] = oracle_estimate(w, spec, macs)
+    del w
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return out
+
+
+def oracle_estimate(w, spec, step_macs):
+    """The fp64 oracle (select + mix) on the workload's first query against its own key set, timed on this
+    host, and that time scaled by multiply-adds to the whole step."""
+    import numpy as np
+
+    import oracle
+
+    threads = host_threads()
+    ko, qo = w.key_offsets_host, w.query_offsets_host
+    s = int(np.searchsorted(qo, 0, side="right") - 1)
+    n = int(ko[s + 1] - ko[s])
+    keys_h, dt = oracle.host_elements(w.keys[ko[s]:ko[s + 1]])
+    q_h, _ = oracle.host_elements(w.queries[:1])
+    vals = w.values[ko[s]:ko[s + 1]].cpu().numpy()
+    p_lm = w.p_lm[:1].cpu().numpy()
+    k1, q1 = np.array([0, n], dtype=np.int64), np.array([0, 1], dtype=np.int64)
+    t0 = time.perf_counter()
+    ids, dists = oracle.select(q_h, keys_h, dt, k1, q1, spec.r, nthreads=threads)
+    oracle.mix(ids, dists, vals, k1, q1, p_lm, spec.mu, spec.lam)
+    el = time.perf_counter() - t0
+    q_macs = n * spec.d
+    return {"one_query_s": round(el, 3), "one_query_macs": int(q_macs),
+            "est_s_per_step": round(el * step_macs / q_macs, 2), "cores": threads}
+
+
+def host_threads():
+    """Threads the oracle uses: every core this process may run on, at most 16 (one GPU's share of the host)."""
+    return max(1, min(16, len(os.sched_getaffinity(0))))
 
 
 def cpu_baseline(w, spec, seed, budget_s):
@@ -291,7 +451,7 @@ def cpu_baseline(w, spec, seed, budget_s):
     import oracle
     from workloads import gen
 
-    threads = min(16, len(os.sched_getaffinity(0)))
+    threads = host_threads()
     n0 = int(w.key_offsets_host[1])  # the sample queries the first key set
     keys_h, dt = oracle.host_elements(w.keys[:n0])
     vals = w.values[:n0].cpu().numpy()
@@ -310,9 +470,10 @@ def cpu_baseline(w, spec, seed, budget_s):
             break
     el = time.perf_counter() - t0
     return {"value": round(done / el, 3), "unit": "queries/s", "cores": threads, "kind": "oracle",
+            "nproc": len(os.sched_getaffinity(0)), "cpu_model": _cpu_model(),
             "sample": (f"{done} decode queries of the same shape (d={spec.d}, one set of {n0} keys, "
-                       f"r={spec.r}) through the fp64 oracle select + mix, {el:.1f} s wall, {threads} threads; "
-                       f"CPU: {_cpu_model()}")}
+                       f"r={spec.r}) through the fp64 oracle select + mix, {el:.1f} s wall, {threads} threads "
+                       f"(every core this process may use, at most 16); CPU: {_cpu_model()}")}
 
 
 def _cpu_model():

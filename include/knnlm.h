@@ -315,6 +315,17 @@ knn_status knn_mix_rrc(const int32_t *nbr_ids, const float *nbr_dists, const int
                        int64_t B, int64_t V, int64_t S, int32_t r, float mu, float alpha, float tau,
                        float *lambda_out, float *p_m, void *stream);
 
+/*
+ * knn_stream_read -- a measurement aid, not a step of the method: one plain
+ * read of `bytes` bytes of device memory at `buf` (16-byte aligned, a multiple
+ * of 16 bytes) with the same 16-byte non-temporal loads the distance stage
+ * streams keys with, over a fixed grid of 2048 workgroups.  Its duration is
+ * the HBM read ceiling the distance stage's key streaming is compared with.
+ * `sink` is a device word that is written only with negligible probability
+ * (it keeps the loads from being optimised away).
+ */
+knn_status knn_stream_read(const void *buf, size_t bytes, uint32_t *sink, void *stream);
+
 /* Static text for a status code. */
 const char *knn_status_string(knn_status status);
 

@@ -19,7 +19,8 @@ from . import _lib
 from ._lib import DTYPES, PARTS, KnnError, load, status_string  # noqa: F401
 
 __all__ = ["MixtureProblem", "mixture", "mixture_noalloc", "distances", "key_sqnorms", "mix", "mix_rrc",
-           "spec_verify", "mask_words", "workspace_size", "KnnError", "load", "status_string", "abi_version"]
+           "spec_verify", "mask_words", "stream_read", "workspace_size", "KnnError", "load", "status_string",
+           "abi_version"]
 
 _TORCH_DTYPES = {torch.float32: "f32", torch.bfloat16: "bf16", torch.float16: "f16"}
 
@@ -267,6 +268,15 @@ def mix_rrc(ids, dists, values, key_offsets, query_offsets, p_lm, mu, alpha, tau
                             _stream(None))
     _lib.check("knn_mix_rrc", st)
     return out, lam
+
+
+def stream_read(buf: torch.Tensor, sink: torch.Tensor, stream=None):
+    """knn_stream_read: one plain read of a contiguous device tensor (a measurement aid: the HBM
+    read ceiling the distance stage is compared with); sink is a 1-element int32 device tensor."""
+    _need(buf.is_cuda and buf.is_contiguous(), "buf: contiguous device tensor")
+    _need(sink.is_cuda and sink.dtype == torch.int32 and sink.numel() >= 1, "sink: int32 device tensor")
+    _lib.check("knn_stream_read", load().knn_stream_read(_ptr(buf), buf.numel() * buf.element_size(), _ptr(sink),
+                                                          _stream(stream)))
 
 
 def mask_words(masked_rows, total_keys: int, device) -> torch.Tensor:

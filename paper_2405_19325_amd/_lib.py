@@ -44,6 +44,7 @@ SIGNATURES: Dict[str, tuple] = {
     "knn_key_sqnorms": (I, [P, I64, I64, I, P, P]),
     "knn_mix": (I, [P, P, P, P, P, P, I64, I64, I64, I32, F, F, P, P]),
     "knn_mix_rrc": (I, [P, P, P, P, P, P, I64, I64, I64, I32, F, F, F, P, P, P]),
+    "knn_stream_read": (I, [P, SZ, P, P]),
     "knn_status_string": (ctypes.c_char_p, [I]),
     "knn_abi_version": (I, []),
 }
