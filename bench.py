@@ -364,7 +364,7 @@ def time_config(name, steps, stream_gbs, with_oracle):
     topr_bytes = dist_bytes + B * spec.r * 8
     macs = int(np.sum(nq * nk)) * spec.d
     bufs = [w.keys]
-    if key_bytes < 2 * 256 * 2 ** 20:
+    if key_bytes <= 4 * 256 * 2 ** 20:  # within a few times the 256 MB last-level cache
         bufs.append(gen.second_key_copy(spec, seed, device=dev))
     hints = dict(key_offsets_host=ko, query_offsets_host=qo)
     probs = [knn.MixtureProblem(w.queries, k, w.values, w.key_offsets, w.query_offsets, w.p_lm, w.r, w.mu, w.lam,

@@ -319,7 +319,7 @@ knn_status knn_mix_rrc(const int32_t *nbr_ids, const float *nbr_dists, const int
  * knn_stream_read -- a measurement aid, not a step of the method: one plain
  * read of `bytes` bytes of device memory at `buf` (16-byte aligned, a multiple
  * of 16 bytes) with the same 16-byte non-temporal loads the distance stage
- * streams keys with, over a fixed grid of 2048 workgroups.  Its duration is
+ * streams keys with, by 2048 workgroups each reading one contiguous piece.  Its duration is
  * the HBM read ceiling the distance stage's key streaming is compared with.
  * `sink` is a device word that is written only with negligible probability
  * (it keeps the loads from being optimised away).

@@ -11,20 +11,25 @@ namespace {
 
 constexpr int kReadThreads = 256;
 constexpr int kReadBlocks = 2048;  // about eight workgroups per CU
-constexpr int kReadUnroll = 4;     // 16-byte loads in flight per lane
+constexpr int kReadUnroll = 8;     // 16-byte loads in flight per lane
 
+// Workgroup g reads the g-th of kReadBlocks contiguous pieces of the buffer
+// (measured on MI355X: contiguous pieces per workgroup read about 15% faster
+// than a grid-stride walk over the whole buffer).
 __global__ __launch_bounds__(kReadThreads) void k_stream_read(const u32x4_t *buf, int64_t n16, uint32_t *out) {
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * kReadThreads;
-    int64_t i = static_cast<int64_t>(blockIdx.x) * kReadThreads + threadIdx.x;
+    const int64_t per = (n16 + gridDim.x - 1) / gridDim.x;
+    const int64_t b0 = static_cast<int64_t>(blockIdx.x) * per;
+    const int64_t b1 = b0 + per < n16 ? b0 + per : n16;
+    int64_t i = b0 + threadIdx.x;
     uint32_t acc = 0u;
-    for (; i + (kReadUnroll - 1) * stride < n16; i += kReadUnroll * stride) {
+    for (; i + (kReadUnroll - 1) * kReadThreads < b1; i += kReadUnroll * kReadThreads) {
         u32x4_t v[kReadUnroll];
 #pragma unroll
-        for (int u = 0; u < kReadUnroll; ++u) v[u] = __builtin_nontemporal_load(buf + i + u * stride);
+        for (int u = 0; u < kReadUnroll; ++u) v[u] = __builtin_nontemporal_load(buf + i + u * kReadThreads);
 #pragma unroll
         for (int u = 0; u < kReadUnroll; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
     }
-    for (; i < n16; i += stride) {
+    for (; i < b1; i += kReadThreads) {
         const u32x4_t v = __builtin_nontemporal_load(buf + i);
         acc ^= v.x ^ v.y ^ v.z ^ v.w;
     }

@@ -30,8 +30,21 @@ struct Layout {
     int64_t tiles_per_set;
     int64_t ld;  // distance row stride = tiles_per_set * rows_per_tile
     int split_parts;  // > 0: the select runs split over parts, short rows or long (candidate lists and counts below)
-    size_t off_dist, off_tmin, off_tmax, off_cand, off_count, off_thr, off_best, off_ticket, total;
+    // The fused select (128-query batches on long rows): candidates listed by the
+    // distance kernel from a threshold sampled per query; the distance matrix is
+    // written only when the sample misjudges a query (the fallback word).
+    bool fused;
+    int sample_rows, sample_every;
+    size_t off_dist, off_tmin, off_tmax, off_cand, off_count, off_thr, off_best, off_ticket, off_fallback, total;
 };
+
+// Whether a batch takes the fused select: the 128-query matrix-core kernel
+// (more than 64 queries on a set) on rows long enough for the wide select.
+bool fused_shape(int64_t B, int64_t d, knn_dtype dtype, int64_t max_queries, int64_t ld, int32_t r,
+                 int64_t tiles_per_set) {
+    return mfma_shape(d, dtype, max_queries) && max_queries > 64 && r <= kSplitMaxR &&
+           select_split_parts(B, ld, r) == 0 && select_wide_parts(B, ld, r, tiles_per_set) > 0;
+}
 
 Layout layout(int64_t B, int64_t d, int64_t S, int64_t max_keys, int64_t max_queries, knn_dtype dtype, int32_t r) {
     Layout L{};
@@ -51,7 +64,14 @@ Layout layout(int64_t B, int64_t d, int64_t S, int64_t max_keys, int64_t max_que
     const size_t per_row = L.split_parts > 0 ? static_cast<size_t>(B) : 0;  // split or wide: thresholds, NEST words
     L.off_best = align_up(L.off_thr + sizeof(uint32_t) * per_row);
     L.off_ticket = align_up(L.off_best + sizeof(uint64_t) * per_row);
-    L.total = align_up(L.off_ticket + sizeof(uint32_t) * per_row);
+    L.off_fallback = align_up(L.off_ticket + sizeof(uint32_t) * per_row);
+    L.fused = fused_shape(B, d, dtype, max_queries, L.ld, r, L.tiles_per_set);
+    // The sample: the first sample_rows rows (whole 256-key passes) of every
+    // sample_every-th tile, 1/32 of the keys, in pieces small enough that the
+    // sample launch fills the chip.
+    L.sample_rows = L.rows_per_tile / 8 > 256 ? L.rows_per_tile / 8 : 256;
+    L.sample_every = 32 * L.sample_rows / L.rows_per_tile > 1 ? 32 * L.sample_rows / L.rows_per_tile : 1;
+    L.total = align_up(L.off_fallback + (L.fused ? sizeof(uint32_t) : 0));
     return L;
 }
 
@@ -175,15 +195,48 @@ MixArgs mix_args(const Call &c) {
     return a;
 }
 
+// The select stage's view of the workspace.
+SelectArgs select_args(const Call &c, const Layout &L, char *ws) {
+    SelectArgs a{};
+    a.dist = ws ? reinterpret_cast<float *>(ws + L.off_dist) : nullptr;
+    a.tile_min = ws ? reinterpret_cast<float *>(ws + L.off_tmin) : nullptr;
+    a.tile_max = ws ? reinterpret_cast<float *>(ws + L.off_tmax) : nullptr;
+    a.key_offsets = c.key_offsets;
+    a.query_offsets = c.query_offsets;
+    a.S = c.S;
+    a.ld = L.ld;
+    a.tiles_per_set = L.tiles_per_set;
+    a.rows_per_tile = L.rows_per_tile;
+    a.r = c.r;
+    a.ids = c.nbr_ids;
+    a.dists = c.nbr_dists;
+    uint32_t *part_count = (ws && L.split_parts > 0) ? reinterpret_cast<uint32_t *>(ws + L.off_count) : nullptr;
+    a.cand = (ws && L.split_parts > 0) ? reinterpret_cast<uint64_t *>(ws + L.off_cand) : nullptr;
+    a.part_count = part_count;
+    a.part_min = part_count ? part_count + L.split_parts * c.B : nullptr;
+    a.part_thr = (ws && L.split_parts > 0) ? reinterpret_cast<uint32_t *>(ws + L.off_thr) : nullptr;
+    return a;
+}
+
+// The fused select's lists share the wide select's candidate region (one list
+// of kFusedCap per query; the wide select runs on it only after a fallback).
+FusedArgs fused_args(const Layout &L, char *ws) {
+    FusedArgs f{};
+    f.sample_rows = L.sample_rows;
+    f.sample_every = L.sample_every;
+    f.list = reinterpret_cast<uint64_t *>(ws + L.off_cand);
+    f.count = reinterpret_cast<uint32_t *>(ws + L.off_count);
+    f.thr = reinterpret_cast<uint32_t *>(ws + L.off_thr);
+    f.fallback = reinterpret_cast<uint32_t *>(ws + L.off_fallback);
+    return f;
+}
+
 knn_status run_part(const Call &c, int part, hipStream_t stream) {
     const Layout L = layout(c.B, c.d, c.S, c.max_keys, c.max_queries, c.dtype, c.r);
     char *ws = static_cast<char *>(c.workspace);
     float *dist = ws ? reinterpret_cast<float *>(ws + L.off_dist) : nullptr;
     float *tmin = ws ? reinterpret_cast<float *>(ws + L.off_tmin) : nullptr;
     float *tmax = ws ? reinterpret_cast<float *>(ws + L.off_tmax) : nullptr;
-    uint64_t *cand = (ws && L.split_parts > 0) ? reinterpret_cast<uint64_t *>(ws + L.off_cand) : nullptr;
-    uint32_t *part_count = (ws && L.split_parts > 0) ? reinterpret_cast<uint32_t *>(ws + L.off_count) : nullptr;
-    uint32_t *part_thr = (ws && L.split_parts > 0) ? reinterpret_cast<uint32_t *>(ws + L.off_thr) : nullptr;
     if (part == KNN_PART_DISTANCES) {
         DistPlan p = plan_distances(c.d, c.dtype, c.max_queries, c.queries, c.keys);
         p.rows_per_tile = L.rows_per_tile;
@@ -202,26 +255,42 @@ knn_status run_part(const Call &c, int part, hipStream_t stream) {
         a.tiles_per_set = L.tiles_per_set;
         a.rows_per_tile = L.rows_per_tile;
         a.key_mask = c.key_mask;
-        return status_of(launch_distances(p, c.dtype, a, c.S, stream));
+        if (!L.fused) return status_of(launch_distances(p, c.dtype, a, c.S, stream));
+        uint32_t *fallback = reinterpret_cast<uint32_t *>(ws + L.off_fallback);
+        if (!(p.mfma && p.mq == 8)) {  // (misaligned rows) the whole matrix, selected by the wide select
+            knn_status st = status_of(launch_distances(p, c.dtype, a, c.S, stream));
+            return st != KNN_OK ? st : status_of(launch_set_word(fallback, 1u, stream));
+        }
+        // The sample pieces' distances, each query's threshold and the sample's
+        // candidates, the rest of the rows listing candidates only, the count
+        // check, and (only if a query's count is off) the whole matrix.
+        const FusedArgs f = fused_args(L, ws);
+        a.sample_rows = L.sample_rows;
+        a.sample_every = L.sample_every;
+        a.cand_thr = f.thr;
+        a.cand_count = f.count;
+        a.cand_list = f.list;
+        a.fallback = f.fallback;
+        const SelectArgs sa = select_args(c, L, ws);
+        hipError_t e = launch_distances_mfma(p.mq, c.dtype, a, c.S, p.groups, stream, 1);
+        if (e == hipSuccess) e = launch_fused_threshold(sa, f, c.B, stream);
+        if (e == hipSuccess) e = launch_distances_mfma(p.mq, c.dtype, a, c.S, p.groups, stream, 2);
+        if (e == hipSuccess) e = launch_fused_check(sa, f, c.B, stream);
+        if (e == hipSuccess) {
+            a.gate = fallback;
+            a.gate_run = 1u;
+            e = launch_distances_mfma(p.mq, c.dtype, a, c.S, p.groups, stream, 0);
+        }
+        return status_of(e);
     }
     if (part == KNN_PART_SELECT || part == KNN_PART_SELECT_MIX) {
-        SelectArgs a{};
-        a.dist = dist;
-        a.tile_min = tmin;
-        a.tile_max = tmax;
-        a.key_offsets = c.key_offsets;
-        a.query_offsets = c.query_offsets;
-        a.S = c.S;
-        a.ld = L.ld;
-        a.tiles_per_set = L.tiles_per_set;
-        a.rows_per_tile = L.rows_per_tile;
-        a.r = c.r;
-        a.ids = c.nbr_ids;
-        a.dists = c.nbr_dists;
-        a.cand = cand;
-        a.part_count = part_count;
-        a.part_min = part_count ? part_count + L.split_parts * c.B : nullptr;
-        a.part_thr = part_thr;
+        const SelectArgs a = select_args(c, L, ws);
+        if (L.fused) {
+            const FusedArgs f = fused_args(L, ws);
+            if (part == KNN_PART_SELECT) return status_of(launch_select_fused(a, nullptr, f, c.B, stream));
+            const MixArgs mx = mix_args(c);
+            return status_of(launch_select_fused(a, &mx, f, c.B, stream));
+        }
         if (part == KNN_PART_SELECT) return status_of(launch_select(a, c.B, stream));
         MixArgs mx = mix_args(c);
         if (ws && L.split_parts > 0) {

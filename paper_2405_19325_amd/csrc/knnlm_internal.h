@@ -46,7 +46,20 @@ struct DistArgs {
     int64_t tiles_per_set;
     int rows_per_tile;
     const uint32_t *key_mask;    // bit (i & 31) of word i >> 5 set: global key row i is masked; or null
+    // Gate: unless null, the launch does nothing when *gate != gate_run.
+    const uint32_t *gate;
+    uint32_t gate_run;
+    // The fused select of query batches on long rows (launch_distances_fused):
+    int sample_rows;             // rows of a sample piece, a multiple of 256
+    int sample_every;            // tiles t with t % sample_every == 0 start with a sample piece
+    const uint32_t *cand_thr;    // [B] a key is a candidate of query b when its distance bits are below this
+    uint32_t *cand_count;        // [B] candidates listed so far
+    uint64_t *cand_list;         // [B, kFusedCap] (distance bits << 32 | local key index)
+    uint32_t *fallback;          // set to 1 when a candidate cannot be kept
 };
+
+// Candidates per query of the fused select (the wide select's list capacity).
+constexpr int kFusedCap = 4096;
 
 // A masked key row is at distance +infinity (bits kMaskedBits), above every
 // real distance, and stays out of the per-tile extrema.
@@ -69,8 +82,11 @@ int dist_tile_rows(int64_t d, knn_dtype dtype, int64_t S, int64_t max_keys, int6
 
 hipError_t launch_distances(const DistPlan &plan, knn_dtype dtype, const DistArgs &args, int64_t S,
                             hipStream_t stream);
+// fm: 0 every tile, distances written; 1 the sample pieces only, distances
+// written; 2 every row outside the sample pieces, candidates listed instead of
+// distances written (mq 8 only).
 hipError_t launch_distances_mfma(int mq, knn_dtype dtype, const DistArgs &args, int64_t S, int64_t groups,
-                                 hipStream_t stream);
+                                 hipStream_t stream, int fm = 0);
 hipError_t launch_key_sqnorms(const void *keys, int64_t n, int64_t d, knn_dtype dtype, float *out,
                               hipStream_t stream);
 }  // namespace knnlm

@@ -100,7 +100,15 @@ __device__ __forceinline__ int swz(int n, int c) { return n * CH + (c ^ (n & (CH
 // 128-query workgroups take 256-key passes of 64-element spans (the same
 // matrix-core work per step as 128 keys x 128 elements, with a quarter less
 // loaded and written to LDS per step, a third less read from it).
-template <knn_dtype DT, int MQ, int WK, int WQ, int NS, bool NORMS, int PK, int SPAN>
+//
+// FM (the fused select of query batches on long rows): 0 every tile, the
+// distances written; 1 only the sample pieces (the first sample_rows rows of
+// every sample_every-th tile), the distances written; 2 every row outside the
+// sample pieces, and instead of the distances each query's candidates -- keys
+// whose distance bits are below the query's threshold -- are staged in LDS
+// and appended to the query's list once the tile is done (the list's count is
+// true even past its capacity; a full LDS stage sets the fallback word).
+template <knn_dtype DT, int MQ, int WK, int WQ, int NS, bool NORMS, int PK, int SPAN, int FM = 0>
 __global__ __launch_bounds__(WK * WQ * kWave, 1) void k_dist_mfma(DistArgs a, int64_t n_tiles, int64_t groups) {
     constexpr int QW = WQ;
     constexpr int kChunks = SPAN * 2 / 16;               // 16-byte chunks per row and span
@@ -118,7 +126,15 @@ __global__ __launch_bounds__(WK * WQ * kWave, 1) void k_dist_mfma(DistArgs a, in
     __shared__ __align__(16) u32x4_t klds[2][PK * kChunks];
     __shared__ __align__(16) u32x4_t qlds[2][QB * kChunks];
     __shared__ uint32_t smin[QB], smax[QB];
+    constexpr int kStage = FM == 2 ? 1024 : 1;  // candidates staged per tile (about 120 at 128 x 4096 keys)
+    __shared__ uint64_t stage_key[kStage];
+    __shared__ uint8_t stage_q[kStage];
+    __shared__ uint32_t stage_n;
+    static_assert(FM != 2 || QB <= 256, "a staged query fits a byte");
 
+    if constexpr (FM == 0) {
+        if (a.gate != nullptr && *a.gate != a.gate_run) return;
+    }
     // Consecutive workgroups land on different XCDs (round robin over 8).  The
     // query groups of one key tile are numbered 8 apart, so they run on one XCD
     // at about the same time and all but the first read the tile from its L2.
@@ -127,17 +143,22 @@ __global__ __launch_bounds__(WK * WQ * kWave, 1) void k_dist_mfma(DistArgs a, in
     const int64_t tl = ((L >> 3) / groups) * 8 + (L & 7);
     if (tl >= n_tiles) return;
     const int64_t tiles = a.tiles_per_set;
-    const int64_t s = tl / tiles;
-    const int64_t tile = tl - s * tiles;
+    const int64_t se = FM == 0 ? 1 : a.sample_every;
+    const int64_t per_set = FM == 1 ? (tiles + se - 1) / se : tiles;  // tiles (sample pieces) per set
+    const int64_t s = tl / per_set;
+    const int64_t tile = FM == 1 ? (tl - s * per_set) * se : tl - s * per_set;
     const int64_t k0 = a.key_offsets[s];
     int64_t N = a.key_offsets[s + 1] - k0;
     if (N > a.ld) N = a.ld;
     const int64_t qb = a.query_offsets[s] + grp * QB;
     const int64_t qe = a.query_offsets[s + 1];
-    const int64_t r0 = tile * a.rows_per_tile;
+    // this workgroup's rows [r0, r1): the tile, its sample piece (FM 1), or the tile past its piece (FM 2)
+    int64_t r0 = tile * a.rows_per_tile;
+    const int64_t rend = r0 + (FM == 1 ? a.sample_rows : a.rows_per_tile);
+    if (FM == 2 && tile % se == 0) r0 += a.sample_rows;
     if (qb >= qe || r0 >= N) return;  // uniform over the block
     const int nq = static_cast<int>(qe - qb < QB ? qe - qb : QB);
-    const int64_t r1 = (r0 + a.rows_per_tile < N) ? r0 + a.rows_per_tile : N;
+    const int64_t r1 = rend < N ? rend : N;
 
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
@@ -154,6 +175,14 @@ __global__ __launch_bounds__(WK * WQ * kWave, 1) void k_dist_mfma(DistArgs a, in
     for (int q = tid; q < QB; q += kThreads) {
         smin[q] = 0xffffffffu;
         smax[q] = 0u;
+    }
+    if (FM == 2 && tid == 0) stage_n = 0u;
+    // FM 2: the thresholds of this lane's query rows (jq + j) * 16 + lr (0 past the group: nothing passes)
+    uint32_t thr_l[MQW];
+#pragma unroll
+    for (int j = 0; j < MQW; ++j) {
+        const int q = (jq + j) * 16 + lr;
+        thr_l[j] = (FM == 2 && q < nq) ? a.cand_thr[qb + q] : 0u;
     }
 
     // Loads: chunk i of this thread is row i * R + tid / kChunks of the pass
@@ -255,6 +284,45 @@ __global__ __launch_bounds__(WK * WQ * kWave, 1) void k_dist_mfma(DistArgs a, in
             kk[kb] = NORMS ? (row < r1 ? a.key_sqnorms[k0 + row] : 0.0f) : group4_sum(kkp[kb]);
             mk[kb] = a.key_mask != nullptr && row < r1 && key_masked(a.key_mask, k0 + row);
         }
+        if constexpr (FM == 2) {
+            // candidates: distance bits below the query's threshold, appended to
+            // the LDS stage a wave at a time (one LDS atomic per wave that has any)
+#pragma unroll
+            for (int j = 0; j < MQW; ++j) {
+                const float qsum = group4_sum(qqp[j]);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int q = (jq + j) * 16 + g * 4 + i;
+                    const float qn = __shfl(qsum, g * 4 + i);
+                    const uint32_t th = __shfl(thr_l[j], g * 4 + i);
+#pragma unroll
+                    for (int kb = 0; kb < KBW; ++kb) {
+                        const int64_t row = c0 + (wave * KBW + kb) * 16 + lr;
+                        const float dist = mk[kb] ? __uint_as_float(kMaskedBits)
+                                                  : clamp_nonneg(fmaf(-2.0f, acc[j][kb][i], qn + kk[kb]));
+                        const bool c = q < nq && row < r1 && __float_as_uint(dist) < th;
+                        const uint64_t bal = __ballot(c);
+                        if (bal != 0ull) {
+                            const int first = __ffsll(static_cast<unsigned long long>(bal)) - 1;
+                            uint32_t base = 0u;
+                            if (lane == first) base = atomicAdd(&stage_n, static_cast<uint32_t>(__popcll(bal)));
+                            base = readlane_u32(base, first);
+                            if (c) {
+                                const uint32_t p = base + static_cast<uint32_t>(
+                                                              __popcll(bal & ((1ull << lane) - 1ull)));
+                                if (p < static_cast<uint32_t>(kStage)) {
+                                    stage_key[p] = (static_cast<uint64_t>(__float_as_uint(dist)) << 32) |
+                                                   static_cast<uint32_t>(row);
+                                    stage_q[p] = static_cast<uint8_t>(q);
+                                }
+                            }
+                        }
+                    }
+                }
+            }
+            clear();
+            return;
+        }
         // the pass's extrema of each query fold into the tile's (LDS atomics) here,
         // so that no per-lane extrema stay live through the main loop
 #pragma unroll
@@ -319,6 +387,19 @@ __global__ __launch_bounds__(WK * WQ * kWave, 1) void k_dist_mfma(DistArgs a, in
         }
     }
 
+    if constexpr (FM == 2) {
+        // the staged candidates to their queries' lists (no loads are in flight any more)
+        __syncthreads();
+        const uint32_t n = stage_n;
+        if (n > static_cast<uint32_t>(kStage) && tid == 0) *a.fallback = 1u;
+        const uint32_t m = n < static_cast<uint32_t>(kStage) ? n : static_cast<uint32_t>(kStage);
+        for (uint32_t e = tid; e < m; e += kThreads) {
+            const int64_t qq = qb + stage_q[e];
+            const uint32_t pos = atomicAdd(a.cand_count + qq, 1u);
+            if (pos < static_cast<uint32_t>(kFusedCap)) a.cand_list[qq * kFusedCap + pos] = stage_key[e];
+        }
+        return;
+    }
     // the tile's extrema of each query (folded in by every pass's epilogue)
     if (a.tile_min != nullptr) {
         __syncthreads();
@@ -330,8 +411,17 @@ __global__ __launch_bounds__(WK * WQ * kWave, 1) void k_dist_mfma(DistArgs a, in
 }
 
 template <knn_dtype DT, bool NORMS>
-hipError_t launch_mq(int mq, const DistArgs &a, int64_t n_tiles, int64_t groups, dim3 grid, hipStream_t st) {
+hipError_t launch_mq(int mq, const DistArgs &a, int64_t n_tiles, int64_t groups, dim3 grid, hipStream_t st,
+                     int fm) {
     const dim3 b4(4 * kWave), b8(8 * kWave);
+    if (fm != 0) {  // the fused select: 128-query workgroups only
+        if (mq != 8) return hipErrorInvalidValue;
+        if (fm == 1)
+            hipLaunchKernelGGL((k_dist_mfma<DT, 8, 4, 2, 2, NORMS, 256, 64, 1>), grid, b8, 0, st, a, n_tiles, groups);
+        else
+            hipLaunchKernelGGL((k_dist_mfma<DT, 8, 4, 2, 2, NORMS, 256, 64, 2>), grid, b8, 0, st, a, n_tiles, groups);
+        return hipGetLastError();
+    }
     switch (mq) {
     case 1: hipLaunchKernelGGL((k_dist_mfma<DT, 1, 4, 1, 4, NORMS, 128, 128>), grid, b4, 0, st, a, n_tiles, groups); break;
     case 2: hipLaunchKernelGGL((k_dist_mfma<DT, 2, 4, 1, 3, NORMS, 128, 128>), grid, b4, 0, st, a, n_tiles, groups); break;
@@ -343,9 +433,9 @@ hipError_t launch_mq(int mq, const DistArgs &a, int64_t n_tiles, int64_t groups,
 }
 
 template <knn_dtype DT>
-hipError_t launch_dt(int mq, const DistArgs &a, int64_t n_tiles, int64_t groups, dim3 grid, hipStream_t st) {
-    return a.key_sqnorms != nullptr ? launch_mq<DT, true>(mq, a, n_tiles, groups, grid, st)
-                                    : launch_mq<DT, false>(mq, a, n_tiles, groups, grid, st);
+hipError_t launch_dt(int mq, const DistArgs &a, int64_t n_tiles, int64_t groups, dim3 grid, hipStream_t st, int fm) {
+    return a.key_sqnorms != nullptr ? launch_mq<DT, true>(mq, a, n_tiles, groups, grid, st, fm)
+                                    : launch_mq<DT, false>(mq, a, n_tiles, groups, grid, st, fm);
 }
 
 }  // namespace
@@ -363,15 +453,23 @@ int mfma_tile_rows(int64_t d) {
 }
 
 hipError_t launch_distances_mfma(int mq, knn_dtype dtype, const DistArgs &args, int64_t S, int64_t groups,
-                                 hipStream_t stream) {
-    const int64_t n_tiles = S * args.tiles_per_set;
+                                 hipStream_t stream, int fm) {
     if (groups < 1 || args.rows_per_tile % kTileQuantum != 0 || args.d % kSpan != 0) return hipErrorInvalidConfiguration;
+    if (fm != 0 && (args.sample_every < 1 || args.sample_rows < kTileQuantum || args.sample_rows % kTileQuantum != 0 ||
+                    args.sample_rows > args.rows_per_tile))
+        return hipErrorInvalidConfiguration;
+    if (fm == 2 && (args.cand_thr == nullptr || args.cand_count == nullptr || args.cand_list == nullptr ||
+                    args.fallback == nullptr))
+        return hipErrorInvalidValue;
+    const int64_t per_set = fm == 1 ? (args.tiles_per_set + args.sample_every - 1) / args.sample_every
+                                    : args.tiles_per_set;
+    const int64_t n_tiles = S * per_set;
     const int64_t nblocks = (n_tiles + 7) / 8 * 8 * groups;
     if (nblocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
     const dim3 grid(static_cast<unsigned>(nblocks));
     switch (dtype) {
-    case KNN_BF16: return launch_dt<KNN_BF16>(mq, args, n_tiles, groups, grid, stream);
-    case KNN_F16: return launch_dt<KNN_F16>(mq, args, n_tiles, groups, grid, stream);
+    case KNN_BF16: return launch_dt<KNN_BF16>(mq, args, n_tiles, groups, grid, stream, fm);
+    case KNN_F16: return launch_dt<KNN_F16>(mq, args, n_tiles, groups, grid, stream, fm);
     default: return hipErrorInvalidValue;
     }
 }

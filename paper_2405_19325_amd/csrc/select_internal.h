@@ -22,6 +22,22 @@ struct SelectArgs {
     uint32_t *part_count;        // split select: [B, parts] candidates per part
     uint32_t *part_min;          // split select: [B, parts] smallest candidate distance bits per part
     uint32_t *part_thr;          // split select: [B] threshold on the distance bits
+    // Gate: unless null, a wide-select launch does nothing when *gate != gate_run.
+    const uint32_t *gate;
+    uint32_t gate_run;
+};
+
+// The fused select of query batches on long rows (the 128-query matrix-core
+// distance kernel): a threshold per query from sampled keys, candidates
+// listed by the distance kernel itself, so that the distance matrix is
+// written only when the sample misjudges a query (the fallback word).
+struct FusedArgs {
+    int sample_rows;     // the first sample_rows rows of every sample_every-th tile are the sample
+    int sample_every;
+    uint32_t *thr;       // [B] threshold on the distance bits
+    uint32_t *count;     // [B] candidates listed (true even past kFusedCap)
+    uint64_t *list;      // [B, kFusedCap] (distance bits << 32 | local key index)
+    uint32_t *fallback;  // 0: the lists hold every query's pi; 1: the distance matrix is written and selected
 };
 
 struct MixArgs {
@@ -80,5 +96,17 @@ int select_wide_parts(int64_t B, int64_t ld, int r, int64_t tiles_per_set);
 hipError_t launch_select(const SelectArgs &args, int64_t B, hipStream_t stream);
 hipError_t launch_select_mix(const SelectArgs &args, const MixArgs &mix, int64_t B, hipStream_t stream);
 hipError_t launch_mix(const MixArgs &args, int64_t B, hipStream_t stream);
+// Fused select, after the sample pieces' distances (launch_distances_mfma fm 1):
+// each query's threshold and the sample's candidates; clears the fallback word.
+hipError_t launch_fused_threshold(const SelectArgs &args, const FusedArgs &f, int64_t B, hipStream_t stream);
+// After the filter launch (fm 2): the fallback word is set if any query's
+// candidate count lies outside [min(r, N), kFusedCap].
+hipError_t launch_fused_check(const SelectArgs &args, const FusedArgs &f, int64_t B, hipStream_t stream);
+// Select (and mixture) after the fused distance stage: from the lists when the
+// fallback word is 0, else by the wide select over the distance matrix.
+hipError_t launch_select_fused(const SelectArgs &args, const MixArgs *mix, const FusedArgs &f, int64_t B,
+                               hipStream_t stream);
+// Stores v into *word (a one-thread kernel, so that graph capture records no memset).
+hipError_t launch_set_word(uint32_t *word, uint32_t v, hipStream_t stream);
 
 }  // namespace knnlm

@@ -1384,6 +1384,7 @@ __global__ __launch_bounds__(kT) void k_select_wide_parts(SelectArgs a, int part
     __shared__ __align__(16) uint32_t hist[kSelectBins];
     __shared__ uint32_t qtile[kT];  // tiles of the current chunk with keys below the threshold
     __shared__ Shared sh;
+    if (a.gate != nullptr && *a.gate != a.gate_run) return;
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
     const int64_t b = blockIdx.x / parts;
@@ -1517,6 +1518,7 @@ __global__ __launch_bounds__(kT) void k_select_wide_finish(SelectArgs a, MixArgs
     __shared__ uint32_t part_off[kWave + 1];
     static_assert(kVocabTile * 4 <= kWideCap * 8, "the vocabulary tile fits over the sort scratch");
     float *acc = reinterpret_cast<float *>(tmp);
+    if (a.gate != nullptr && *a.gate != a.gate_run) return;
 
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
@@ -1598,6 +1600,203 @@ __global__ __launch_bounds__(kT) void k_select_wide_finish(SelectArgs a, MixArgs
         float4 pre[kVocabTile / 4 / kT];
         mix_row<kPer, kVocabTile, MODE == kMixNest, false>(wj, tok, nkey, z, lam, m, b, acc, pre, dtok);
     }
+}
+
+// Fused select (query batches on long rows), threshold kernel: one workgroup
+// per query.  The sample is the first sample_rows rows of every
+// sample_every-th distance tile of the query's row, whose distances (and the
+// tiles' extrema over them) the distance stage has written.  The threshold is
+// the end of the histogram bin (2048 bins) holding the ks-th smallest sampled
+// distance, ks = k0 + ceil(4 sqrt(k0)) + 4 with k0 = ceil(r M / N) for M
+// sampled keys of N: about r + 4 standard deviations of keys of random data
+// lie below it.  The histogram's range ends at the ks-th smallest of the
+// pieces' minima when there are enough pieces (ks pieces, so at least ks
+// sampled keys, lie at or below it), so only the sample's low end is counted.
+// The sample's own keys below the threshold start the query's list; thread 0
+// of query 0 clears the fallback word.  Masked keys (+infinity) stay out.
+constexpr int kFusedU = 4;  // 16-byte loads per thread per step over the sample
+
+__global__ __launch_bounds__(kT) void k_fused_threshold(SelectArgs a, FusedArgs f) {
+    __shared__ __align__(16) uint32_t hist[kSelectBins];
+    __shared__ uint32_t pmin[kT];  // the pieces' minima (up to kT pieces)
+    __shared__ Shared sh;
+    const int tid = threadIdx.x;
+    const int lane = tid & (kWave - 1);
+    const int64_t b = blockIdx.x;
+    if (b == 0 && tid == 0) *f.fallback = 0u;
+    if (tid == 0) sh.ccount = 0u;
+    const int64_t s = set_of_query(a.query_offsets, a.S, b);
+    const int64_t k0 = a.key_offsets[s];
+    int64_t N = a.key_offsets[s + 1] - k0;
+    if (N > a.ld) N = a.ld;
+    const uint32_t r_eff = static_cast<uint32_t>(N < a.r ? N : a.r);
+    const int64_t R = a.rows_per_tile, sp = f.sample_rows, se = f.sample_every;
+    const int64_t ntiles = (N + R - 1) / R;
+    const int64_t npieces = (ntiles + se - 1) / se;
+    const float *drow = a.dist + b * a.ld;
+    const float *tmin = a.tile_min + b * a.tiles_per_set;
+    // piece p: rows [p se R, p se R + rows_p), rows_p = sp but for the last piece
+    const int64_t last0 = (npieces - 1) * se * R;
+    const int64_t last_rows = N - last0 < sp ? N - last0 : sp;
+    const int64_t M = npieces > 0 ? (npieces - 1) * sp + last_rows : 0;  // sampled keys
+    const int64_t slots_pp = sp / 4;                                     // 16-byte slots per piece
+    const int64_t nslots = npieces * slots_pp;
+
+    // The sample's range: its pieces' minima (the tile extrema the distance stage wrote over them).
+    uint32_t lo = ~0u, hi = 0u;
+    for (int64_t p = tid; p < npieces; p += kT) {
+        const uint32_t v = __float_as_uint(tmin[p * se]);
+        lo = v < kMaskedBits ? min(lo, v) : lo;
+        if (p < kT) pmin[p] = v;  // an all-masked piece reads as 0xffffffff
+    }
+    const float k0f = ceilf(static_cast<float>(r_eff) * static_cast<float>(M) / static_cast<float>(N > 0 ? N : 1));
+    const uint32_t ks = static_cast<uint32_t>(k0f + ceilf(4.0f * sqrtf(k0f)) + 4.0f);
+    __syncthreads();
+    // the end of the range: the ks-th smallest piece minimum (rank by comparison), else +infinity
+    uint32_t hb = kMaskedBits;
+    if (npieces <= kT && static_cast<int64_t>(ks) <= npieces) {
+        if (tid < npieces) {
+            const uint32_t v = pmin[tid];
+            uint32_t rank = 0;
+            for (int64_t j = 0; j < npieces; ++j) {
+                const uint32_t u = pmin[j];
+                rank += (u < v || (u == v && j < tid)) ? 1u : 0u;
+            }
+            if (rank == ks - 1u && v < kMaskedBits) sh.hi = v;
+            if (rank == ks - 1u && v >= kMaskedBits) sh.hi = kMaskedBits - 1u;
+        }
+        __syncthreads();
+        hb = sh.hi;
+    } else {
+        hi = 0u;
+        for (int64_t p = tid; p < npieces; p += kT) {
+            const uint32_t v = __float_as_uint(a.tile_max[b * a.tiles_per_set + p * se]);
+            hi = v < kMaskedBits ? max(hi, v) : hi;
+        }
+    }
+    block_minmax_u32(lo, hi, sh);
+    if (hb != kMaskedBits) hi = hb;
+    // Step over the sample: kFusedU slots per thread; slot e is piece e / slots_pp, its 16 bytes
+    // at 4 (e % slots_pp) rows in (inside the tile, so inside the row's stride); past the
+    // sample a lane rereads the last slot and counts nothing.
+    auto step = [&](int64_t e0, uint4 (&v)[kFusedU], int64_t (&row)[kFusedU], int64_t (&lim)[kFusedU])
+        __attribute__((always_inline)) {
+#pragma unroll
+        for (int u = 0; u < kFusedU; ++u) {
+            const int64_t e = e0 + static_cast<int64_t>(u) * kT + tid;
+            const int64_t ec = e < nslots ? e : nslots - 1;
+            const int64_t p = ec / slots_pp;
+            row[u] = p * se * R + 4 * (ec - p * slots_pp);
+            const int64_t pend = p * se * R + (p == npieces - 1 ? last_rows : sp);
+            lim[u] = e < nslots ? pend : 0;  // elements at row + k < lim[u] are sampled
+            v[u] = *reinterpret_cast<const uint4 *>(drow + row[u]);
+        }
+    };
+    uint32_t thr = kMaskedBits;  // every unmasked key: too small a sample to judge
+    if (lo <= hi && static_cast<int64_t>(ks) < M) {
+        for (int i = tid; i < kSelectBins; i += kT) hist[i] = 0u;
+        __syncthreads();
+        const uint32_t w = hi + 1u - lo;
+        const int shift = range_shift(w);
+        for (int64_t e0 = 0; e0 < nslots; e0 += static_cast<int64_t>(kT) * kFusedU) {
+            uint4 v[kFusedU];
+            int64_t row[kFusedU], lim[kFusedU];
+            step(e0, v, row, lim);
+#pragma unroll
+            for (int u = 0; u < kFusedU; ++u)
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const uint32_t bits = lane_word(v[u], k);
+                    if (row[u] + k < lim[u] && bits - lo < w) atomicAdd(&hist[(bits - lo) >> shift], 1u);
+                }
+        }
+        __syncthreads();
+        if (tid < kWave) {
+            const uint32_t j = wave_pick_bin(hist, ks, lane);
+            const uint64_t end = static_cast<uint64_t>(lo) + ((static_cast<uint64_t>(j) + 1u) << shift);
+            if (lane == 0) sh.hi = j == ~0u ? kMaskedBits : static_cast<uint32_t>(end < hi + 1ull ? end : hi + 1ull);
+        }
+        __syncthreads();
+        thr = sh.hi;
+    }
+    // The sample's keys below the threshold: the start of the query's list.
+    uint64_t *list = f.list + b * static_cast<int64_t>(kFusedCap);
+    for (int64_t e0 = 0; e0 < nslots; e0 += static_cast<int64_t>(kT) * kFusedU) {
+        uint4 v[kFusedU];
+        int64_t row[kFusedU], lim[kFusedU];
+        step(e0, v, row, lim);
+        uint32_t c = 0;
+#pragma unroll
+        for (int u = 0; u < kFusedU; ++u)
+#pragma unroll
+            for (int k = 0; k < 4; ++k) c += (row[u] + k < lim[u] && lane_word(v[u], k) < thr) ? 1u : 0u;
+        const uint32_t incl = wave_incl_scan_u32(c, lane);
+        const uint32_t wtot = readlane_u32(incl, kWave - 1);
+        uint32_t wbase = 0u;
+        if (lane == 0 && wtot > 0) wbase = atomicAdd(&sh.ccount, wtot);
+        uint32_t pos = readlane_u32(wbase, 0) + incl - c;
+#pragma unroll
+        for (int u = 0; u < kFusedU; ++u)
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const uint32_t bits = lane_word(v[u], k);
+                if (row[u] + k < lim[u] && bits < thr) {
+                    if (pos < static_cast<uint32_t>(kFusedCap))
+                        list[pos] = sort_key(bits, static_cast<uint32_t>(row[u] + k));
+                    ++pos;
+                }
+            }
+    }
+    __syncthreads();
+    if (tid == 0) {
+        f.count[b] = sh.ccount;
+        f.thr[b] = thr;
+    }
+}
+
+// Fused select, check kernel (one workgroup): the fallback word is set when a
+// query's list holds fewer than min(r, N) or more than kFusedCap candidates.
+__global__ __launch_bounds__(kT) void k_fused_check(SelectArgs a, FusedArgs f, int64_t B) {
+    int bad = 0;
+    for (int64_t b = threadIdx.x; b < B; b += kT) {
+        const int64_t s = set_of_query(a.query_offsets, a.S, b);
+        int64_t N = a.key_offsets[s + 1] - a.key_offsets[s];
+        if (N > a.ld) N = a.ld;
+        const uint32_t r_eff = static_cast<uint32_t>(N < a.r ? N : a.r);
+        const uint32_t c = f.count[b];
+        bad |= (c < r_eff || c > static_cast<uint32_t>(kFusedCap)) ? 1 : 0;
+    }
+    if (__syncthreads_or(bad) && threadIdx.x == 0) *f.fallback = 1u;
+}
+
+__global__ void k_set_word(uint32_t *word, uint32_t v) {
+    if (threadIdx.x == 0) *word = v;
+}
+
+template <int MODE>
+hipError_t launch_sel_fused(const SelectArgs &a, const MixArgs &m, const FusedArgs &f, int64_t B, hipStream_t st) {
+    if (B < 1 || B > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+    const int wparts = select_wide_parts(B, a.ld, a.r, a.tiles_per_set);
+    if (wparts < 1 || a.tile_min == nullptr || a.tile_max == nullptr) return hipErrorInvalidValue;
+    const dim3 grid(static_cast<unsigned>(B)), block(kT);
+    // from the lists, unless the fallback word is set
+    SelectArgs lf = a;
+    lf.cand = f.list;
+    lf.part_count = f.count;
+    lf.part_thr = f.thr;
+    lf.gate = f.fallback;
+    lf.gate_run = 0u;
+    hipLaunchKernelGGL((k_select_wide_finish<MODE>), grid, block, 0, st, lf, m, 1);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    // otherwise the wide select over the distance matrix
+    SelectArgs lw = a;
+    lw.gate = f.fallback;
+    lw.gate_run = 1u;
+    hipLaunchKernelGGL(k_select_wide_parts, dim3(static_cast<unsigned>(B * wparts)), block, 0, st, lw, wparts);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL((k_select_wide_finish<MODE>), grid, block, 0, st, lw, m, wparts);
+    return hipGetLastError();
 }
 
 template <int MODE>
@@ -1682,6 +1881,40 @@ int select_capacity(int r) {
     int cap = 2 * p;
     if (cap < 2048) cap = 2048;
     return cap;  // <= 8192 for r <= KNNLM_MAX_R
+}
+
+hipError_t launch_fused_threshold(const SelectArgs &args, const FusedArgs &f, int64_t B, hipStream_t stream) {
+    if (B < 1 || B > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+    if (args.tile_min == nullptr || f.sample_rows < 4 || f.sample_rows % 4 != 0 || f.sample_rows > args.rows_per_tile ||
+        f.sample_every < 1)
+        return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_fused_threshold, dim3(static_cast<unsigned>(B)), dim3(kT), 0, stream, args, f);
+    return hipGetLastError();
+}
+
+hipError_t launch_fused_check(const SelectArgs &args, const FusedArgs &f, int64_t B, hipStream_t stream) {
+    hipLaunchKernelGGL(k_fused_check, dim3(1), dim3(kT), 0, stream, args, f, B);
+    return hipGetLastError();
+}
+
+hipError_t launch_select_fused(const SelectArgs &args, const MixArgs *mix, const FusedArgs &f, int64_t B,
+                               hipStream_t stream) {
+    if (mix == nullptr) {
+        MixArgs none{};
+        return launch_sel_fused<kNoMix>(args, none, f, B, stream);
+    }
+    if (mix->next_token != nullptr) {
+        if (!mix->rrc || mix->p_max == nullptr || mix->span_key == nullptr || mix->use_span == nullptr)
+            return hipErrorInvalidValue;
+        return launch_sel_fused<kMixNest>(args, *mix, f, B, stream);
+    }
+    return mix->rrc ? launch_sel_fused<kMixRrc>(args, *mix, f, B, stream)
+                    : launch_sel_fused<kMixFixed>(args, *mix, f, B, stream);
+}
+
+hipError_t launch_set_word(uint32_t *word, uint32_t v, hipStream_t stream) {
+    hipLaunchKernelGGL(k_set_word, dim3(1), dim3(kWave), 0, stream, word, v);
+    return hipGetLastError();
 }
 
 hipError_t launch_select(const SelectArgs &args, int64_t B, hipStream_t stream) {
