@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define KNNLM_ABI_VERSION 1
+#define KNNLM_ABI_VERSION 2
 
 /* Largest r accepted (the paper retrieves r = 1024, Appendix A). */
 #define KNNLM_MAX_R 4096
@@ -67,8 +67,24 @@ typedef enum {
     KNN_ERR_HIP = 5           /* a HIP launch failed */
 } knn_status;
 
-/* Element type of queries and keys. */
-typedef enum { KNN_F32 = 0, KNN_BF16 = 1, KNN_F16 = 2 } knn_dtype;
+/*
+ * Element type of queries and keys.  KNN_KEYS_PACKED, OR'ed into a 16-bit type
+ * (KNN_BF16_PACKED, KNN_F16_PACKED), says that `keys` is the packed copy of
+ * the key matrix written by knn_pack_keys rather than the row-major matrix;
+ * queries stay row-major.  Packed keys are read by the matrix-core distance
+ * kernels only, which serve calls with d % 128 == 0, d <= 65536 and
+ * max_queries_per_set >= 16 (and 16-byte aligned queries and keys); a call
+ * with packed keys outside that returns KNN_ERR_UNSUPPORTED.  Results are
+ * bit for bit those of the same call on the row-major keys.
+ */
+typedef enum {
+    KNN_F32 = 0,
+    KNN_BF16 = 1,
+    KNN_F16 = 2,
+    KNN_KEYS_PACKED = 0x100,
+    KNN_BF16_PACKED = 0x101,
+    KNN_F16_PACKED = 0x102
+} knn_dtype;
 
 /* Stages of knn_lm_mixture, runnable one at a time by knn_lm_mixture_part().
  * knn_lm_mixture itself runs KNN_PART_DISTANCES then KNN_PART_SELECT_MIX. */
@@ -288,6 +304,30 @@ knn_status knn_distances(const void *queries, const void *keys, const float *key
  */
 knn_status knn_key_sqnorms(const void *keys, int64_t n, int64_t d, knn_dtype dtype, float *out,
                            void *stream);
+
+/*
+ * knn_pack_keys -- the packed copy of a key matrix for query batches on the
+ * matrix cores.  Like knn_key_sqnorms it is computed once per key store (the
+ * store is built before decoding starts, paper Algorithm 1) and then passed as
+ * `keys` with dtype KNN_BF16_PACKED / KNN_F16_PACKED to every later call.
+ *
+ * Layout: the n x d row-major matrix `keys` (16-bit dtype, d % 128 == 0,
+ * d <= 65536) is cut into blocks of 16 consecutive rows (the last one padded
+ * with zero rows).  Block b, 32-element step c of d, occupies the 1024 bytes
+ * at byte offset (b * d / 32 + c) * 1024; its 16-byte chunk l (l = 0..63) holds
+ * elements 32 c + 8 (l / 16) .. 32 c + 8 (l / 16) + 7 of row 16 b + l % 16 --
+ * the B operand of one 16x16x32 matrix-core step for lane l.  `packed` must
+ * hold knn_packed_keys_bytes(n, d, dtype) bytes; both pointers 16-byte aligned
+ * device memory, not overlapping.  Key sets keep their row offsets: a set may
+ * start anywhere, not only on a block boundary.
+ * Errors: KNN_ERR_INVALID_ARG for null or misaligned pointers or n, d < 1;
+ * KNN_ERR_UNSUPPORTED for an fp32 dtype, d % 128 != 0 or d > 65536.
+ */
+knn_status knn_pack_keys(const void *keys, int64_t n, int64_t d, knn_dtype dtype, void *packed, void *stream);
+
+/* Bytes of the packed copy of n key rows of d elements: ceil(n / 16) * 16 * d * 2,
+ * or 0 where knn_pack_keys would refuse the sizes or dtype. */
+size_t knn_packed_keys_bytes(int64_t n, int64_t d, knn_dtype dtype);
 
 /*
  * knn_mix -- the softmax / scatter / mixture stage alone (eq. non-parametric

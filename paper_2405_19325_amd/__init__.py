@@ -16,11 +16,11 @@ import numpy as np
 import torch
 
 from . import _lib
-from ._lib import DTYPES, PARTS, KnnError, load, status_string  # noqa: F401
+from ._lib import DTYPES, KEYS_PACKED, PARTS, KnnError, load, status_string  # noqa: F401
 
-__all__ = ["MixtureProblem", "mixture", "mixture_noalloc", "distances", "key_sqnorms", "mix", "mix_rrc",
-           "spec_verify", "mask_words", "stream_read", "workspace_size", "KnnError", "load", "status_string",
-           "abi_version"]
+__all__ = ["MixtureProblem", "mixture", "mixture_noalloc", "distances", "key_sqnorms", "pack_keys",
+           "packed_keys_bytes", "mix", "mix_rrc", "spec_verify", "mask_words", "stream_read", "workspace_size",
+           "KnnError", "load", "status_string", "abi_version"]
 
 _TORCH_DTYPES = {torch.float32: "f32", torch.bfloat16: "bf16", torch.float16: "f16"}
 
@@ -62,14 +62,16 @@ class MixtureProblem:
     queries [B, d], keys [total_keys, d] (same dtype: f32/bf16/f16), values
     [total_keys] int32, key_offsets / query_offsets [S+1] int64, p_lm [B, V]
     fp32, all on one GPU.  The host copies of the offsets (derived once here
-    unless given) provide the planning hints.
+    unless given) provide the planning hints.  packed_keys, the packed copy of
+    `keys` from pack_keys(), makes the distance stage read that copy instead
+    (query batches on the matrix cores only; the results are the same bits).
     """
 
     def __init__(self, queries: torch.Tensor, keys: torch.Tensor, values: torch.Tensor,
                  key_offsets: torch.Tensor, query_offsets: torch.Tensor, p_lm: torch.Tensor, r: int,
                  mu: Optional[float] = None, lam: float = 0.3, key_sqnorms: Optional[torch.Tensor] = None,
                  key_offsets_host: Optional[Sequence[int]] = None,
-                 query_offsets_host: Optional[Sequence[int]] = None):
+                 query_offsets_host: Optional[Sequence[int]] = None, packed_keys: Optional[torch.Tensor] = None):
         _need(queries.dim() == 2 and keys.dim() == 2, "queries and keys must be 2-D")
         _need(queries.dtype == keys.dtype, "queries must carry the key element type")
         _need(queries.shape[1] == keys.shape[1], "queries and keys must have the same width")
@@ -96,6 +98,15 @@ class MixtureProblem:
         self.max_keys = int(nk.max())
         self.max_queries = int(nq.max())
         self.dtype = _dtype_code(queries)
+        self.packed_keys = packed_keys
+        self.keys_arg = keys  # what the distance stage reads
+        if packed_keys is not None:
+            want = packed_keys_bytes(self.total_keys, self.d, keys.dtype)
+            _need(packed_keys.is_cuda and packed_keys.is_contiguous() and
+                  packed_keys.numel() * packed_keys.element_size() == want,
+                  f"packed_keys: the {want}-byte packed copy of keys (pack_keys)")
+            self.keys_arg = packed_keys
+            self.dtype |= KEYS_PACKED
         self.r = int(r)
         self.mu = float(1.0 / math.sqrt(self.d) if mu is None else mu)
         self.lam = float(lam)
@@ -112,7 +123,7 @@ class MixtureProblem:
         self.lambdas = torch.empty(self.B, dtype=torch.float32, device=dev)  # lambda_t of run_rrc
 
     def _args(self, stream):
-        return (_ptr(self.queries), _ptr(self.keys), _ptr(self.key_sqnorms), _ptr(self.values),
+        return (_ptr(self.queries), _ptr(self.keys_arg), _ptr(self.key_sqnorms), _ptr(self.values),
                 _ptr(self.key_offsets), _ptr(self.query_offsets), _ptr(self.p_lm), self.B, self.d, self.V, self.S,
                 self.total_keys, self.min_keys, self.max_keys, self.max_queries, self.dtype, self.r, self.mu,
                 self.lam, _ptr(self.p_m), _ptr(self.ids), _ptr(self.dists), _ptr(self.workspace),
@@ -120,7 +131,7 @@ class MixtureProblem:
 
     def _validate(self, ws, ws_bytes):
         return load().knn_lm_mixture_validate(
-            _ptr(self.queries), _ptr(self.keys), _ptr(self.values), _ptr(self.key_offsets), _ptr(self.query_offsets),
+            _ptr(self.queries), _ptr(self.keys_arg), _ptr(self.values), _ptr(self.key_offsets), _ptr(self.query_offsets),
             _ptr(self.p_lm), self.B, self.d, self.V, self.S, self.total_keys, self.min_keys, self.max_keys,
             self.max_queries, self.dtype, self.r, self.mu, self.lam, 1, 1, 1, ws, ws_bytes)
 
@@ -133,7 +144,7 @@ class MixtureProblem:
         """One knn_lm_mixture_rrc call (lambda_t per query from relative retrieval
         confidence); returns (p_m, nbr_ids, nbr_dists, lambda_t [B]), valid after stream sync."""
         st = load().knn_lm_mixture_rrc(
-            _ptr(self.queries), _ptr(self.keys), _ptr(self.key_sqnorms), _ptr(self.values), _ptr(self.key_offsets),
+            _ptr(self.queries), _ptr(self.keys_arg), _ptr(self.key_sqnorms), _ptr(self.values), _ptr(self.key_offsets),
             _ptr(self.query_offsets), _ptr(self.p_lm), self.B, self.d, self.V, self.S, self.total_keys,
             self.min_keys, self.max_keys, self.max_queries, self.dtype, self.r, self.mu, float(alpha), float(tau),
             _ptr(self.lambdas), _ptr(self.p_m), _ptr(self.ids), _ptr(self.dists), _ptr(self.workspace),
@@ -161,7 +172,7 @@ class MixtureProblem:
             _need(draft_tokens.is_cuda and draft_tokens.dtype == torch.int32 and draft_tokens.numel() == self.B,
                   "draft_tokens: [B] int32 device tensor")
         st = load().knn_nest_step(
-            _ptr(self.queries), _ptr(self.keys), _ptr(self.key_sqnorms), _ptr(self.values), _ptr(self.key_offsets),
+            _ptr(self.queries), _ptr(self.keys_arg), _ptr(self.key_sqnorms), _ptr(self.values), _ptr(self.key_offsets),
             _ptr(self.query_offsets), _ptr(self.p_lm), self.B, self.d, self.V, self.S, self.total_keys,
             self.min_keys, self.max_keys, self.max_queries, self.dtype, self.r, self.mu, float(alpha), float(tau),
             float(delta), _ptr(key_mask), _ptr(draft_tokens), _ptr(self.lambdas), _ptr(self.p_m), _ptr(self.ids),
@@ -214,8 +225,9 @@ def mixture_noalloc(queries, keys, values, key_offsets, query_offsets, p_lm, r, 
 
 
 def distances(queries, keys, key_offsets, query_offsets, key_sqnorms=None, key_offsets_host=None,
-              query_offsets_host=None, ld: Optional[int] = None):
-    """knn_distances: squared distances [B, ld] of every query to its own set (entries past N_s untouched, NaN)."""
+              query_offsets_host=None, ld: Optional[int] = None, packed_keys: Optional[torch.Tensor] = None):
+    """knn_distances: squared distances [B, ld] of every query to its own set (entries past N_s untouched, NaN);
+    with packed_keys (pack_keys(keys)) the distance kernels read that copy."""
     ko = np.asarray(key_offsets_host if key_offsets_host is not None else key_offsets.cpu().numpy(), np.int64)
     qo = np.asarray(query_offsets_host if query_offsets_host is not None else query_offsets.cpu().numpy(), np.int64)
     B, d = queries.shape
@@ -223,9 +235,32 @@ def distances(queries, keys, key_offsets, query_offsets, key_sqnorms=None, key_o
     max_q = int(np.diff(qo).max())
     ld = max_keys if ld is None else ld
     out = torch.full((B, ld), float("nan"), dtype=torch.float32, device=queries.device)
-    st = load().knn_distances(_ptr(queries), _ptr(keys), _ptr(key_sqnorms), _ptr(key_offsets), _ptr(query_offsets),
-                              B, d, len(ko) - 1, max_keys, max_q, _dtype_code(queries), _ptr(out), ld, _stream(None))
+    code = _dtype_code(queries) | (KEYS_PACKED if packed_keys is not None else 0)
+    src = keys if packed_keys is None else packed_keys
+    st = load().knn_distances(_ptr(queries), _ptr(src), _ptr(key_sqnorms), _ptr(key_offsets), _ptr(query_offsets),
+                              B, d, len(ko) - 1, max_keys, max_q, code, _ptr(out), ld, _stream(None))
     _lib.check("knn_distances", st)
+    return out
+
+
+def packed_keys_bytes(n: int, d: int, dtype: torch.dtype) -> int:
+    """knn_packed_keys_bytes: bytes of the packed copy of n key rows of d elements (0: not packable)."""
+    return int(load().knn_packed_keys_bytes(int(n), int(d), DTYPES[_TORCH_DTYPES[dtype]]))
+
+
+def pack_keys(keys: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """knn_pack_keys: the packed copy of a [n, d] bf16/f16 key matrix (uint8 device tensor, into `out`
+    when given), read by the matrix-core distance kernels in place of the row-major keys."""
+    _need(keys.is_cuda and keys.is_contiguous() and keys.dim() == 2, "keys: contiguous 2-D device tensor")
+    nbytes = packed_keys_bytes(keys.shape[0], keys.shape[1], keys.dtype) if keys.dtype in _TORCH_DTYPES else 0
+    _need(nbytes > 0, "keys cannot be packed (bf16/f16 with d % 128 == 0 and d <= 65536)")
+    if out is None:
+        out = torch.empty(nbytes, dtype=torch.uint8, device=keys.device)
+    _need(out.is_cuda and out.is_contiguous() and out.numel() * out.element_size() == nbytes,
+          f"out: contiguous device tensor of {nbytes} bytes")
+    st = load().knn_pack_keys(_ptr(keys), keys.shape[0], keys.shape[1], _dtype_code(keys), _ptr(out),
+                              _stream(stream))
+    _lib.check("knn_pack_keys", st)
     return out
 
 

@@ -24,6 +24,7 @@ KNN_OK = 0
 STATUS_NAMES = {0: "KNN_OK", 1: "KNN_ERR_INVALID_ARG", 2: "KNN_ERR_R_EXCEEDS_N", 3: "KNN_ERR_UNSUPPORTED",
                 4: "KNN_ERR_WORKSPACE", 5: "KNN_ERR_HIP"}
 DTYPES = {"f32": 0, "bf16": 1, "f16": 2}
+KEYS_PACKED = 0x100  # OR'ed into a 16-bit dtype: the keys are the packed copy (knn_pack_keys)
 PARTS = {"distances": 1, "select": 2, "mix": 3, "select_mix": 4}
 
 _MIX_ARGS = [P, P, P, P, P, P, P, I64, I64, I64, I64, I64, I64, I64, I64, I, I32, F, F, P, P, P, P, SZ, P]
@@ -42,6 +43,8 @@ SIGNATURES: Dict[str, tuple] = {
                                     P, P, P, P, SZ]),
     "knn_distances": (I, [P, P, P, P, P, I64, I64, I64, I64, I64, I, P, I64, P]),
     "knn_key_sqnorms": (I, [P, I64, I64, I, P, P]),
+    "knn_pack_keys": (I, [P, I64, I64, I, P, P]),
+    "knn_packed_keys_bytes": (SZ, [I64, I64, I]),
     "knn_mix": (I, [P, P, P, P, P, P, I64, I64, I64, I32, F, F, P, P]),
     "knn_mix_rrc": (I, [P, P, P, P, P, P, I64, I64, I64, I32, F, F, F, P, P, P]),
     "knn_stream_read": (I, [P, SZ, P, P]),

@@ -545,7 +545,9 @@ DistPlan plan_distances(int64_t d, knn_dtype dtype, int64_t max_queries, const v
 
 hipError_t launch_distances(const DistPlan &plan, knn_dtype dtype, const DistArgs &args, int64_t S,
                             hipStream_t stream) {
+    if (plan.mfma && plan.packed) return launch_distances_packed(plan.mq, dtype, args, S, plan.groups, stream);
     if (plan.mfma) return launch_distances_mfma(plan.mq, dtype, args, S, plan.groups, stream);
+    if (plan.packed) return hipErrorInvalidValue;  // packed keys are read by the matrix-core kernels only
     const int64_t nblocks = S * plan.tiles_per_set;
     if (nblocks > 0x7fffffffLL || plan.groups > 65535) return hipErrorInvalidConfiguration;
     const dim3 grid(static_cast<unsigned>(nblocks), static_cast<unsigned>(plan.groups));

@@ -25,6 +25,10 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 bool valid_dtype(knn_dtype t) { return t == KNN_F32 || t == KNN_BF16 || t == KNN_F16; }
 
+// The element type of a dtype argument, and whether it carries the packed-keys flag.
+knn_dtype base_dtype(knn_dtype t) { return static_cast<knn_dtype>(static_cast<int>(t) & ~static_cast<int>(KNN_KEYS_PACKED)); }
+bool packed_flag(knn_dtype t) { return (static_cast<int>(t) & static_cast<int>(KNN_KEYS_PACKED)) != 0; }
+
 struct Layout {
     int rows_per_tile;
     int64_t tiles_per_set;
@@ -121,7 +125,8 @@ struct Call {
     const int64_t *query_offsets;
     const float *p_lm;
     int64_t B, d, V, S, total_keys, min_keys, max_keys, max_queries;
-    knn_dtype dtype;
+    knn_dtype dtype;     // element type (the packed flag stripped)
+    bool packed;         // keys: the packed copy (knn_pack_keys)
     int32_t r;
     float mu, lambda;
     int rrc;             // 1: lambda_t per query (eq. rrc) instead of lambda
@@ -149,6 +154,10 @@ knn_status validate_part(const Call &c, int part) {
     const bool sel = part == 0 || part == KNN_PART_SELECT || part == KNN_PART_SELECT_MIX;
     const bool mix = part == 0 || part == KNN_PART_MIX || part == KNN_PART_SELECT_MIX;
     if (dist && (!c.queries || !c.keys)) return KNN_ERR_INVALID_ARG;
+    if (c.packed) {  // packed keys: 16-bit elements, read by the matrix-core kernels only
+        if (c.dtype != KNN_BF16 && c.dtype != KNN_F16) return KNN_ERR_INVALID_ARG;
+        if (dist && !plan_distances(c.d, c.dtype, c.max_queries, c.queries, c.keys).mfma) return KNN_ERR_UNSUPPORTED;
+    }
     if ((sel || mix) && (!c.nbr_ids || !c.nbr_dists)) return KNN_ERR_INVALID_ARG;
     if (mix && (!c.values || !c.p_lm || !c.p_m)) return KNN_ERR_INVALID_ARG;
     if (mix && (st = check_scalars(c.mu, c.lambda)) != KNN_OK) return st;
@@ -239,6 +248,7 @@ knn_status run_part(const Call &c, int part, hipStream_t stream) {
     float *tmax = ws ? reinterpret_cast<float *>(ws + L.off_tmax) : nullptr;
     if (part == KNN_PART_DISTANCES) {
         DistPlan p = plan_distances(c.d, c.dtype, c.max_queries, c.queries, c.keys);
+        p.packed = c.packed;
         p.rows_per_tile = L.rows_per_tile;
         p.tiles_per_set = L.tiles_per_set;
         DistArgs a{};
@@ -272,14 +282,18 @@ knn_status run_part(const Call &c, int part, hipStream_t stream) {
         a.cand_list = f.list;
         a.fallback = f.fallback;
         const SelectArgs sa = select_args(c, L, ws);
-        hipError_t e = launch_distances_mfma(p.mq, c.dtype, a, c.S, p.groups, stream, 1);
+        auto mfma = [&](int fm) {
+            return p.packed ? launch_distances_packed(p.mq, c.dtype, a, c.S, p.groups, stream, fm)
+                            : launch_distances_mfma(p.mq, c.dtype, a, c.S, p.groups, stream, fm);
+        };
+        hipError_t e = mfma(1);
         if (e == hipSuccess) e = launch_fused_threshold(sa, f, c.B, stream);
-        if (e == hipSuccess) e = launch_distances_mfma(p.mq, c.dtype, a, c.S, p.groups, stream, 2);
+        if (e == hipSuccess) e = mfma(2);
         if (e == hipSuccess) e = launch_fused_check(sa, f, c.B, stream);
         if (e == hipSuccess) {
             a.gate = fallback;
             a.gate_run = 1u;
-            e = launch_distances_mfma(p.mq, c.dtype, a, c.S, p.groups, stream, 0);
+            e = mfma(0);
         }
         return status_of(e);
     }
@@ -324,7 +338,8 @@ Call make_call(const void *queries, const void *keys, const float *key_sqnorms, 
     c.min_keys = min_keys;
     c.max_keys = max_keys;
     c.max_queries = max_queries;
-    c.dtype = dtype;
+    c.dtype = base_dtype(dtype);
+    c.packed = packed_flag(dtype);
     c.r = r;
     c.mu = mu;
     c.lambda = lambda;
@@ -398,9 +413,9 @@ knn_status knn_lm_mixture_noalloc(const void *queries, const void *keys, const f
                                   int32_t r, float mu, float lambda, float *p_m, int32_t *nbr_ids,
                                   float *nbr_dists, void *stream) {
     knn_status st = check_sizes(B, d, V, S, total_keys, min_keys_per_set, max_keys_per_set, max_queries_per_set,
-                                dtype, r, true);
+                                base_dtype(dtype), r, true);
     if (st != KNN_OK) return st;
-    const size_t need = layout(B, d, S, max_keys_per_set, max_queries_per_set, dtype, r).total;
+    const size_t need = layout(B, d, S, max_keys_per_set, max_queries_per_set, base_dtype(dtype), r).total;
     if (need > static_cast<size_t>(KNNLM_NOALLOC_SCRATCH_BYTES)) return KNN_ERR_WORKSPACE;
     void *ws = nullptr;
     if ((st = scratch_of_current_device(&ws)) != KNN_OK) return st;
@@ -495,10 +510,11 @@ knn_status knn_lm_mixture_part(knn_part part, const void *queries, const void *k
 size_t knn_lm_mixture_workspace_size(int64_t B, int64_t d, int64_t V, int64_t S, int64_t total_keys,
                                      int64_t min_keys_per_set, int64_t max_keys_per_set,
                                      int64_t max_queries_per_set, knn_dtype dtype, int32_t r) {
-    if (check_sizes(B, d, V, S, total_keys, min_keys_per_set, max_keys_per_set, max_queries_per_set, dtype, r,
+    const knn_dtype et = base_dtype(dtype);
+    if (check_sizes(B, d, V, S, total_keys, min_keys_per_set, max_keys_per_set, max_queries_per_set, et, r,
                     true) != KNN_OK)
         return 0;
-    return layout(B, d, S, max_keys_per_set, max_queries_per_set, dtype, r).total;
+    return layout(B, d, S, max_keys_per_set, max_queries_per_set, et, r).total;
 }
 
 knn_status knn_lm_mixture_validate(const void *queries, const void *keys, const int32_t *values,
@@ -525,9 +541,14 @@ knn_status knn_distances(const void *queries, const void *keys, const float *key
     if (!queries || !keys || !key_offsets || !query_offsets || !out) return KNN_ERR_INVALID_ARG;
     if (B < 1 || d < 1 || S < 1 || max_keys_per_set < 1 || max_queries_per_set < 1 || max_queries_per_set > B)
         return KNN_ERR_INVALID_ARG;
+    const bool packed = packed_flag(dtype);
+    dtype = base_dtype(dtype);
     if (!valid_dtype(dtype) || ld_out < max_keys_per_set) return KNN_ERR_INVALID_ARG;
+    if (packed && dtype != KNN_BF16 && dtype != KNN_F16) return KNN_ERR_INVALID_ARG;
     if (B > 0x7fffffffLL || max_keys_per_set > 0x7fffffffLL || max_queries_per_set > 65535) return KNN_ERR_UNSUPPORTED;
     DistPlan p = plan_distances(d, dtype, max_queries_per_set, queries, keys);
+    if (packed && !p.mfma) return KNN_ERR_UNSUPPORTED;
+    p.packed = packed;
     p.rows_per_tile = dist_tile_rows(d, dtype, S, max_keys_per_set, max_queries_per_set);
     p.tiles_per_set = (max_keys_per_set + p.rows_per_tile - 1) / p.rows_per_tile;
     if (S * p.tiles_per_set > 0x7fffffffLL || p.groups > 65535) return KNN_ERR_UNSUPPORTED;
@@ -550,6 +571,21 @@ knn_status knn_distances(const void *queries, const void *keys, const float *key
 knn_status knn_key_sqnorms(const void *keys, int64_t n, int64_t d, knn_dtype dtype, float *out, void *stream) {
     if (!keys || !out || n < 0 || d < 1 || !valid_dtype(dtype)) return KNN_ERR_INVALID_ARG;
     return status_of(launch_key_sqnorms(keys, n, d, dtype, out, static_cast<hipStream_t>(stream)));
+}
+
+size_t knn_packed_keys_bytes(int64_t n, int64_t d, knn_dtype dtype) {
+    const knn_dtype et = base_dtype(dtype);
+    if (n < 1 || d < 1 || (et != KNN_BF16 && et != KNN_F16) || d % kMfmaSpan != 0 || d > kMfmaMaxD) return 0;
+    if (n > (int64_t(1) << 40) / (2 * d)) return 0;
+    return static_cast<size_t>(packed_key_bytes(n, d));
+}
+
+knn_status knn_pack_keys(const void *keys, int64_t n, int64_t d, knn_dtype dtype, void *packed, void *stream) {
+    if (!keys || !packed) return KNN_ERR_INVALID_ARG;
+    if (knn_packed_keys_bytes(n, d, dtype) == 0) return n < 1 || d < 1 ? KNN_ERR_INVALID_ARG : KNN_ERR_UNSUPPORTED;
+    if ((reinterpret_cast<uintptr_t>(keys) & 15u) || (reinterpret_cast<uintptr_t>(packed) & 15u))
+        return KNN_ERR_INVALID_ARG;
+    return status_of(launch_pack_keys(keys, n, d, base_dtype(dtype), packed, static_cast<hipStream_t>(stream)));
 }
 
 }  // extern "C"

@@ -23,6 +23,7 @@ inline int vec_elems(knn_dtype t) { return 16 / elem_bytes(t); }
 // How the distance kernel covers the (set, key tile, query group) space.
 struct DistPlan {
     bool mfma;              // query batches: q.k on the matrix cores (16-bit elements, >= 16 queries per set)
+    bool packed;            // MFMA path: the keys are the packed copy (knn_pack_keys)
     int mq;                 // MFMA path: 16-query blocks per workgroup (1, 2, 4 or 8)
     bool vec;               // 16-byte loads (d % VEC == 0, aligned rows) vs element loads
     int cpl;                // chunks per lane (vector path), power of two <= kMaxCplVec
@@ -87,6 +88,14 @@ hipError_t launch_distances(const DistPlan &plan, knn_dtype dtype, const DistArg
 // distances written (mq 8 only).
 hipError_t launch_distances_mfma(int mq, knn_dtype dtype, const DistArgs &args, int64_t S, int64_t groups,
                                  hipStream_t stream, int fm = 0);
+// The same stages over keys in the packed layout (mfma_packed.hip).
+hipError_t launch_distances_packed(int mq, knn_dtype dtype, const DistArgs &args, int64_t S, int64_t groups,
+                                   hipStream_t stream, int fm = 0);
+// Bytes of the packed copy of n rows of d 16-bit elements: blocks of 16 rows
+// (the last one padded), each its fragments and then its rows' ||k||^2.
+int64_t packed_key_bytes(int64_t n, int64_t d);
+hipError_t launch_pack_keys(const void *keys, int64_t n, int64_t d, knn_dtype dtype, void *packed,
+                            hipStream_t stream);
 hipError_t launch_key_sqnorms(const void *keys, int64_t n, int64_t d, knn_dtype dtype, float *out,
                               hipStream_t stream);
 }  // namespace knnlm

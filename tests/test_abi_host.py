@@ -29,7 +29,7 @@ def test_exports_every_declared_function(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert lib.knn_abi_version() == 1
+    assert lib.knn_abi_version() == 2
     for s in range(6):
         assert lib.knn_status_string(s).decode()
     assert lib.knn_status_string(99).decode() == "unknown status"
@@ -132,3 +132,52 @@ def test_mixture_part_stage_pointer_rules(lib):
     assert args(2, None, None, FAKE, None, None) == INVALID
     # mix stage: mu = NaN is rejected
     assert args(3, None, None, None, FAKE, FAKE) == INVALID
+
+
+BF16_PACKED, F16_PACKED, KEYS_PACKED = 0x101, 0x102, 0x100
+
+
+def test_packed_keys_bytes(lib):
+    # blocks of 16 rows, each 32 d bytes of fragments then 16 fp32 norms
+    assert lib.knn_packed_keys_bytes(16, 128, 1) == 32 * 128 + 64
+    assert lib.knn_packed_keys_bytes(17, 128, 2) == 2 * (32 * 128 + 64)
+    assert lib.knn_packed_keys_bytes(8388608, 1024, 2) == 8388608 // 16 * (32 * 1024 + 64)
+    assert lib.knn_packed_keys_bytes(1000, 256, BF16_PACKED) == 63 * (32 * 256 + 64)  # the flag is ignored here
+    for n, d, t in ((0, 128, 1), (16, 0, 1), (16, 128, 0), (16, 192, 1), (16, 65536 + 128, 1), (16, 128, 7)):
+        assert lib.knn_packed_keys_bytes(n, d, t) == 0, (n, d, t)
+
+
+def test_pack_keys_rejects_before_touching_the_device(lib):
+    assert lib.knn_pack_keys(None, 16, 128, 1, FAKE, None) == INVALID
+    assert lib.knn_pack_keys(FAKE, 16, 128, 1, None, None) == INVALID
+    assert lib.knn_pack_keys(FAKE, 0, 128, 1, FAKE, None) == INVALID
+    assert lib.knn_pack_keys(FAKE + 8, 16, 128, 1, FAKE, None) == INVALID  # not 16-byte aligned
+    assert lib.knn_pack_keys(FAKE, 16, 128, 0, FAKE, None) == UNSUPPORTED  # fp32
+    assert lib.knn_pack_keys(FAKE, 16, 192, 1, FAKE, None) == UNSUPPORTED  # d % 128 != 0
+
+
+def test_packed_dtype_validation(lib):
+    # a batch the matrix cores serve: 128 queries on one set of 65536 keys at d = 1024
+    mc = dict(B=128, d=1024, max_queries=128, min_keys=65536, max_keys=65536)
+    ws = _ws_size(lib, dict(BASE, **mc))
+    assert _validate(lib, ws_bytes=ws, dtype=2, **mc) == OK
+    assert _validate(lib, ws_bytes=ws, dtype=F16_PACKED, **mc) == OK
+    assert _validate(lib, ws_bytes=ws, dtype=BF16_PACKED, **mc) == OK
+    assert _ws_size(lib, dict(BASE, dtype=F16_PACKED, **mc)) == ws
+    # fp32 keys cannot be packed; the flag on its own is no element type
+    assert _validate(lib, ws_bytes=ws, dtype=KEYS_PACKED, **mc) == INVALID
+    # fewer than 16 queries per set (the streaming kernel), or d % 128 != 0: not served packed
+    assert _validate(lib, dtype=BF16_PACKED) == UNSUPPORTED
+    mc_odd = dict(mc, d=1000)
+    assert _validate(lib, ws_bytes=_ws_size(lib, dict(BASE, **mc_odd)), dtype=BF16_PACKED, **mc_odd) == UNSUPPORTED
+    # the select and mix stages read no keys: the flag changes nothing there
+    a = dict(BASE, **mc)
+    st = lib.knn_lm_mixture_part(3, None, None, None, FAKE, FAKE, FAKE, FAKE, a["B"], a["d"], a["V"], a["S"],
+                                 a["total_keys"], a["min_keys"], a["max_keys"], a["max_queries"], BF16_PACKED,
+                                 a["r"], a["mu"], a["lam"], FAKE, FAKE, FAKE, None, 0, None)
+    assert st == OK or st == HIP  # validated; the launch itself needs a GPU
+    # knn_distances: packed keys with a streaming-path batch are refused
+    assert lib.knn_distances(FAKE, FAKE, None, FAKE, FAKE, 1, 1024, 1, 100, 1, BF16_PACKED, FAKE, 100, None) == \
+        UNSUPPORTED
+    assert lib.knn_distances(FAKE, FAKE, None, FAKE, FAKE, 16, 1024, 1, 100, 16, KEYS_PACKED, FAKE, 100, None) == \
+        INVALID

@@ -3,7 +3,9 @@ times (the distance stage, then the fused select and mixture), against the CPU
 oracle under rules P2-P5 (tests/parity.py).
 
 Every query of decode_7b, ragged_batch, decode_70b and specverify_seq is
-compared with the oracle element by element.  specverify_static (128 queries
+compared with the oracle element by element.  The two matrix-core workloads
+also run over the packed copy of their keys, which must select the same
+neighbours at the same distance bits.  specverify_static (128 queries
 on one store of 8,388,608 keys) is compared on all 128 queries too, in four
 tests of 32 rows each (rows b with b mod 4 = c), so every 16-query block of the
 matrix-core workgroup is covered by every test; the workload, its GPU result
@@ -45,14 +47,29 @@ def _free():
     torch.cuda.empty_cache()
 
 
-def _bench_step(w):
-    """The benchmark's step: the distance stage, then the fused select and mixture."""
+def _bench_step(w, packed=None):
+    """The benchmark's step: the distance stage, then the fused select and mixture (with packed, over
+    the packed copy of the keys)."""
     prob = knn.MixtureProblem(w.queries, w.keys, w.values, w.key_offsets, w.query_offsets, w.p_lm, w.r, w.mu,
-                              w.lam, key_offsets_host=w.key_offsets_host, query_offsets_host=w.query_offsets_host)
+                              w.lam, key_offsets_host=w.key_offsets_host, query_offsets_host=w.query_offsets_host,
+                              packed_keys=packed)
     prob.run_part("distances")
     prob.run_part("select_mix")
     torch.cuda.synchronize()
     return prob
+
+
+def _same_as_packed(w, prob):
+    """The step over the packed copy of the keys selects the same neighbours at the same distance bits."""
+    t0 = time.time()
+    packed = knn.pack_keys(w.keys)
+    pk = _bench_step(w, packed)
+    assert torch.equal(pk.ids, prob.ids)
+    assert torch.equal(pk.dists.view(torch.int32), prob.dists.view(torch.int32))
+    torch.testing.assert_close(pk.p_m, prob.p_m, rtol=0, atol=1e-6)
+    _say(f"packed keys: the same neighbours and distances ({time.time() - t0:.1f} s)")
+    del packed, pk
+    _free()
 
 
 def _every_query_properties(w, p_m, ids, dists):
@@ -74,6 +91,8 @@ def test_full_size_every_query(name):
     prob = _bench_step(w)
     p_m, ids, dists = prob.p_m, prob.ids, prob.dists
     _every_query_properties(w, p_m, ids, dists)
+    if name == "specverify_seq":
+        _same_as_packed(w, prob)
     B = int(w.query_offsets_host[-1])
     t1 = time.time()
     _say(f"full workload {name}: oracle on all {B} queries, {parity.host_threads()} host threads")
@@ -95,6 +114,7 @@ def static_store():
     _say("full workload specverify_static: running")
     prob = _bench_step(w)
     _every_query_properties(w, prob.p_m, prob.ids, prob.dists)
+    _same_as_packed(w, prob)
     keys_h, dt = oracle.host_elements(w.keys)
     _say(f"specverify_static: step run and keys on the host in {time.time() - t0:.1f} s")
     yield w, prob, (keys_h, dt)

@@ -59,10 +59,11 @@ def _store(case, seed):
     return rng, q, k, sample
 
 
+@pytest.mark.parametrize("layout", ["row-major", "packed"])
 @pytest.mark.parametrize("case", ["listed", "sample-far", "sample-near"])
 @pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float16])
-def test_fused_select_exact_integers(case, dtype):
-    _say(f"fused select: {case}, {dtype}")
+def test_fused_select_exact_integers(case, dtype, layout):
+    _say(f"fused select: {case}, {dtype}, {layout} keys")
     rng, q, k, _ = _store(case, 120 + len(case))
     vals = rng.integers(0, 1000, N).astype(np.int32)
     p_lm = rng.dirichlet(np.ones(1000), B).astype(np.float32)
@@ -72,7 +73,9 @@ def test_fused_select_exact_integers(case, dtype):
     tk = torch.as_tensor(k, device=dev).to(dtype).contiguous()
     tv, tp = torch.as_tensor(vals, device=dev), torch.as_tensor(p_lm, device=dev)
     tko, tqo = torch.as_tensor(ko, device=dev), torch.as_tensor(qo, device=dev)
-    prob = knn.MixtureProblem(tq, tk, tv, tko, tqo, tp, R, 0.01, 0.3, key_offsets_host=ko, query_offsets_host=qo)
+    packed = knn.pack_keys(tk) if layout == "packed" else None
+    prob = knn.MixtureProblem(tq, tk, tv, tko, tqo, tp, R, 0.01, 0.3, key_offsets_host=ko, query_offsets_host=qo,
+                              packed_keys=packed)
     p_m, ids, dists = prob.run()
     torch.cuda.synchronize()
     o_ids, o_d = oracle.select(q, k, "f32", ko, qo, R)
@@ -83,15 +86,16 @@ def test_fused_select_exact_integers(case, dtype):
     # the same call with precomputed key norms, and the stages one at a time
     norms = knn.key_sqnorms(tk)
     prob2 = knn.MixtureProblem(tq, tk, tv, tko, tqo, tp, R, 0.01, 0.3, key_sqnorms=norms, key_offsets_host=ko,
-                               query_offsets_host=qo)
+                               query_offsets_host=qo, packed_keys=packed)
     prob2.run_part("distances")
     prob2.run_part("select")
     torch.cuda.synchronize()
     assert torch.equal(prob2.ids, ids) and torch.equal(prob2.dists, dists)
-    del tk, prob, prob2
+    del tk, prob, prob2, packed
 
 
-def test_fused_nest_step_with_masked_keys():
+@pytest.mark.parametrize("layout", ["row-major", "packed"])
+def test_fused_nest_step_with_masked_keys(layout):
     """A NEST step (lambda_t, masked keys, decoding outputs) through the fused select: a third of the keys
     masked, among them the exact nearest keys of the first queries."""
     _say("fused select: NEST step with masked keys")
@@ -111,7 +115,8 @@ def test_fused_nest_step_with_masked_keys():
     tk = torch.as_tensor(k, device=dev).to(torch.bfloat16).contiguous()
     prob = knn.MixtureProblem(tq, tk, torch.as_tensor(vals, device=dev), torch.as_tensor(ko, device=dev),
                               torch.as_tensor(qo, device=dev), torch.as_tensor(p_lm, device=dev), R, 0.01,
-                              key_offsets_host=ko, query_offsets_host=qo)
+                              key_offsets_host=ko, query_offsets_host=qo,
+                              packed_keys=knn.pack_keys(tk) if layout == "packed" else None)
     out = prob.run_nest(0.3, 0.1, 0.5, key_mask=knn.mask_words(masked, N, dev))
     torch.cuda.synchronize()
     o_ids, o_d = oracle.select(q, k, "f32", ko, qo, R, key_mask=words)
