@@ -405,12 +405,39 @@ def time_config(name, steps, stream_gbs, with_oracle):
         tflops = 2.0 * macs / (dist_ms / 1e3) / 1e12
         out["matrix_cores"] = {"alg_flops": 2 * macs, "tflops": round(tflops, 1),
                                "frac_of_dense_peak": round(tflops / PEAK_MFMA_16BIT_TFLOPS, 4)}
+        out["packed_keys"] = time_packed(knn, torch, w, bufs, hints, steps, dist_bytes, step_bytes)
     del probs, bufs
     if with_oracle:
         out["oracle"] = oracle_estimate(w, spec, macs)
     del w
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
+    return out
+
+
+def time_packed(knn, torch, w, bufs, hints, steps, dist_bytes, step_bytes):
+    """The same workload over the packed copy of its keys (knn_pack_keys, run once per key store and timed
+    apart): the distance stage and the whole step, as above."""
+    packed = [knn.pack_keys(k) for k in bufs]
+    pack_ms = _events_ms(torch, lambda i: knn.pack_keys(bufs[0], out=packed[0]), 2)
+    probs = [knn.MixtureProblem(w.queries, k, w.values, w.key_offsets, w.query_offsets, w.p_lm, w.r, w.mu, w.lam,
+                                packed_keys=pk, **hints) for k, pk in zip(bufs, packed)]
+    nb = len(probs)
+    for i in range(2):
+        probs[i % nb].run()
+
+    def full(i):
+        probs[i % nb].run_part("distances")
+        probs[i % nb].run_part("select_mix")
+
+    step_ms = _events_ms(torch, full, steps)
+    dist_ms = _events_ms(torch, lambda i: probs[i % nb].run_part("distances"), steps)
+    out = {"pack_ms": round(pack_ms, 3), "packed_bytes": int(packed[0].numel()),
+           "ms_per_step": round(step_ms, 5), "queries_per_s": round(w.spec.B / (step_ms / 1e3), 1),
+           "step_hbm_frac": round(step_bytes / (step_ms / 1e3) / 1e9 / PEAK_HBM_GBS, 4),
+           "distance_ms": round(dist_ms, 5),
+           "distance_hbm_frac": round(dist_bytes / (dist_ms / 1e3) / 1e9 / PEAK_HBM_GBS, 4)}
+    del probs, packed
     return out
 
 

@@ -25,9 +25,15 @@
 // The queries (A operand) come from
 //   QM = 0: global memory, loaded into the same ring (16-query groups: the
 //           set's queries stay in L2, a quarter of the key bytes per step);
-//   QM = 1: an LDS ring of two span buffers that all waves fill together, one
-//           barrier per step (larger groups: their A fragments are read by
-//           every wave, which would multiply L2 traffic).
+//   QM = 1: two LDS span buffers that all waves fill together, one barrier
+//           per step (larger groups: their A fragments are read by every wave,
+//           which would multiply L2 traffic).  Each thread's share of a step's
+//           query span loads into the same ring set as that step's keys: the
+//           memory counter completes loads in order, so a separate, shallower
+//           query prefetch would make every wait for it a wait for all older
+//           key loads as well, and the key ring would be as shallow as the
+//           query prefetch (measured at 128 queries x 8.4 M keys of d = 1024:
+//           4.0 ms with a two-step query prefetch, 3.0 ms in the key ring).
 // Every step does the same MFMAs in the same k order as the row-major kernel,
 // and ||k||^2 and ||q||^2 are accumulated over the same fragments in the same
 // order, so every distance equals the row-major kernel's bit for bit.
@@ -70,6 +76,11 @@ __global__ __launch_bounds__(NW * kWave, 8 / NW) void k_dist_packed(DistArgs a, 
     static_assert(FM == 0 || MQ == 8, "the fused select runs on 128-query groups");
     __shared__ __align__(16) u32x4_t qlds[QM == 1 ? 2 : 1][QM == 1 ? QB * kPkChunks : 1];
     __shared__ uint32_t smin[QB], smax[QB];
+    // ||q||^2 of the group's queries (written by every wave after each pass:
+    // every wave sums the same A fragments in the same order) and, for FM 2,
+    // their thresholds, read by the epilogue four queries at a time
+    __shared__ __align__(16) float sqn[QB];
+    __shared__ __align__(16) uint32_t sthr[FM == 2 ? QB : 4];
     constexpr int kStage = FM == 2 ? 1024 : 1;  // candidates staged per tile
     __shared__ uint64_t stage_key[kStage];
     __shared__ uint8_t stage_q[kStage];
@@ -87,18 +98,22 @@ __global__ __launch_bounds__(NW * kWave, 8 / NW) void k_dist_packed(DistArgs a, 
     if (tl >= n_tiles) return;
     const int64_t tiles = a.tiles_per_set;
     const int64_t se = FM == 0 ? 1 : a.sample_every;
-    const int64_t per_set = FM == 1 ? (tiles + se - 1) / se : tiles;
+    // FM 1 takes one sample piece, FM 2 one whole sampling group of se tiles
+    // (it writes no per-tile extrema, and long streams per workgroup run
+    // faster: fewer pipeline fills and drains), FM 0 one tile
+    const int64_t per_set = FM != 0 ? (tiles + se - 1) / se : tiles;
     const int64_t s = tl / per_set;
-    const int64_t tile = FM == 1 ? (tl - s * per_set) * se : tl - s * per_set;
+    const int64_t tile = FM != 0 ? (tl - s * per_set) * se : tl - s * per_set;
     const int64_t k0 = a.key_offsets[s];
     int64_t N = a.key_offsets[s + 1] - k0;
     if (N > a.ld) N = a.ld;
     const int64_t qb = a.query_offsets[s] + grp * QB;
     const int64_t qe = a.query_offsets[s + 1];
-    // this workgroup's rows [r0, r1): the tile, its sample piece (FM 1), or the tile past its piece (FM 2)
+    // this workgroup's rows [r0, r1): the tile, its sample piece (FM 1), or the
+    // group's tiles past the piece at the start of its first (FM 2)
     int64_t r0 = tile * a.rows_per_tile;
-    const int64_t rend = r0 + (FM == 1 ? a.sample_rows : a.rows_per_tile);
-    if (FM == 2 && tile % se == 0) r0 += a.sample_rows;
+    const int64_t rend = r0 + (FM == 1 ? a.sample_rows : FM == 2 ? se * a.rows_per_tile : a.rows_per_tile);
+    if (FM == 2) r0 += a.sample_rows;
     if (qb >= qe || r0 >= N) return;  // uniform over the block
     const int nq = static_cast<int>(qe - qb < QB ? qe - qb : QB);
     const int64_t r1 = rend < N ? rend : N;
@@ -130,17 +145,25 @@ __global__ __launch_bounds__(NW * kWave, 8 / NW) void k_dist_packed(DistArgs a, 
         smax[q] = 0u;
     }
     if (FM == 2 && tid == 0) stage_n = 0u;
-    uint32_t thr_l[MQ];  // FM 2: thresholds of query rows j * 16 + lr (0 past the group: nothing passes)
-#pragma unroll
-    for (int j = 0; j < MQ; ++j) {
-        const int q = j * 16 + lr;
-        thr_l[j] = (FM == 2 && q < nq) ? a.cand_thr[qb + q] : 0u;
+    if constexpr (FM == 2) {  // thresholds (0 past the group: nothing passes)
+        for (int q = tid; q < QB; q += NT) sthr[q] = q < nq ? a.cand_thr[qb + q] : 0u;
     }
 
     // Register ring: set `set` holds one step's B fragments of this wave's
     // KBW blocks (two MFMA steps each) and, for QM 0, the A fragments.
     u32x4_t kr[NS][KBW][2];
     u32x4_t ar[QM == 0 ? NS : 1][QM == 0 ? MQ : 1][2];
+    // QM 1: the step's query span, chunk i of this thread being row e / 8,
+    // column e % 8 (e = i * NT + tid), bound for swizzled LDS slot swz(row, column)
+    u32x4_t qr[QM == 1 ? NS : 1][QCH];
+    uint32_t qso[QCH];
+    int qslot[QCH];
+#pragma unroll
+    for (int i = 0; i < QCH; ++i) {
+        const int e = i * NT + tid, n = e / kPkChunks, c = e % kPkChunks;
+        qso[i] = static_cast<uint32_t>(n < nq ? n : 0) * rb + static_cast<uint32_t>(c * 16);
+        qslot[i] = swz<kPkChunks>(n, c);
+    }
     uint32_t qoff[MQ];  // QM 0: query row j * 16 + lr (the group's first past its end), this lane's 16 bytes
 #pragma unroll
     for (int j = 0; j < MQ; ++j) {
@@ -163,22 +186,7 @@ __global__ __launch_bounds__(NW * kWave, 8 / NW) void k_dist_packed(DistArgs a, 
 #pragma unroll
                 for (int c = 0; c < 2; ++c)
                     ar[set][j][c] = *reinterpret_cast<const u32x4_t *>(qbase + qoff[j] + sp * 128u + c * 64);
-        }
-    };
-    // QM 1: chunk i of this thread is row e / 8, column e % 8 of the step's
-    // query span, e = i * NT + tid; swizzled LDS slot swz(row, column).
-    u32x4_t qr[2][QCH];
-    uint32_t qso[QCH];
-    int qslot[QCH];
-#pragma unroll
-    for (int i = 0; i < QCH; ++i) {
-        const int e = i * NT + tid, n = e / kPkChunks, c = e % kPkChunks;
-        qso[i] = static_cast<uint32_t>(n < nq ? n : 0) * rb + static_cast<uint32_t>(c * 16);
-        qslot[i] = swz<kPkChunks>(n, c);
-    }
-    auto qload = [&](int set, uint32_t t) __attribute__((always_inline)) {
-        if constexpr (QM == 1) {
-            const uint32_t sp = t % nspan;
+        } else {
 #pragma unroll
             for (int i = 0; i < QCH; ++i) qr[set][i] = *reinterpret_cast<const u32x4_t *>(qbase + qso[i] + sp * 128u);
         }
@@ -256,35 +264,60 @@ __global__ __launch_bounds__(NW * kWave, 8 / NW) void k_dist_packed(DistArgs a, 
             kk[kb] = kn[kb];
             mk[kb] = ok_row[kb] && ((mw[kb] >> ((k0 + row[kb]) & 31)) & 1u) != 0u;
         }
+        // ||q||^2 of this lane's rows j * 16 + lr to LDS; this wave reads back those of
+        // rows j * 16 + 4 g .. + 3, the queries whose products it holds (LDS
+        // operations of one wave complete in order)
+#pragma unroll
+        for (int j = 0; j < MQ; ++j) {
+            const float qsum = group4_sum(qqp[j]);  // every lane takes part in the exchange
+            if (g == 0) sqn[j * 16 + lr] = qsum;
+        }
+        auto dist_of = [&](int j, int kb, int i, float qn) __attribute__((always_inline)) {
+            return mk[kb] ? __uint_as_float(kMaskedBits) : clamp_nonneg(fmaf(-2.0f, acc[j][kb][i], qn + kk[kb]));
+        };
         if constexpr (FM == 2) {
-            // candidates: distance bits below the query's threshold, appended to
-            // the LDS stage a wave at a time (one LDS atomic per wave that has any)
+            // candidates: distance bits below the query's threshold.  They are
+            // rare (about 1.2 r of a row's keys), so one ballot first tells
+            // whether any lane of the wave holds one in this pass.
+            bool any = false;
 #pragma unroll
             for (int j = 0; j < MQ; ++j) {
-                const float qsum = group4_sum(qqp[j]);
+                const f32x4_t qn4 = *reinterpret_cast<const f32x4_t *>(&sqn[j * 16 + 4 * g]);
+                const u32x4_t th4 = *reinterpret_cast<const u32x4_t *>(&sthr[j * 16 + 4 * g]);
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int q = j * 16 + g * 4 + i;
-                    const float qn = __shfl(qsum, g * 4 + i);
-                    const uint32_t th = __shfl(thr_l[j], g * 4 + i);
+                for (int i = 0; i < 4; ++i)
 #pragma unroll
-                    for (int kb = 0; kb < KBW; ++kb) {
-                        const float dist = mk[kb] ? __uint_as_float(kMaskedBits)
-                                                  : clamp_nonneg(fmaf(-2.0f, acc[j][kb][i], qn + kk[kb]));
-                        const bool c = q < nq && ok_row[kb] && __float_as_uint(dist) < th;
-                        const uint64_t bal = __ballot(c);
-                        if (bal != 0ull) {
-                            const int first = __ffsll(static_cast<unsigned long long>(bal)) - 1;
-                            uint32_t base = 0u;
-                            if (lane == first) base = atomicAdd(&stage_n, static_cast<uint32_t>(__popcll(bal)));
-                            base = readlane_u32(base, first);
-                            if (c) {
-                                const uint32_t pos =
-                                    base + static_cast<uint32_t>(__popcll(bal & ((1ull << lane) - 1ull)));
-                                if (pos < static_cast<uint32_t>(kStage)) {
-                                    stage_key[pos] = (static_cast<uint64_t>(__float_as_uint(dist)) << 32) |
-                                                     static_cast<uint32_t>(row[kb]);
-                                    stage_q[pos] = static_cast<uint8_t>(q);
+                    for (int kb = 0; kb < KBW; ++kb)
+                        any |= ok_row[kb] && __float_as_uint(dist_of(j, kb, i, qn4[i])) < th4[i];
+            }
+            if (__ballot(any) != 0ull) {
+                // append them to the LDS stage a wave at a time (one LDS atomic per
+                // wave that has any); queries past the group have threshold 0
+#pragma unroll
+                for (int j = 0; j < MQ; ++j) {
+                    const f32x4_t qn4 = *reinterpret_cast<const f32x4_t *>(&sqn[j * 16 + 4 * g]);
+                    const u32x4_t th4 = *reinterpret_cast<const u32x4_t *>(&sthr[j * 16 + 4 * g]);
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int q = j * 16 + g * 4 + i;
+#pragma unroll
+                        for (int kb = 0; kb < KBW; ++kb) {
+                            const float dist = dist_of(j, kb, i, qn4[i]);
+                            const bool c = ok_row[kb] && __float_as_uint(dist) < th4[i];
+                            const uint64_t bal = __ballot(c);
+                            if (bal != 0ull) {
+                                const int first = __ffsll(static_cast<unsigned long long>(bal)) - 1;
+                                uint32_t base = 0u;
+                                if (lane == first) base = atomicAdd(&stage_n, static_cast<uint32_t>(__popcll(bal)));
+                                base = readlane_u32(base, first);
+                                if (c) {
+                                    const uint32_t pos =
+                                        base + static_cast<uint32_t>(__popcll(bal & ((1ull << lane) - 1ull)));
+                                    if (pos < static_cast<uint32_t>(kStage)) {
+                                        stage_key[pos] = (static_cast<uint64_t>(__float_as_uint(dist)) << 32) |
+                                                         static_cast<uint32_t>(row[kb]);
+                                        stage_q[pos] = static_cast<uint8_t>(q);
+                                    }
                                 }
                             }
                         }
@@ -297,16 +330,14 @@ __global__ __launch_bounds__(NW * kWave, 8 / NW) void k_dist_packed(DistArgs a, 
         // the pass's extrema of each query fold into the tile's (LDS atomics)
 #pragma unroll
         for (int j = 0; j < MQ; ++j) {
-            const float qsum = group4_sum(qqp[j]);  // ||q||^2 of query j*16 + lr
+            const f32x4_t qn4 = *reinterpret_cast<const f32x4_t *>(&sqn[j * 16 + 4 * g]);
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int q = j * 16 + g * 4 + i;
-                const float qn = __shfl(qsum, g * 4 + i);
                 float tmn = __builtin_huge_valf(), tmx = 0.0f;
 #pragma unroll
                 for (int kb = 0; kb < KBW; ++kb) {
-                    const float dist = mk[kb] ? __uint_as_float(kMaskedBits)
-                                              : clamp_nonneg(fmaf(-2.0f, acc[j][kb][i], qn + kk[kb]));
+                    const float dist = dist_of(j, kb, i, qn4[i]);
                     const bool ok = q < nq && ok_row[kb];
                     // no branch around the store
                     *(ok ? a.dist + (qb + q) * a.ld + row[kb] : &g_packed_sink) = dist;
@@ -325,9 +356,9 @@ __global__ __launch_bounds__(NW * kWave, 8 / NW) void k_dist_packed(DistArgs a, 
     };
 
     // Step t: the matrix cores on set t % NS (queries from LDS buffer t % 2),
-    // then the set reloads step t + NS; with the LDS ring, the next step's
-    // query span goes from its register set to the other buffer, that set
-    // loads the span of step t + 3, and the barrier orders the buffers.
+    // then the set reloads step t + NS; with the LDS buffers, the next step's
+    // query span goes from its ring set to the other buffer, and the barrier
+    // orders the buffers.
     // Steps past the last one re-read it, and the step count is padded to a
     // multiple of NS with steps whose products are never stored.  A pass is a
     // whole number of groups of NS steps (the host launches NS dividing the
@@ -336,12 +367,7 @@ __global__ __launch_bounds__(NW * kWave, 8 / NW) void k_dist_packed(DistArgs a, 
 #pragma unroll
     for (int k = 0; k < NS; ++k) load(k, static_cast<uint32_t>(k) < T ? static_cast<uint32_t>(k) : T - 1);
     load_rows(NS - 1);
-    if constexpr (QM == 1) {
-        qload(0, 0);
-        qwrite(0, 0);
-        qload(1, 1);
-        qload(0, 2);
-    }
+    if constexpr (QM == 1) qwrite(0, 0);
     __syncthreads();  // the query span buffer, the extrema and the stage counter are set
     for (uint32_t t0 = 0; t0 < T; t0 += NS) {
 #pragma unroll
@@ -351,8 +377,7 @@ __global__ __launch_bounds__(NW * kWave, 8 / NW) void k_dist_packed(DistArgs a, 
             const uint32_t tn = t + NS;
             load(k, tn < T ? tn : T - 1);
             if constexpr (QM == 1) {
-                qwrite((k + 1) & 1, (k + 1) & 1);
-                qload((k + 1) & 1, t + 3);
+                qwrite((k + 1) % NS, (k + 1) & 1);
                 __syncthreads();
             }
         }
@@ -432,7 +457,7 @@ __global__ __launch_bounds__(256) void k_pack_norms(const u32x4_t *keys, int64_t
 // Ring depth NS of each group size, used when NS divides the steps per pass
 // (d / 64, always even); other passes take a ring of two.
 template <int MQ>
-constexpr int packed_ring() { return MQ == 1 ? 4 : 8; }
+constexpr int packed_ring() { return 4; }
 
 template <knn_dtype DT, int MQ, int KBW, int NW, int QM, int FM>
 void launch_packed_ns(bool deep, const DistArgs &a, int64_t n_tiles, int64_t groups, dim3 grid, hipStream_t st) {
@@ -477,10 +502,11 @@ hipError_t launch_distances_packed(int mq, knn_dtype dtype, const DistArgs &args
     if (fm == 2 && (args.cand_thr == nullptr || args.cand_count == nullptr || args.cand_list == nullptr ||
                     args.fallback == nullptr))
         return hipErrorInvalidValue;
-    // a tile spans at most rows_per_tile / 16 + 1 blocks: its byte offsets fit 32 bits
-    if ((args.rows_per_tile / kBlockRows + 2) * packed_block_bytes(args.d) > 0xffffffffLL)
-        return hipErrorInvalidConfiguration;
-    const int64_t per_set = fm == 1 ? (args.tiles_per_set + args.sample_every - 1) / args.sample_every
+    // a workgroup's rows (a tile, or a sampling group of tiles for fm 2) span at most
+    // rows / 16 + 1 blocks: their byte offsets fit 32 bits
+    const int64_t wg_rows = static_cast<int64_t>(args.rows_per_tile) * (fm == 2 ? args.sample_every : 1);
+    if ((wg_rows / kBlockRows + 2) * packed_block_bytes(args.d) > 0xffffffffLL) return hipErrorInvalidConfiguration;
+    const int64_t per_set = fm != 0 ? (args.tiles_per_set + args.sample_every - 1) / args.sample_every
                                     : args.tiles_per_set;
     const int64_t n_tiles = S * per_set;
     const int64_t nblocks = (n_tiles + 7) / 8 * 8 * groups;
