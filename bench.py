@@ -31,6 +31,9 @@ PEAK_MFMA_16BIT_TFLOPS = 2500.0  # MI355X dense bf16 / fp16 matrix cores, publis
 PER_CONFIG_STEPS = {"tiny": 200, "decode_7b": 200, "ragged_batch": 20, "decode_70b": 20, "specverify_seq": 10,
                     "specverify_static": 10}
 PMC_FILE = os.path.join(ROOT, "profiles", "dist_kernel_{workload}_pmc.json")
+# The sources the distance kernels are built from (a change makes committed counters stale).
+DIST_SOURCES = ("dist_kernels.hip", "mfma_kernels.hip", "mfma_packed.hip", "mfma_device.h", "knnlm_device.h",
+                "knnlm_internal.h")
 
 
 def _args():
@@ -39,6 +42,8 @@ def _args():
     ap.add_argument("--steps", type=int, default=1000)
     ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--workload", default="decode_7b")
+    ap.add_argument("--packed-keys", action="store_true",
+                    help="read the keys through their packed copy (knn_pack_keys; matrix-core workloads only)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle sample")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -51,7 +56,7 @@ def _args():
 
 def dist_kernel_source_hash() -> str:
     h = hashlib.sha256()
-    for f in ("dist_kernels.hip", "mfma_kernels.hip", "knnlm_device.h", "knnlm_internal.h"):
+    for f in DIST_SOURCES:
         h.update(open(os.path.join(ROOT, "paper_2405_19325_amd", "csrc", f), "rb").read())
     return h.hexdigest()[:16]
 
@@ -88,8 +93,9 @@ def main():
     w = gen.make(spec, seed, device=dev)
     keys2 = gen.second_key_copy(spec, seed, device=dev)
     hints = dict(key_offsets_host=w.key_offsets_host, query_offsets_host=w.query_offsets_host)
+    packed = [knn.pack_keys(k) for k in (w.keys, keys2)] if a.packed_keys else [None, None]
     probs = [knn.MixtureProblem(w.queries, k, w.values, w.key_offsets, w.query_offsets, w.p_lm, w.r, w.mu, w.lam,
-                                **hints) for k in (w.keys, keys2)]
+                                packed_keys=pk, **hints) for k, pk in zip((w.keys, keys2), packed)]
     torch.cuda.synchronize()
 
     B = spec.B
@@ -234,10 +240,11 @@ def main():
     max_q = int(np.diff(w.query_offsets_host).max())
     matrix_core = spec.dtype in ("bf16", "f16") and spec.d % 8 == 0 and max_q >= 16
     achieved = dist_alg_bytes / (dist_launch_ms / 1e3) / 1e9
-    traffic = measured_traffic(a.workload)
+    traffic = measured_traffic(a.workload + ("_packed" if a.packed_keys else ""))
+    kname = ("k_dist_packed" if a.packed_keys else "k_dist_mfma") if matrix_core else "k_dist_vec"
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
-                "kernel": "distance stage (" + ("k_dist_mfma" if matrix_core else "k_dist_vec") + ")",
+                "kernel": "distance stage (" + kname + ")",
                 "alg_bytes_per_launch": dist_alg_bytes,
                 "avg_launch_ms": round(dist_launch_ms, 5), "timed_launches": n_dist,
                 "in_step_event_ms": round(avg_dist_ms, 5)}
@@ -288,6 +295,7 @@ def main():
             "r": spec.r,
             "parallelism": "single GPU",
             "key_buffers_rotated": 2,
+            "key_layout": "packed" if a.packed_keys else "row-major",
         },
         "select_mix_ms": round(avg_tail_ms, 5),
         "step_alg_bytes": step_alg_bytes,

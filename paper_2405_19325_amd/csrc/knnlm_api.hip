@@ -71,10 +71,12 @@ Layout layout(int64_t B, int64_t d, int64_t S, int64_t max_keys, int64_t max_que
     L.off_fallback = align_up(L.off_ticket + sizeof(uint32_t) * per_row);
     L.fused = fused_shape(B, d, dtype, max_queries, L.ld, r, L.tiles_per_set);
     // The sample: the first sample_rows rows (whole 256-key passes) of every
-    // sample_every-th tile, 1/32 of the keys, in pieces small enough that the
-    // sample launch fills the chip.
+    // sample_every-th tile, 1/64 of the keys, in pieces small enough that the
+    // sample launch fills the chip.  (1/64 keeps about 2,300 candidates per
+    // query for r = 1024 against about 1,900 at 1/32, both well inside the
+    // lists, and halves the sample pass and the threshold kernel's reads.)
     L.sample_rows = L.rows_per_tile / 8 > 256 ? L.rows_per_tile / 8 : 256;
-    L.sample_every = 32 * L.sample_rows / L.rows_per_tile > 1 ? 32 * L.sample_rows / L.rows_per_tile : 1;
+    L.sample_every = 64 * L.sample_rows / L.rows_per_tile > 1 ? 64 * L.sample_rows / L.rows_per_tile : 1;
     L.total = align_up(L.off_fallback + (L.fused ? sizeof(uint32_t) : 0));
     return L;
 }

@@ -1,6 +1,6 @@
 """The fused select of query batches on long rows (the 128-query matrix-core
 distance kernel): each query's threshold comes from a sample of its keys
-(the first 512 rows of every fourth 4096-row tile), the distance kernel lists
+(the first 512 rows of every eighth 4096-row tile), the distance kernel lists
 the keys below it instead of writing the distance matrix, and when a query's
 list holds fewer than r or more than its capacity the distance matrix is
 written and selected by the wide select instead.
@@ -23,7 +23,7 @@ pytestmark = pytest.mark.gpu
 knn = pytest.importorskip("paper_2405_19325_amd")
 
 N, D, B, R = 600000, 128, 80, 64
-TILE, PIECE, EVERY = 4096, 512, 4  # the distance tiles of d = 128 and the sample's geometry
+TILE, PIECE, EVERY = 4096, 512, 8  # the distance tiles of d = 128 and the sample's geometry
 
 
 def _say(msg):
