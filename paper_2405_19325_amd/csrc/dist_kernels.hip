@@ -59,10 +59,14 @@ __device__ __forceinline__ bool tile_work(const DistArgs &a, TileWork &t) {
     return true;
 }
 
-// Block-wide min/max of each query's distances over this tile, for the select stage.
+// Block-wide min/max of each query's distances over this tile, for the select
+// stage, and (group_min) each wave's minimum: the select's group minima, group
+// 4 * tile + wave holding the rows r0 + wave, r0 + wave + 4, ... of the tile
+// (+infinity where the wave has no row or only masked ones).
 template <int NQ>
 __device__ __forceinline__ void write_tile_extrema(const DistArgs &a, const TileWork &t, const float (&mn)[NQ],
                                                    const float (&mx)[NQ]) {
+    static_assert(kWavesPerDistBlock == 4, "one 16-byte word of group minima per tile");
     constexpr int NW = kWavesPerDistBlock;
     __shared__ float smin[NW][NQ];
     __shared__ float smax[NW][NQ];
@@ -84,9 +88,21 @@ __device__ __forceinline__ void write_tile_extrema(const DistArgs &a, const Tile
             M = fmaxf(M, smax[w][j]);
         }
         const int64_t tile = t.r0 / a.rows_per_tile;
-        a.tile_min[(t.qb + j) * a.tiles_per_set + tile] = m;
-        a.tile_max[(t.qb + j) * a.tiles_per_set + tile] = M;
+        if (a.tile_min != nullptr) {
+            a.tile_min[(t.qb + j) * a.tiles_per_set + tile] = m;
+            a.tile_max[(t.qb + j) * a.tiles_per_set + tile] = M;
+        }
+        if (a.group_min != nullptr)
+            *reinterpret_cast<float4 *>(a.group_min + (t.qb + j) * a.groups_per_set + 4 * tile) =
+                make_float4(smin[0][j], smin[1][j], smin[2][j], smin[3][j]);
     }
+}
+
+// The select stage's counters, cleared by the launch's first workgroup (so
+// that no memset is needed between the stages, and a captured graph holds none).
+__device__ __forceinline__ void clear_select_words(const DistArgs &a) {
+    if (a.zero_words == nullptr || blockIdx.x != 0 || blockIdx.y != 0) return;
+    for (int64_t i = threadIdx.x; i < a.n_zero_words; i += blockDim.x) a.zero_words[i] = 0u;
 }
 
 // 16-byte loads: d % VEC == 0, 16-byte aligned rows, at most CPL chunks per lane.
@@ -119,6 +135,7 @@ __global__ __launch_bounds__(kDistThreads) void k_dist_vec(DistArgs a) {
     constexpr int RPI = D / SPR;            // rows per loop iteration
     static_assert(CPL % CPS == 0 && D % SPR == 0, "whole sets per row, whole rows per iteration");
     constexpr int EB = Elem<DT>::BYTES;
+    clear_select_words(a);
     TileWork t;
     if (!tile_work<NQ>(a, t)) return;
 
@@ -246,7 +263,7 @@ __global__ __launch_bounds__(kDistThreads) void k_dist_vec(DistArgs a) {
         }
     }
     __builtin_amdgcn_sched_barrier(0);
-    if (a.tile_min != nullptr) write_tile_extrema<NQ>(a, t, mn, mx);
+    if (a.tile_min != nullptr || a.group_min != nullptr) write_tile_extrema<NQ>(a, t, mn, mx);
 }
 
 // --------------------------------------------------- element path (any d)
@@ -260,6 +277,7 @@ __global__ __launch_bounds__(kDistThreads) void k_dist_elem(DistArgs a) {
     constexpr int EB = Elem<DT>::BYTES;
     constexpr int PW = Elem<DT>::PER_WORD;
     constexpr int NW = kWavesPerDistBlock;
+    clear_select_words(a);
     TileWork t;
     if (!tile_work<NQ>(a, t)) return;
 
@@ -328,7 +346,7 @@ __global__ __launch_bounds__(kDistThreads) void k_dist_elem(DistArgs a) {
             }
         }
     }
-    if (a.tile_min != nullptr) write_tile_extrema<NQ>(a, t, mn, mx);
+    if (a.tile_min != nullptr || a.group_min != nullptr) write_tile_extrema<NQ>(a, t, mn, mx);
 }
 
 // ------------------------------------------------------------ key norms

@@ -39,7 +39,11 @@ struct Layout {
     // written only when the sample misjudges a query (the fallback word).
     bool fused;
     int sample_rows, sample_every;
-    size_t off_dist, off_tmin, off_tmax, off_cand, off_count, off_thr, off_best, off_ticket, off_fallback, total;
+    // Split select from group minima (the streaming distance kernels write
+    // each wave's smallest distance; no parts kernel): rows per group, or 0.
+    int group_rows;
+    size_t off_dist, off_tmin, off_tmax, off_cand, off_count, off_thr, off_best, off_ticket, off_fallback, off_gmin,
+        total;
 };
 
 // Whether a batch takes the fused select: the 128-query matrix-core kernel
@@ -77,7 +81,10 @@ Layout layout(int64_t B, int64_t d, int64_t S, int64_t max_keys, int64_t max_que
     // lists, and halves the sample pass and the threshold kernel's reads.)
     L.sample_rows = L.rows_per_tile / 8 > 256 ? L.rows_per_tile / 8 : 256;
     L.sample_every = 64 * L.sample_rows / L.rows_per_tile > 1 ? 64 * L.sample_rows / L.rows_per_tile : 1;
-    L.total = align_up(L.off_fallback + (L.fused ? sizeof(uint32_t) : 0));
+    L.group_rows = select_group_rows(B, L.ld, r, L.rows_per_tile, !mfma_shape(d, dtype, max_queries));
+    L.off_gmin = align_up(L.off_fallback + (L.fused ? sizeof(uint32_t) : 0));
+    const size_t gmin_words = L.group_rows > 0 ? static_cast<size_t>(B) * static_cast<size_t>(4 * L.tiles_per_set) : 0;
+    L.total = align_up(L.off_gmin + sizeof(float) * gmin_words);
     return L;
 }
 
@@ -226,6 +233,9 @@ SelectArgs select_args(const Call &c, const Layout &L, char *ws) {
     a.part_count = part_count;
     a.part_min = part_count ? part_count + L.split_parts * c.B : nullptr;
     a.part_thr = (ws && L.split_parts > 0) ? reinterpret_cast<uint32_t *>(ws + L.off_thr) : nullptr;
+    a.group_min = (ws && L.group_rows > 0) ? reinterpret_cast<const float *>(ws + L.off_gmin) : nullptr;
+    a.groups_per_set = 4 * L.tiles_per_set;
+    a.group_rows = L.group_rows;
     return a;
 }
 
@@ -267,6 +277,12 @@ knn_status run_part(const Call &c, int part, hipStream_t stream) {
         a.tiles_per_set = L.tiles_per_set;
         a.rows_per_tile = L.rows_per_tile;
         a.key_mask = c.key_mask;
+        if (ws && L.group_rows > 0) {  // the group minima, and the sliced finish's counters cleared
+            a.group_min = reinterpret_cast<float *>(ws + L.off_gmin);
+            a.groups_per_set = 4 * L.tiles_per_set;
+            a.zero_words = reinterpret_cast<uint32_t *>(ws + L.off_best);
+            a.n_zero_words = static_cast<int64_t>((L.off_ticket + sizeof(uint32_t) * c.B - L.off_best) / sizeof(uint32_t));
+        }
         if (!L.fused) return status_of(launch_distances(p, c.dtype, a, c.S, stream));
         uint32_t *fallback = reinterpret_cast<uint32_t *>(ws + L.off_fallback);
         if (!(p.mfma && p.mq == 8)) {  // (misaligned rows) the whole matrix, selected by the wide select

@@ -57,6 +57,15 @@ struct DistArgs {
     uint32_t *cand_count;        // [B] candidates listed so far
     uint64_t *cand_list;         // [B, kFusedCap] (distance bits << 32 | local key index)
     uint32_t *fallback;          // set to 1 when a candidate cannot be kept
+    // Streaming kernels: per query, the smallest unmasked distance of each
+    // wave's rows of each tile (group 4 t + w: rows r0 + w, r0 + w + 4, ... of
+    // tile t), [B, groups_per_set]; or null.
+    float *group_min;
+    int64_t groups_per_set;
+    // Words the select stage expects zero (its cross-workgroup counters),
+    // cleared by the launch's first workgroup; or null.
+    uint32_t *zero_words;
+    int64_t n_zero_words;
 };
 
 // Candidates per query of the fused select (the wide select's list capacity).

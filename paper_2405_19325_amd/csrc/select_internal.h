@@ -22,6 +22,13 @@ struct SelectArgs {
     uint32_t *part_count;        // split select: [B, parts] candidates per part
     uint32_t *part_min;          // split select: [B, parts] smallest candidate distance bits per part
     uint32_t *part_thr;          // split select: [B] threshold on the distance bits
+    // Split select from group minima: the smallest unmasked distance of every
+    // group of group_rows keys of a row ([B, groups_per_set], written by the
+    // distance stage; group 4 t + w: rows 4 group_rows t + w + 4 e, e <
+    // group_rows), or null.
+    const float *group_min;
+    int64_t groups_per_set;
+    int group_rows;
     // Gate: unless null, a wide-select launch does nothing when *gate != gate_run.
     const uint32_t *gate;
     uint32_t gate_run;
@@ -67,7 +74,7 @@ struct MixArgs {
     float delta;
     // Split select whose finish writes each row in slices (NEST outputs):
     // [B] each, the row's largest entry key and its workgroup count, cleared
-    // by the parts kernel; or null.
+    // by the parts kernel or (no parts kernel) by the distance stage; or null.
     uint64_t *best;
     uint32_t *ticket;
 };
@@ -87,6 +94,14 @@ constexpr int64_t kSplitMaxN = 65536;
 constexpr int kSplitMaxR = 1024;
 constexpr int64_t kSplitMaxBlocks = 256;
 int select_split_parts(int64_t B, int64_t ld, int r);
+// Split select from group minima (no parts kernel): the rows per key group
+// (4 or 8) when a batch of split rows is served by the streaming distance
+// kernels with rows_per_tile = 4 * group rows and every row of ld keys has at
+// least 2 r groups; else 0.  The finish reads each row's group minima, takes
+// as threshold the end of the histogram bin holding the r-th smallest (so at
+// least r keys lie below it), and gathers the keys of the groups below it.
+constexpr int kGroupMaxPerRow = 4 * kSelectThreads * 4;  // 16384: four 16-byte loads per thread
+int select_group_rows(int64_t B, int64_t ld, int r, int rows_per_tile, bool streaming);
 // Wide select: rows longer than kSplitMaxN keys are cut into parts (their
 // candidate lists use the split layout, [B, parts, kSplitKeys]) when r <= 2048
 // and the row has at least 2 r distance tiles; returns the parts per query

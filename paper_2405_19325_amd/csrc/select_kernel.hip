@@ -146,6 +146,9 @@ __device__ __forceinline__ float block_min(float v, float *red) {
 }
 
 // min and max of the per-thread values over the block (every thread gets both).
+// Without TAIL_BARRIER the caller must pass a barrier before sh.red_u is
+// written again.
+template <bool TAIL_BARRIER = true>
 __device__ __forceinline__ void block_minmax_u32(uint32_t &mn, uint32_t &mx, Shared &sh) {
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
@@ -163,7 +166,7 @@ __device__ __forceinline__ void block_minmax_u32(uint32_t &mn, uint32_t &mx, Sha
         mn = min(mn, sh.red_u[0][w]);
         mx = max(mx, sh.red_u[1][w]);
     }
-    __syncthreads();
+    if constexpr (TAIL_BARRIER) __syncthreads();
 }
 
 // Range of a query's distance bits from the distance stage's per-tile extrema.
@@ -939,8 +942,11 @@ __global__ __launch_bounds__(kT) void k_select_fast(SelectArgs a, MixArgs m) {
 }
 
 // Split path: rows of at most kSplitMaxN keys, r <= kSplitMaxR, few queries.
-// Query b's row is cut into `parts` parts of kSplitKeys keys so that one query
-// keeps many CUs busy; two kernels, and no atomics or fences between
+// Where the streaming distance kernels left group minima (16- or 32-row tiles,
+// at least 2 r groups a row) and the finish runs without a mixture or in
+// vocabulary slices, the finish alone selects from them (GROUPS below).
+// Otherwise query b's row is cut into `parts` parts of kSplitKeys keys so that
+// one query keeps many CUs busy; two kernels, and no atomics or fences between
 // workgroups (the kernel boundary orders them).
 //
 // Parts kernel (blockIdx.x = b * parts + part): every part of query b reads
@@ -1112,8 +1118,20 @@ __device__ __forceinline__ void finish_sort(uint64_t *cand, uint32_t total, uint
                                              NoHook(), keep);
 }
 
-template <int MODE, bool SLICED>
+// GROUPS: no parts kernel.  The finish reads the row's group minima (from the
+// distance stage: group 4 t + w holds the rows of distance tile t that wave w
+// of the streaming kernel took, rows 4 gr t + w + 4 e for e < gr), takes as
+// threshold the end of the histogram bin holding the r-th smallest of them, so
+// that at least r groups, hence at least r keys, lie below it, lists in LDS
+// the groups whose minimum is below it (a group whose minimum is not below it
+// holds no key below it), loads those groups' distances, and keeps the keys
+// below the threshold.  Then the same sort, fallback and mixture.
+constexpr int kGroupItems = 12;                          // distances of listed groups loaded per thread
+constexpr int kGroupList = kGroupItems * kT / 4;         // listed groups kept (of at least 4 keys each)
+
+template <int MODE, bool SLICED, bool GROUPS, int GL = 0>
 __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, int parts, int slices) {
+    static_assert(!GROUPS || GL == 2 || GL == 4, "GL 16-byte loads of group minima per thread");
     constexpr bool MIX = MODE != kNoMix;
     static_assert(!SLICED || MIX, "slices are of the p_M row");
     constexpr int PER = kSplitCap / kT;
@@ -1129,6 +1147,11 @@ __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, i
     // sliced: the slice's tile, over the sort's scratch (dead once the sort returns)
     float *acc_s = reinterpret_cast<float *>(tmp);
     static_assert(kVocabSlice * 4 <= kSplitCap * 8, "the slice's tile fits over the sort scratch");
+    // GROUPS: the minima's histogram and the list of groups below the
+    // threshold, over the sort's scratch too (both dead before the sort)
+    uint32_t *ghist = reinterpret_cast<uint32_t *>(tmp);                           // [kSelectBins]
+    uint32_t *glist = ghist + kSelectBins;                                         // [kGroupList]
+    static_assert((kSelectBins + kGroupList) * 4 <= kSplitCap * 8, "histogram and list fit the sort scratch");
     __shared__ Shared sh;
     __shared__ uint32_t part_off[kWave + 1];
 
@@ -1138,18 +1161,36 @@ __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, i
     const int g = SLICED ? static_cast<int>(blockIdx.x - b * slices) : 0;  // the row's slice
     const int32_t dtok = draft_token<MODE>(m, b);
     const uint64_t *lists = a.cand + b * parts * kSplitKeys;
+    const float *drow = a.dist + b * a.ld;
 
-    // Counts, threshold and the first `win` entries of every list, all in flight together.
-    const uint32_t win = static_cast<uint32_t>(kSplitCap / parts);
-    const uint32_t cnt = (tid < kWave && lane < parts) ? a.part_count[b * parts + lane] : 0u;
-    const uint32_t pmin = (tid < kWave && lane < parts) ? a.part_min[b * parts + lane] : ~0u;
-    const uint32_t thr = a.part_thr[b];
+    // Lists: counts, threshold and the first `win` entries of every list, all
+    // in flight together.  Groups: the row's group minima.
+    const uint32_t win = GROUPS ? 0u : static_cast<uint32_t>(kSplitCap / parts);
+    uint32_t cnt = 0u, pmin = ~0u, thr = 0u;
     uint64_t key[PER];
+    uint4 gv[GROUPS ? GL : 1];
+    if constexpr (GROUPS) {
+        const int64_t nq4 = a.groups_per_set / 4;  // 16-byte words of a row's minima (groups_per_set % 4 == 0)
+        const uint4 *gm = reinterpret_cast<const uint4 *>(a.group_min + b * a.groups_per_set);
 #pragma unroll
-    for (int q = 0; q < PER; ++q) {
-        const uint32_t e = static_cast<uint32_t>(q * kT + tid);
-        const uint32_t p = e / win;
-        key[q] = p < static_cast<uint32_t>(parts) ? lists[p * kSplitKeys + (e - p * win)] : ~0ull;
+        for (int u = 0; u < GL; ++u) {
+            const int64_t i = static_cast<int64_t>(u) * kT + tid;
+            gv[u] = gm[i < nq4 ? i : 0];  // unconditional: words past the row reread its first
+        }
+        if (tid == 0) {
+            sh.total = 0u;
+            sh.ccount = 0u;
+        }
+    } else {
+        cnt = (tid < kWave && lane < parts) ? a.part_count[b * parts + lane] : 0u;
+        pmin = (tid < kWave && lane < parts) ? a.part_min[b * parts + lane] : ~0u;
+        thr = a.part_thr[b];
+#pragma unroll
+        for (int q = 0; q < PER; ++q) {
+            const uint32_t e = static_cast<uint32_t>(q * kT + tid);
+            const uint32_t p = e / win;
+            key[q] = p < static_cast<uint32_t>(parts) ? lists[p * kSplitKeys + (e - p * win)] : ~0ull;
+        }
     }
     // The p_LM entries this workgroup mixes: its slice, or the row's first tile
     // (loaded during the write-out below).
@@ -1163,20 +1204,126 @@ __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, i
     const uint32_t r_eff = static_cast<uint32_t>(N < a.r ? N : a.r);
     // Bucket counts to clear while the loads are in flight.
     for (int i = tid; i < (1 << kFinishBinsLog2); i += kT) hist[i] = 0u;
-    if (tid < kWave) {  // list starts, and whether any list is longer than its window
-        const uint32_t incl = wave_incl_scan_u32(cnt, lane);
-        if (lane < parts) part_off[lane] = incl - cnt;
-        if (lane == parts - 1) part_off[parts] = incl;
-        const uint32_t longest = wave_allmax_u32(cnt);
-        const uint32_t cmin = wave_allmin_u32(pmin);
-        if (lane == 0) {
-            sh.found = longest > win ? 1u : 0u;
-            sh.cmin = cmin;  // the smallest candidate distance bits
+    uint32_t total, lo;
+    bool fast;
+    if constexpr (GROUPS) {
+        for (int i = tid; i < kSelectBins; i += kT) ghist[i] = 0u;
+        const int gr = a.group_rows;  // 4 or 8
+        // every group of the tiles that hold the row's keys (a group of the
+        // last tile may hold no key: its minimum is then +infinity)
+        const uint32_t ng = static_cast<uint32_t>((N + 4 * gr - 1) / (4 * gr) * 4);
+        // groups past the row read as all-ones, above +infinity (masked keys) and any threshold
+        uint32_t gmn = ~0u, gmx = 0u;
+#pragma unroll
+        for (int u = 0; u < GL; ++u) {
+            const uint32_t g0 = static_cast<uint32_t>(u * kT + tid) * 4u;
+            gv[u].x = g0 < ng ? gv[u].x : ~0u;
+            gv[u].y = g0 + 1u < ng ? gv[u].y : ~0u;
+            gv[u].z = g0 + 2u < ng ? gv[u].z : ~0u;
+            gv[u].w = g0 + 3u < ng ? gv[u].w : ~0u;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const uint32_t v = lane_word(gv[u], e);
+                gmn = v < kMaskedBits ? min(gmn, v) : gmn;
+                gmx = v < kMaskedBits ? max(gmx, v) : gmx;
+            }
         }
+        block_minmax_u32<false>(gmn, gmx, sh);  // its barrier also orders the clears above
+        lo = gmn;
+        if (gmn <= gmx) {
+            const uint32_t w = gmx + 1u - gmn;
+            const int shift = range_shift(w);
+#pragma unroll
+            for (int u = 0; u < GL; ++u)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const uint32_t v = lane_word(gv[u], e);
+                    if (v < kMaskedBits) atomicAdd(&ghist[(v - gmn) >> shift], 1u);
+                }
+            __syncthreads();
+            if (tid < kWave) {
+                // fewer than r groups: every unmasked key (then more than the sort holds, or all of them)
+                const uint32_t j = wave_pick_bin(ghist, r_eff > 0 ? r_eff : 1u, lane);
+                const uint64_t end = static_cast<uint64_t>(gmn) + ((static_cast<uint64_t>(j) + 1u) << shift);
+                if (lane == 0) sh.hi = j == ~0u ? kMaskedBits : static_cast<uint32_t>(end < gmx + 1ull ? end : gmx + 1ull);
+            }
+            __syncthreads();
+            thr = sh.hi;
+        }
+        // The groups below the threshold, listed in LDS (each wave reserves its slots with one LDS atomic).
+        {
+            uint32_t c = 0u;
+#pragma unroll
+            for (int u = 0; u < GL; ++u)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) c += lane_word(gv[u], e) < thr ? 1u : 0u;
+            const uint32_t incl = wave_incl_scan_u32(c, lane);
+            const uint32_t wtot = readlane_u32(incl, kWave - 1);
+            uint32_t base = 0u;
+            if (lane == 0 && wtot > 0u) base = atomicAdd(&sh.total, wtot);
+            uint32_t pos = readlane_u32(base, 0) + incl - c;
+#pragma unroll
+            for (int u = 0; u < GL; ++u)
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (lane_word(gv[u], e) < thr) {
+                        if (pos < static_cast<uint32_t>(kGroupList)) glist[pos] = static_cast<uint32_t>(u * kT + tid) * 4u + e;
+                        ++pos;
+                    }
+        }
+        __syncthreads();
+        // The listed groups' distances, one word per key, all in flight
+        // together: group 4 t + w holds rows 4 gr t + w + 4 e, e < gr, of the row.
+        const uint32_t items = sh.total * static_cast<uint32_t>(gr);
+        const bool fits = items <= static_cast<uint32_t>(kGroupItems * kT);
+        const int lg = gr == 8 ? 3 : 2;
+        uint32_t dv[kGroupItems];
+        uint32_t key_of[kGroupItems];  // each word's key index (N: none)
+#pragma unroll
+        for (int u = 0; u < kGroupItems; ++u) {
+            const uint32_t i = static_cast<uint32_t>(u * kT + tid);
+            const bool in = i < items && fits;
+            const uint32_t gi = in ? glist[i >> lg] : 0u;
+            const uint32_t row = ((gi >> 2) << (lg + 2)) + (gi & 3u) + 4u * (i & static_cast<uint32_t>(gr - 1));
+            key_of[u] = in ? row : static_cast<uint32_t>(N);
+            dv[u] = __float_as_uint(drow[in ? row : 0u]);  // unconditional: the row's first word otherwise
+        }
+        // The keys below the threshold, into the sort's buffer (each with its slot).
+        uint32_t c = 0u;
+#pragma unroll
+        for (int u = 0; u < kGroupItems; ++u) c += (key_of[u] < N && dv[u] < thr) ? 1u : 0u;
+        const uint32_t incl = wave_incl_scan_u32(c, lane);
+        const uint32_t wtot = readlane_u32(incl, kWave - 1);
+        uint32_t base = 0u;
+        if (lane == 0 && wtot > 0u) base = atomicAdd(&sh.ccount, wtot);
+        uint32_t pos = readlane_u32(base, 0) + incl - c;
+#pragma unroll
+        for (int u = 0; u < kGroupItems; ++u)
+            if (key_of[u] < N && dv[u] < thr) {
+                if (pos < static_cast<uint32_t>(kSplitCap))
+                    cand[pos] = (static_cast<uint64_t>(dv[u]) << 32) | (static_cast<uint64_t>(key_of[u]) << 12) | pos;
+                ++pos;
+            }
+        __syncthreads();  // the candidates are in LDS
+        total = sh.ccount;
+        fast = fits && total >= r_eff && total <= static_cast<uint32_t>(kSplitCap);
+    } else {
+        if (tid < kWave) {  // list starts, and whether any list is longer than its window
+            const uint32_t incl = wave_incl_scan_u32(cnt, lane);
+            if (lane < parts) part_off[lane] = incl - cnt;
+            if (lane == parts - 1) part_off[parts] = incl;
+            const uint32_t longest = wave_allmax_u32(cnt);
+            const uint32_t cmin = wave_allmin_u32(pmin);
+            if (lane == 0) {
+                sh.found = longest > win ? 1u : 0u;
+                sh.cmin = cmin;  // the smallest candidate distance bits
+            }
+        }
+        __syncthreads();
+        total = part_off[parts];
+        lo = sh.cmin;
+        fast = total >= r_eff && total <= static_cast<uint32_t>(kSplitCap);
     }
-    __syncthreads();
-    const uint32_t total = part_off[parts];
-    const bool fast = total >= r_eff && total <= static_cast<uint32_t>(kSplitCap);
 
     uint64_t x = ~0ull;
     uint32_t id = 0;
@@ -1188,36 +1335,47 @@ __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, i
     if (fast) {
         uint32_t slot[PER];
         bool valid[PER];
-        const uint32_t lo = sh.cmin;
-#pragma unroll
-        for (int q = 0; q < PER; ++q) {
-            const uint32_t e = static_cast<uint32_t>(q * kT + tid);
-            const uint32_t p = e / win;
-            const uint32_t pc = p < static_cast<uint32_t>(parts) ? p : static_cast<uint32_t>(parts - 1);
-            const uint32_t i = e - p * win;
-            const uint32_t start = part_off[pc], end = part_off[pc + 1];
-            valid[q] = p < static_cast<uint32_t>(parts) && i < end - start;
-            slot[q] = start + i;
-            if (valid[q]) cand[slot[q]] = key[q] | slot[q];
-        }
-        // Tokens: unconditional loads (an invalid entry reads key 0's), so
-        // that nothing waits for them before the sort needs them.
         int32_t tv[PER];
+        if constexpr (GROUPS) {
+            // Tokens of the listed keys: unconditional loads (past the list, key 0's).
 #pragma unroll
-        for (int q = 0; q < PER; ++q)
-            tv[q] = MIX ? m.values[k0 + (valid[q] ? (static_cast<uint32_t>(key[q]) >> 12) : 0u)] : -1;
-        if (sh.found != 0u) {  // longer lists: the rest, one part after another (rare)
-            for (int p = 0; p < parts; ++p) {
-                const uint32_t n_p = part_off[p + 1] - part_off[p];
-                for (uint32_t i = win + tid; i < n_p; i += kT) {
-                    const uint64_t k = lists[p * kSplitKeys + i];
-                    const uint32_t sl = part_off[p] + i;
-                    cand[sl] = k | sl;
-                    if constexpr (MIX) tok_of[sl] = m.values[k0 + (static_cast<uint32_t>(k) >> 12)];
+            for (int q = 0; q < PER; ++q) {
+                const uint32_t e = static_cast<uint32_t>(q * kT + tid);
+                valid[q] = e < total;
+                slot[q] = e;
+                const uint32_t i = valid[q] ? static_cast<uint32_t>(cand[e]) >> 12 : 0u;
+                tv[q] = MIX ? m.values[k0 + i] : -1;
+            }
+        } else {
+#pragma unroll
+            for (int q = 0; q < PER; ++q) {
+                const uint32_t e = static_cast<uint32_t>(q * kT + tid);
+                const uint32_t p = e / win;
+                const uint32_t pc = p < static_cast<uint32_t>(parts) ? p : static_cast<uint32_t>(parts - 1);
+                const uint32_t i = e - p * win;
+                const uint32_t start = part_off[pc], end = part_off[pc + 1];
+                valid[q] = p < static_cast<uint32_t>(parts) && i < end - start;
+                slot[q] = start + i;
+                if (valid[q]) cand[slot[q]] = key[q] | slot[q];
+            }
+            // Tokens: unconditional loads (an invalid entry reads key 0's), so
+            // that nothing waits for them before the sort needs them.
+#pragma unroll
+            for (int q = 0; q < PER; ++q)
+                tv[q] = MIX ? m.values[k0 + (valid[q] ? (static_cast<uint32_t>(key[q]) >> 12) : 0u)] : -1;
+            if (sh.found != 0u) {  // longer lists: the rest, one part after another (rare)
+                for (int p = 0; p < parts; ++p) {
+                    const uint32_t n_p = part_off[p + 1] - part_off[p];
+                    for (uint32_t i = win + tid; i < n_p; i += kT) {
+                        const uint64_t k = lists[p * kSplitKeys + i];
+                        const uint32_t sl = part_off[p] + i;
+                        cand[sl] = k | sl;
+                        if constexpr (MIX) tok_of[sl] = m.values[k0 + (static_cast<uint32_t>(k) >> 12)];
+                    }
                 }
             }
+            __syncthreads();  // the candidates are in LDS
         }
-        __syncthreads();  // the candidates are in LDS
         if (total <= static_cast<uint32_t>(kSplitCap / 2))
             finish_sort<PER / 2>(cand, total, lo, thr, hist, tmp, sh, r_eff);
         else
@@ -1815,6 +1973,26 @@ hipError_t launch_sel(const SelectArgs &a, const MixArgs &m, int64_t B, hipStrea
         const int64_t slices = MIX ? (m.V + kVocabSlice - 1) / kVocabSlice : 1;
         const bool sliced = MIX && B * slices <= kSliceMaxBlocks &&
                             (MODE != kMixNest || (m.best != nullptr && m.ticket != nullptr));
+        if (a.group_min != nullptr && (!MIX || sliced)) {  // no parts kernel: the finish reads the group minima
+            if (a.group_rows != 4 && a.group_rows != 8) return hipErrorInvalidValue;
+            if (a.groups_per_set % 4 != 0 || a.groups_per_set > kGroupMaxPerRow) return hipErrorInvalidValue;
+            const bool wide = a.groups_per_set > 2 * 4 * kT;  // more than two 16-byte words of minima per thread
+            if constexpr (MIX) {
+                const dim3 sgrid(static_cast<unsigned>(B * slices));
+                if (wide)
+                    hipLaunchKernelGGL((k_select_finish<MODE, true, true, 4>), sgrid, block, 0, st, a, m, 0,
+                                       static_cast<int>(slices));
+                else
+                    hipLaunchKernelGGL((k_select_finish<MODE, true, true, 2>), sgrid, block, 0, st, a, m, 0,
+                                       static_cast<int>(slices));
+            } else {
+                if (wide)
+                    hipLaunchKernelGGL((k_select_finish<MODE, false, true, 4>), grid, block, 0, st, a, m, 0, 1);
+                else
+                    hipLaunchKernelGGL((k_select_finish<MODE, false, true, 2>), grid, block, 0, st, a, m, 0, 1);
+            }
+            return hipGetLastError();
+        }
         const dim3 pgrid(static_cast<unsigned>(B * parts));
         if constexpr (MODE == kMixFixed) {  // the dense term: in the parts kernel unless the finish is sliced
             if (sliced)
@@ -1828,12 +2006,12 @@ hipError_t launch_sel(const SelectArgs &a, const MixArgs &m, int64_t B, hipStrea
         if (e != hipSuccess) return e;
         if constexpr (MIX) {
             if (sliced) {
-                hipLaunchKernelGGL((k_select_finish<MODE, true>), dim3(static_cast<unsigned>(B * slices)), block, 0,
+                hipLaunchKernelGGL((k_select_finish<MODE, true, false>), dim3(static_cast<unsigned>(B * slices)), block, 0,
                                    st, a, m, parts, static_cast<int>(slices));
                 return hipGetLastError();
             }
         }
-        hipLaunchKernelGGL((k_select_finish<MODE, false>), grid, block, 0, st, a, m, parts, 1);
+        hipLaunchKernelGGL((k_select_finish<MODE, false, false>), grid, block, 0, st, a, m, parts, 1);
         return hipGetLastError();
     }
     const int wparts = select_wide_parts(B, a.ld, a.r, a.tiles_per_set);
@@ -1864,6 +2042,15 @@ int select_split_parts(int64_t B, int64_t ld, int r) {
     if (B < 1 || ld < 1 || ld > kSplitMaxN || r > kSplitMaxR) return 0;
     const int64_t parts = (ld + kSplitKeys - 1) / kSplitKeys;
     return B * parts <= kSplitMaxBlocks ? static_cast<int>(parts) : 0;
+}
+
+int select_group_rows(int64_t B, int64_t ld, int r, int rows_per_tile, bool streaming) {
+    if (!streaming || select_split_parts(B, ld, r) == 0) return 0;
+    if (rows_per_tile != 16 && rows_per_tile != 32) return 0;
+    const int gr = rows_per_tile / 4;  // the streaming kernels' four waves each take a quarter of a tile
+    const int64_t groups = ld / gr;
+    if (groups > kGroupMaxPerRow || groups < 2 * static_cast<int64_t>(r)) return 0;
+    return gr;
 }
 
 int select_wide_parts(int64_t B, int64_t ld, int r, int64_t tiles_per_set) {

@@ -181,3 +181,35 @@ def test_packed_dtype_validation(lib):
         UNSUPPORTED
     assert lib.knn_distances(FAKE, FAKE, None, FAKE, FAKE, 16, 1024, 1, 100, 16, KEYS_PACKED, FAKE, 100, None) == \
         INVALID
+
+
+def test_select_path_rules_match_the_workspace_layout(lib):
+    """The tests' restatement of which split rows take the group-minima select
+    (tests/select_paths.py) against the library: the workspace holds B * 4 *
+    tiles fp32 group minima exactly when it says so."""
+    import select_paths
+
+    def ws(**over):
+        return _ws_size(lib, dict(BASE, **over))
+
+    # decode shape: 32-row tiles, 8192 groups of 8 rows: on for every r <= 1024
+    assert select_paths.group_rows(1, 4096, 2, 1, 65536, 1, 1024) == 8
+    # 4096 keys in 16-row tiles: 1024 groups of 4 rows, so r <= 512
+    small = dict(total_keys=4096, min_keys=4096, max_keys=4096)
+    assert select_paths.tile_rows(4096, 2, 1, 4096) == 16
+    assert select_paths.group_rows(1, 4096, 2, 1, 4096, 1, 512) == 4
+    assert select_paths.group_rows(1, 4096, 2, 1, 4096, 1, 513) == 0
+    assert ws(r=512, **small) - ws(r=513, **small) == 1024 * 4
+    # three queries: three rows of minima
+    assert ws(B=3, max_queries=3, r=512, **small) - ws(B=3, max_queries=3, r=513, **small) == 3 * 1024 * 4
+    # 16 bf16 queries on a set take the matrix cores: no group minima
+    assert select_paths.group_rows(16, 4096, 2, 1, 4096, 16, 512) == 0
+    assert ws(B=16, max_queries=16, r=512, **small) == ws(B=16, max_queries=16, r=513, **small)
+    # fp32 keys of width 16 on 40,000-key rows: 16-row tiles, 10,000 groups of 4
+    assert select_paths.tile_rows(16, 4, 1, 40000) == 16
+    assert select_paths.group_rows(1, 16, 4, 1, 40000, 1, 1024) == 4
+    # 64-row tiles (many sets): the parts kernel samples the rows
+    many = dict(B=32, S=32, d=256, total_keys=32 * 4096, min_keys=4096, max_keys=4096, max_queries=1, r=256)
+    assert select_paths.tile_rows(256, 2, 32, 4096) == 64
+    assert select_paths.split_path(32, 256, 2, 32, 4096, 1, 256, V=32000) == "parts"
+    assert ws(**many) == ws(**dict(many, r=255))

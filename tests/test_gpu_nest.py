@@ -330,9 +330,9 @@ def test_nest_step_synthetic_workloads(name, spec, seed):
 
 
 def test_steps_replay_from_graphs():
-    """The fixed-lambda step and the NEST step (split select, finish in
-    vocabulary slices with its cross-slice maximum and count, which the parts
-    kernel clears, so no memset) captured in HIP graphs: three rounds of
+    """The fixed-lambda step and the NEST step (split select from group
+    minima, finish in vocabulary slices with its cross-slice maximum and
+    count, which the distance stage clears, so no memset) captured in HIP graphs: three rounds of
     replays, with eager steps and synchronisations between and every output
     overwritten before each replay, each equal to the eager results: ids,
     distances and decisions exactly, p_M and the p_M values among the outputs
