@@ -33,7 +33,9 @@
 // in LDS vocabulary tiles with LDS float atomics (tokens no neighbour carries
 // get 0; duplicates accumulate), then p_M = fmaf(lambda, p_LM, acc * ((1 -
 // lambda) / Z)), so lambda = 1 returns p_LM bit for bit.  The order of the LDS
-// atomics is not fixed, so p_kNN may differ between runs in the last bits.
+// atomics is not fixed, so p_kNN may differ between runs in the last bits,
+// except in the split select's sliced finish, which adds the weights as 64-bit
+// fixed-point integers (weight * 2^31, exact) and rounds each sum to fp32 once.
 // With relative retrieval confidence (Section 3.2, eq. rrc) lambda is each
 // query's own lambda_t = sigmoid((d_(1) / d_(r) - alpha) / tau), from the
 // nearest and the r-th nearest distance (|s| is the distance); the split path
@@ -1118,6 +1120,21 @@ __device__ __forceinline__ void finish_sort(uint64_t *cand, uint32_t total, uint
                                              NoHook(), keep);
 }
 
+// Zeroes the sliced finish's fixed-point vocabulary tile (32 bytes per thread).
+__device__ __forceinline__ void clear_slice_tile(uint64_t *acc_s) {
+    static_assert(kVocabSlice == 4 * kT, "four entries per thread");
+    const uint4 z = make_uint4(0u, 0u, 0u, 0u);
+    reinterpret_cast<uint4 *>(acc_s)[2 * threadIdx.x] = z;
+    reinterpret_cast<uint4 *>(acc_s)[2 * threadIdx.x + 1] = z;
+}
+
+// The nonnegative 64-bit integer (hi << 32 | lo), below 2^42, in fp32: hi is
+// exact in fp32 and hi * 2^32 + fp32(lo) is rounded once more (within an ulp
+// of the integer; the same bits for the same integer).
+__device__ __forceinline__ float fixed_to_float(uint32_t lo, uint32_t hi) {
+    return fmaf(static_cast<float>(hi), 4294967296.0f, static_cast<float>(lo));
+}
+
 // GROUPS: no parts kernel.  The finish reads the row's group minima (from the
 // distance stage: group 4 t + w holds the rows of distance tile t that wave w
 // of the streaming kernel took, rows 4 gr t + w + 4 e for e < gr), takes as
@@ -1144,9 +1161,14 @@ __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, i
     uint32_t *hist = reinterpret_cast<uint32_t *>(tmp + kSplitCap);                // [2 << kFinishBinsLog2]: counts, starts
     int32_t *tok_of = reinterpret_cast<int32_t *>(smem + kSortBytes);              // [kSplitCap]
     float *acc = reinterpret_cast<float *>(smem);  // mixture: a vocabulary tile, over everything above
-    // sliced: the slice's tile, over the sort's scratch (dead once the sort returns)
-    float *acc_s = reinterpret_cast<float *>(tmp);
-    static_assert(kVocabSlice * 4 <= kSplitCap * 8, "the slice's tile fits over the sort scratch");
+    // sliced: the slice's tile in fixed point (weight * 2^31, 64-bit integer
+    // LDS atomics: exact, so independent of their order, and faster than fp32
+    // LDS atomics where many neighbours share a token) over the sort's scratch,
+    // then in fp32 over the bucket counts (both dead once the sort returns)
+    uint64_t *acc_s = tmp;
+    float *acc_f = reinterpret_cast<float *>(hist);
+    static_assert(kVocabSlice * 8 <= kSplitCap * 8 && kVocabSlice * 4 <= (8 << kFinishBinsLog2),
+                  "the slice's tiles fit over the sort scratch and the bucket counts");
     // GROUPS: the minima's histogram and the list of groups below the
     // threshold, over the sort's scratch too (both dead before the sort)
     uint32_t *ghist = reinterpret_cast<uint32_t *>(tmp);                           // [kSelectBins]
@@ -1384,7 +1406,7 @@ __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, i
 #pragma unroll
             for (int q = 0; q < PER; ++q)
                 if (valid[q]) tok_of[slot[q]] = tv[q];
-            if constexpr (SLICED) reinterpret_cast<float4 *>(acc_s)[tid] = make_float4(0.f, 0.f, 0.f, 0.f);
+            if constexpr (SLICED) clear_slice_tile(acc_s);
             __syncthreads();
         }
         x = ok ? cand[tid] : ~0ull;
@@ -1401,7 +1423,7 @@ __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, i
         id = static_cast<uint32_t>(x);
         if (MIX && ok) tok = m.values[k0 + id];
         if constexpr (SLICED) {
-            reinterpret_cast<float4 *>(acc_s)[tid] = make_float4(0.f, 0.f, 0.f, 0.f);
+            clear_slice_tile(acc_s);
             __syncthreads();
         }
     }
@@ -1420,7 +1442,11 @@ __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, i
         const float wj = ok ? expf(-m.mu * (dj - d0)) : 0.0f;
         const int64_t c0 = static_cast<int64_t>(g) * kVocabSlice;  // sliced: this workgroup's entries
         if constexpr (SLICED) {
-            if (tok >= c0 && tok < c0 + kVocabSlice) atomicAdd(&acc_s[tok - c0], wj);
+            // wj <= 1, so wj * 2^31 fits 32 bits; it is an integer for wj >= 2^-8 (conversion exact) and
+            // loses less than 2^-31 below; r such terms stay below 2^42
+            if (tok >= c0 && tok < c0 + kVocabSlice)
+                atomicAdd(reinterpret_cast<unsigned long long *>(acc_s + (tok - c0)),
+                          static_cast<unsigned long long>(static_cast<uint32_t>(wj * 2147483648.0f)));
         }
         // Z; the barrier also ends every use of the sort buffers, which an
         // unsliced vocabulary tile then takes over, and orders a slice's
@@ -1438,7 +1464,16 @@ __global__ __launch_bounds__(kT) void k_select_finish(SelectArgs a, MixArgs m, i
         if constexpr (SLICED) {
             // this workgroup's slice of the row, with any lambda
             const int64_t c1 = m.V - c0 < kVocabSlice ? m.V : c0 + kVocabSlice;
-            mix_row<1, kVocabSlice, MODE == kMixNest, true, true, true>(w1, t1, k1, z, lam, m, b, acc_s, pre, dtok,
+            // each thread's four entries back to fp32 (the row writer's 16-byte path reads its own
+            // 16 bytes; its 4-byte path, entries tid + 1024 k, needs a barrier)
+            const uint4 e01 = reinterpret_cast<const uint4 *>(acc_s)[2 * tid];
+            const uint4 e23 = reinterpret_cast<const uint4 *>(acc_s)[2 * tid + 1];
+            constexpr float kInv = 1.0f / 2147483648.0f;
+            reinterpret_cast<float4 *>(acc_f)[tid] =
+                make_float4(fixed_to_float(e01.x, e01.y) * kInv, fixed_to_float(e01.z, e01.w) * kInv,
+                            fixed_to_float(e23.x, e23.y) * kInv, fixed_to_float(e23.z, e23.w) * kInv);
+            if (!mix_vec4(m, b)) __syncthreads();
+            mix_row<1, kVocabSlice, MODE == kMixNest, true, true, true>(w1, t1, k1, z, lam, m, b, acc_f, pre, dtok,
                                                                         c0, c1, slices, g == 0);
             return;
         } else if constexpr (rrc_mode(MODE)) {
