@@ -75,7 +75,7 @@ constexpr bool rrc_mode(int mode) { return mode == kMixRrc || mode == kMixNest; 
 
 struct Shared {
     uint32_t red_u[2][kNumWaves];
-    uint32_t wave_tot[kNumWaves];
+    alignas(16) uint32_t wave_tot[kNumWaves];
     float red_f[kNumWaves];
     uint32_t lo, hi, below, cnt, found, total;
     uint32_t ccount, cmin;  // split path: a part's candidates so far, and their smallest distance bits
@@ -103,21 +103,26 @@ __device__ __forceinline__ uint64_t sort_key(uint32_t dbits, uint32_t i) {
     return (static_cast<uint64_t>(dbits) << 32) | i;
 }
 
-// Exclusive prefix sum of one value per thread over the block.
+// Exclusive prefix sum of one value per thread over the block: a scan within
+// each wave, then every wave adds the totals of the waves before it (one
+// barrier between).  Without TAIL_BARRIER the caller must pass a barrier
+// before wave_tot is written again.
+template <bool TAIL_BARRIER = true>
 __device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t *wave_tot) {
+    static_assert(kNumWaves % 4 == 0, "whole 16-byte words of wave totals");
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
     const uint32_t incl = wave_incl_scan_u32(v, lane);
     if (lane == kWave - 1) wave_tot[wave] = incl;
     __syncthreads();
-    if (wave == 0) {
-        uint32_t t = lane < kNumWaves ? wave_tot[lane] : 0u;
-        t = wave_incl_scan_u32(t, lane);
-        if (lane < kNumWaves) wave_tot[lane] = t;  // inclusive totals
+    uint32_t before = 0u;
+#pragma unroll
+    for (int i = 0; i < kNumWaves / 4; ++i) {
+        const uint4 t = reinterpret_cast<const uint4 *>(wave_tot)[i];
+        before += (4 * i < wave ? t.x : 0u) + (4 * i + 1 < wave ? t.y : 0u) + (4 * i + 2 < wave ? t.z : 0u) +
+                  (4 * i + 3 < wave ? t.w : 0u);
     }
-    __syncthreads();
-    const uint32_t before = wave == 0 ? 0u : wave_tot[wave - 1];
-    __syncthreads();  // wave_tot may be reused right after
+    if constexpr (TAIL_BARRIER) __syncthreads();
     return before + incl - v;
 }
 
@@ -282,12 +287,6 @@ __device__ __forceinline__ void lds_bitonic(uint64_t *cand, uint32_t P) {
     }
 }
 
-// Ascending sort of the n <= PER * 1024 keys in cand[0, n), in place, by
-// buckets of their distance bits over [lo, lo + w): each key takes a slot in
-// its bucket with an LDS atomic, a block scan turns bucket sizes into bucket
-// starts, the keys are scattered to tmp, and each key's final place is its
-// bucket start plus its rank among the (few) keys of its bucket.  A bucket
-// holding many equal distances only costs time, never order.
 struct NoHook {
     __device__ void operator()() const {}
 };
@@ -296,8 +295,9 @@ struct NoHook {
 // 2^BLOG buckets of their distance bits over [lo, lo + w): each key takes a
 // slot in its bucket with an LDS atomic, a block scan turns bucket sizes into
 // bucket starts, the keys are scattered to tmp, and each key's final place is
-// its bucket start plus its rank among the (few) keys of its bucket (the first
-// eight compared at once; reads past the bucket are discarded).  A bucket
+// its bucket start plus its rank among the (few) keys of its bucket (a key
+// alone in its bucket compares nothing; otherwise the first eight are compared
+// at once, reads past the bucket discarded).  A bucket
 // holding many equal distances only costs time, never order.  With ZEROED the
 // caller has cleared count[] and ordered that with a barrier.  `mid` runs
 // between the scan and the scatter (callers issue loads there that the rest
@@ -333,7 +333,7 @@ __device__ __forceinline__ void bucket_sort(uint64_t *cand, uint32_t n, uint32_t
         cb[i] = count[BPT * tid + i];
         tsum += cb[i];
     }
-    uint32_t run = block_excl_scan(tsum, sh.wave_tot);
+    uint32_t run = block_excl_scan<false>(tsum, sh.wave_tot);  // the barrier below ends its reads
 #pragma unroll
     for (int i = 0; i < BPT; ++i) {
         start[BPT * tid + i] = run;
@@ -354,10 +354,12 @@ __device__ __forceinline__ void bucket_sort(uint64_t *cand, uint32_t n, uint32_t
     }
 #pragma unroll
     for (int q = 0; q < PER; ++q) {
+        if (nb[q] > 1u) {
 #pragma unroll
-        for (uint32_t i = 0; i < 8; ++i) {
-            const uint32_t at = b0[q] + i < static_cast<uint32_t>(PER * kT) ? b0[q] + i : PER * kT - 1;
-            rank[q] += (i < nb[q] && tmp[at] < key[q]) ? 1u : 0u;
+            for (uint32_t i = 0; i < 8; ++i) {
+                const uint32_t at = b0[q] + i < static_cast<uint32_t>(PER * kT) ? b0[q] + i : PER * kT - 1;
+                rank[q] += (i < nb[q] && tmp[at] < key[q]) ? 1u : 0u;
+            }
         }
     }
 #pragma unroll
