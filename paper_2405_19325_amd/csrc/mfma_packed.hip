@@ -33,7 +33,15 @@
 //           query prefetch would make every wait for it a wait for all older
 //           key loads as well, and the key ring would be as shallow as the
 //           query prefetch (measured at 128 queries x 8.4 M keys of d = 1024:
-//           4.0 ms with a two-step query prefetch, 3.0 ms in the key ring).
+//           4.0 ms with a two-step query prefetch, 3.0 ms in the key ring);
+//   QM = 2: (128-query groups, four dividing the steps per pass) each step's
+//           span loads straight into one of four LDS buffers three steps
+//           ahead, so no registers hold it and the barrier that ends a step
+//           waits only for loads issued two steps before (the kernel counts
+//           those waits itself: the loads are assembly, load_to_lds_16); the
+//           loop is unrolled over the four buffers, so every buffer address is
+//           fixed (2-3% faster than QM 1 at the shape above; a barrier every
+//           second step over eight buffers spilled registers and was no faster).
 // Every step does the same MFMAs in the same k order as the row-major kernel,
 // and ||k||^2 and ||q||^2 are accumulated over the same fragments in the same
 // order, so every distance equals the row-major kernel's bit for bit.
@@ -61,6 +69,11 @@ __device__ uint32_t g_packed_no_mask;
 constexpr int kPkSpan = 64;                 // elements of d per pipeline step
 constexpr int kPkChunks = kPkSpan * 2 / 16;  // 16-byte chunks per row and step (LDS ring)
 constexpr int kBlockRows = 16;
+// QM 2: query spans load straight into LDS kPkQAhead steps ahead, into a ring of
+// kPkQBufs span buffers (each span's buffer is reloaded only after the barrier
+// that ends its step).
+constexpr int kPkQAhead = 3;
+constexpr int kPkQBufs = kPkQAhead + 1;
 
 // Bytes of one packed block of 16 rows of d 16-bit elements: fragments, then norms.
 __host__ __device__ constexpr int64_t packed_block_bytes(int64_t d) { return 32 * d + 4 * kBlockRows; }
@@ -70,11 +83,16 @@ __global__ __launch_bounds__(NW * kWave, 8 / NW) void k_dist_packed(DistArgs a, 
     constexpr int NT = NW * kWave;
     constexpr int QB = MQ * 16;
     constexpr int PB = NW * KBW;  // key blocks per pass
-    constexpr int QCH = QM == 1 ? QB * kPkChunks / NT : 1;
-    static_assert(QM != 1 || (QB * kPkChunks) % NT == 0, "whole query chunks per thread");
+    constexpr int QCH = QM != 0 ? QB * kPkChunks / NT : 1;
+    static_assert(QM == 0 || (QB * kPkChunks) % NT == 0, "whole query chunks per thread");
     static_assert(QM != 1 || NS % 2 == 0, "the LDS ring alternates with the step's parity");
     static_assert(FM == 0 || MQ == 8, "the fused select runs on 128-query groups");
     __shared__ __align__(16) u32x4_t qlds[QM == 1 ? 2 : 1][QM == 1 ? QB * kPkChunks : 1];
+    // QM 2: four span buffers (the loop is unrolled over them)
+    static_assert(kPkQBufs == 4, "four span buffers");
+    constexpr int QSZ = QM == 2 ? QB * kPkChunks : 1;
+    __shared__ __align__(16) u32x4_t qb0[QSZ], qb1[QSZ], qb2[QSZ], qb3[QSZ];
+    auto qbuf = [&](int i) __attribute__((always_inline)) { return i == 0 ? qb0 : i == 1 ? qb1 : i == 2 ? qb2 : qb3; };
     __shared__ uint32_t smin[QB], smax[QB];
     // ||q||^2 of the group's queries (written by every wave after each pass:
     // every wave sums the same A fragments in the same order) and, for FM 2,
@@ -160,9 +178,18 @@ __global__ __launch_bounds__(NW * kWave, 8 / NW) void k_dist_packed(DistArgs a, 
     int qslot[QCH];
 #pragma unroll
     for (int i = 0; i < QCH; ++i) {
-        const int e = i * NT + tid, n = e / kPkChunks, c = e % kPkChunks;
-        qso[i] = static_cast<uint32_t>(n < nq ? n : 0) * rb + static_cast<uint32_t>(c * 16);
-        qslot[i] = swz<kPkChunks>(n, c);
+        const int e = i * NT + tid;
+        if constexpr (QM == 2) {
+            // LDS slot e (lane-consecutive, as the direct load writes them) holds the
+            // chunk that the swizzle puts there: row e / 8, column (e % 8) ^ (row % 8)
+            const int n = e / kPkChunks, c = (e % kPkChunks) ^ (n & (kPkChunks - 1));
+            qso[i] = static_cast<uint32_t>(n < nq ? n : 0) * rb + static_cast<uint32_t>(c * 16);
+            qslot[i] = e;
+        } else {
+            const int n = e / kPkChunks, c = e % kPkChunks;
+            qso[i] = static_cast<uint32_t>(n < nq ? n : 0) * rb + static_cast<uint32_t>(c * 16);
+            qslot[i] = swz<kPkChunks>(n, c);
+        }
     }
     uint32_t qoff[MQ];  // QM 0: query row j * 16 + lr (the group's first past its end), this lane's 16 bytes
 #pragma unroll
@@ -195,6 +222,18 @@ __global__ __launch_bounds__(NW * kWave, 8 / NW) void k_dist_packed(DistArgs a, 
         if constexpr (QM == 1) {
 #pragma unroll
             for (int i = 0; i < QCH; ++i) qlds[buf][qslot[i]] = qr[set][i];
+        }
+    };
+    // QM 2: step t's query span straight into LDS buffer t % kPkQBufs; every
+    // wave fills 64 consecutive slots per instruction (the LDS address is the
+    // wave's, each lane's data lands 16 bytes after the previous lane's)
+    auto qload = [&](uint32_t t, int b) __attribute__((always_inline)) {
+        if constexpr (QM == 2) {
+            const uint32_t sp = t % nspan;
+            u32x4_t *buf = qbuf(b);
+#pragma unroll
+            for (int i = 0; i < QCH; ++i)
+                load_to_lds_16(qbase + qso[i] + sp * 128u, buf + (i * NT + wave * kWave));
         }
     };
 
@@ -237,7 +276,8 @@ __global__ __launch_bounds__(NW * kWave, 8 / NW) void k_dist_packed(DistArgs a, 
             u32x4_t af[MQ];
 #pragma unroll
             for (int j = 0; j < MQ; ++j) {
-                if constexpr (QM == 1) af[j] = qlds[buf][swz<kPkChunks>(j * 16 + lr, c * 4 + g)];
+                if constexpr (QM == 2) af[j] = qbuf(buf)[swz<kPkChunks>(j * 16 + lr, c * 4 + g)];
+                else if constexpr (QM == 1) af[j] = qlds[buf][swz<kPkChunks>(j * 16 + lr, c * 4 + g)];
                 else af[j] = ar[set][j][c];
             }
 #pragma unroll
@@ -368,20 +408,42 @@ __global__ __launch_bounds__(NW * kWave, 8 / NW) void k_dist_packed(DistArgs a, 
     for (int k = 0; k < NS; ++k) load(k, static_cast<uint32_t>(k) < T ? static_cast<uint32_t>(k) : T - 1);
     load_rows(NS - 1);
     if constexpr (QM == 1) qwrite(0, 0);
-    __syncthreads();  // the query span buffer, the extrema and the stage counter are set
-    for (uint32_t t0 = 0; t0 < T; t0 += NS) {
+    if constexpr (QM == 2) {
 #pragma unroll
-        for (int k = 0; k < NS; ++k) {
+        for (int k = 0; k < kPkQAhead; ++k) qload(static_cast<uint32_t>(k) < T ? static_cast<uint32_t>(k) : T - 1, k);
+        __builtin_amdgcn_s_waitcnt(kVmcntZero);  // the direct loads are known to no register dependence
+    }
+    __syncthreads();  // the query span buffers, the extrema and the stage counter are set
+    // QM 2 unrolls over the four span buffers (the host launches it when four divide the steps per pass)
+    constexpr int U = QM == 2 ? kPkQBufs : NS;
+    static_assert(U % NS == 0, "whole ring turns per loop body");
+    for (uint32_t t0 = 0; t0 < T; t0 += U) {
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
             const uint32_t t = t0 + static_cast<uint32_t>(k);
-            compute(k, k & 1, t < nspan);
+            compute(k % NS, QM == 2 ? k : (k & 1), t < nspan);
             const uint32_t tn = t + NS;
-            load(k, tn < T ? tn : T - 1);
+            load(k % NS, tn < T ? tn : T - 1);
             if constexpr (QM == 1) {
                 qwrite((k + 1) % NS, (k + 1) & 1);
                 __syncthreads();
             }
+            if constexpr (QM == 2) {
+                // span t + kPkQAhead; then span t + 1 (loaded kPkQAhead - 1 steps ago) must
+                // have landed: every step issues the same loads (KBW x 2 key fragments,
+                // QCH query chunks), so at least that many per newer step are still
+                // allowed in flight
+                const uint32_t tq = t + kPkQAhead;
+                qload(tq < T ? tq : T - 1, (k + kPkQAhead) % kPkQBufs);
+                __builtin_amdgcn_s_waitcnt(vmcnt_encoding<(kPkQAhead - 1) * (2 * KBW + QCH)>());
+                // a bare barrier: a fenced one would wait for every load in flight,
+                // those of the spans ahead included; no memory access moves across it
+                asm volatile("" ::: "memory");
+                __builtin_amdgcn_s_barrier();
+                asm volatile("" ::: "memory");
+            }
         }
-        const uint32_t te = t0 + NS;  // steps done
+        const uint32_t te = t0 + U;  // steps done
         if (te % nspan == 0) epilogue(te / nspan - 1);
         load_rows(te + NS - 1);  // the row data of the next group's pass
     }
@@ -478,10 +540,13 @@ template <knn_dtype DT>
 hipError_t launch_packed_mq(int mq, const DistArgs &a, int64_t n_tiles, int64_t groups, dim3 grid, hipStream_t st,
                             int fm) {
     const int64_t nspan = a.d / kPkSpan;
+    const bool direct = nspan % kPkQBufs == 0;  // 128-query groups: query spans loaded straight into LDS
     if (fm != 0) {  // the fused select: 128-query workgroups only
         if (mq != 8) return hipErrorInvalidValue;
         const bool deep = nspan % packed_ring<8>() == 0;
-        if (fm == 1) launch_packed_ns<DT, 8, 2, 8, 1, 1>(deep, a, n_tiles, groups, grid, st);
+        if (direct && fm == 1) launch_packed_ns<DT, 8, 2, 8, 2, 1>(deep, a, n_tiles, groups, grid, st);
+        else if (direct) launch_packed_ns<DT, 8, 2, 8, 2, 2>(deep, a, n_tiles, groups, grid, st);
+        else if (fm == 1) launch_packed_ns<DT, 8, 2, 8, 1, 1>(deep, a, n_tiles, groups, grid, st);
         else launch_packed_ns<DT, 8, 2, 8, 1, 2>(deep, a, n_tiles, groups, grid, st);
         return hipGetLastError();
     }
@@ -489,7 +554,10 @@ hipError_t launch_packed_mq(int mq, const DistArgs &a, int64_t n_tiles, int64_t 
     case 1: launch_packed_ns<DT, 1, 4, 4, 0, 0>(nspan % packed_ring<1>() == 0, a, n_tiles, groups, grid, st); break;
     case 2: launch_packed_ns<DT, 2, 2, 4, 1, 0>(nspan % packed_ring<2>() == 0, a, n_tiles, groups, grid, st); break;
     case 4: launch_packed_ns<DT, 4, 2, 8, 1, 0>(nspan % packed_ring<4>() == 0, a, n_tiles, groups, grid, st); break;
-    case 8: launch_packed_ns<DT, 8, 2, 8, 1, 0>(nspan % packed_ring<8>() == 0, a, n_tiles, groups, grid, st); break;
+    case 8:
+        if (direct) launch_packed_ns<DT, 8, 2, 8, 2, 0>(nspan % packed_ring<8>() == 0, a, n_tiles, groups, grid, st);
+        else launch_packed_ns<DT, 8, 2, 8, 1, 0>(nspan % packed_ring<8>() == 0, a, n_tiles, groups, grid, st);
+        break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
