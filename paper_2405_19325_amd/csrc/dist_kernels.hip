@@ -353,15 +353,20 @@ __global__ __launch_bounds__(kDistThreads) void k_dist_elem(DistArgs a) {
 
 // ||k||^2 per row: the wave-per-row layout and word order of the distance
 // kernel (so the values equal its on-the-fly norms bit for bit), over a fixed
-// grid whose waves stride over the rows, two rows in flight per wave in
-// register sets used in turn (half-row sets for 16-chunk rows), every load
-// unconditional: rows past the end read row 0 and store into a sink word.
+// grid, two rows in flight per wave in register sets used in turn (half-row
+// sets for 16-chunk rows), every load unconditional (rows past the end read
+// row 0).  Rows of at most 4 KB (BLOCKED) go to the waves in blocks of 64
+// consecutive rows: lane i keeps the norm of the block's row i, and the
+// block's 64 norms leave in one 256-byte store (a store per row, 63 lanes of
+// it idle, held such rows near 70% of 8 TB/s).  Longer rows stride over the
+// waves one at a time, each norm stored as it is made.
 template <knn_dtype DT, int CPL>
 __global__ __launch_bounds__(kDistThreads) void k_sqnorm_vec(const void *keys, int64_t n, int64_t d, float *out) {
     constexpr int EB = Elem<DT>::BYTES;
     constexpr int CPS = CPL > 8 ? 8 : CPL;  // chunks per set
     constexpr int SPR = CPL / CPS;          // sets per row
     constexpr int D = 2 * SPR;              // sets in flight: two rows
+    constexpr bool BLOCKED = CPL <= 4;
     const int lane = threadIdx.x & (kWave - 1);
     const int64_t wave_global = (static_cast<int64_t>(blockIdx.x) * kDistThreads + threadIdx.x) / kWave;
     const int64_t nwaves = static_cast<int64_t>(gridDim.x) * (kDistThreads / kWave);
@@ -370,15 +375,10 @@ __global__ __launch_bounds__(kDistThreads) void k_sqnorm_vec(const void *keys, i
     const char *base = static_cast<const char *>(keys);
     const u32x4_t zero = {0u, 0u, 0u, 0u};
     u32x4_t kv[D][CPS];
-    int64_t rc[D];
-    bool in[D];
     float acc = 0.0f;
     auto load = [&](int s, int64_t rw) __attribute__((always_inline)) {
         const int part = s % SPR;
-        const bool inside = rw < n;
-        rc[s] = inside ? rw : 0;
-        in[s] = inside;
-        const char *krow = base + rc[s] * row_bytes;
+        const char *krow = base + (rw < n ? rw : 0) * row_bytes;
 #pragma unroll
         for (int c = 0; c < CPS; ++c) {
             const int ch = lane + kWave * (part * CPS + c);
@@ -394,19 +394,50 @@ __global__ __launch_bounds__(kDistThreads) void k_sqnorm_vec(const void *keys, i
             const uint4 k4 = make_uint4(kc.x, kc.y, kc.z, kc.w);
             acc = dot_chunk<DT>(k4, k4, acc);
         }
-        if (part != SPR - 1) return;
-        const float v = wave_allsum(acc);
-        *(in[s] ? out + rc[s] : &g_dist_sink) = v;
     };
-    int64_t row = wave_global;
+    if constexpr (BLOCKED) {
+        // row i of this wave's block blk (i in [0, 64)); the two rows after
+        // it follow in the block or start the wave's next block
+        const int64_t nblk = (n + kWave - 1) / kWave;
+        int64_t blk = wave_global;
+        auto row_at = [&](int64_t bk, int i) __attribute__((always_inline)) {
+            return i < kWave ? bk * kWave + i : (bk + nwaves) * kWave + (i - kWave);
+        };
 #pragma unroll
-    for (int s = 0; s < D; ++s) load(s, row + static_cast<int64_t>(s / SPR) * nwaves);
-    for (; row < n; row += 2 * nwaves) {
+        for (int s = 0; s < D; ++s) load(s, row_at(blk, s / SPR));
+        float mine = 0.0f;  // lane i: the norm of row i of the block
+        for (; blk < nblk; blk += nwaves) {
+            for (int i = 0; i < kWave; i += 2) {
 #pragma unroll
-        for (int s = 0; s < D; ++s) {
-            __builtin_amdgcn_sched_barrier(0);  // keep the sets' work apart (see the distance kernel)
-            consume(s);
-            load(s, row + static_cast<int64_t>(s / SPR + 2) * nwaves);
+                for (int s = 0; s < D; ++s) {
+                    __builtin_amdgcn_sched_barrier(0);  // keep the sets' work apart (see the distance kernel)
+                    consume(s);
+                    if (s % SPR == SPR - 1) {
+                        const float v = wave_allsum(acc);
+                        mine = lane == i + s / SPR ? v : mine;
+                    }
+                    load(s, row_at(blk, i + s / SPR + 2));
+                }
+            }
+            const int64_t r = blk * kWave + lane;
+            *(r < n ? out + r : &g_dist_sink) = mine;
+        }
+    } else {
+        int64_t row = wave_global;
+#pragma unroll
+        for (int s = 0; s < D; ++s) load(s, row + static_cast<int64_t>(s / SPR) * nwaves);
+        for (; row < n; row += 2 * nwaves) {
+#pragma unroll
+            for (int s = 0; s < D; ++s) {
+                __builtin_amdgcn_sched_barrier(0);  // keep the sets' work apart (see the distance kernel)
+                consume(s);
+                if (s % SPR == SPR - 1) {
+                    const float v = wave_allsum(acc);
+                    const int64_t rw = row + static_cast<int64_t>(s / SPR) * nwaves;
+                    *(rw < n ? out + rw : &g_dist_sink) = v;
+                }
+                load(s, row + static_cast<int64_t>(s / SPR + 2) * nwaves);
+            }
         }
     }
     __builtin_amdgcn_sched_barrier(0);
@@ -580,14 +611,15 @@ hipError_t launch_distances(const DistPlan &plan, knn_dtype dtype, const DistArg
 hipError_t launch_key_sqnorms(const void *keys, int64_t n, int64_t d, knn_dtype dtype, float *out,
                               hipStream_t stream) {
     if (n == 0) return hipSuccess;
-    const int64_t waves_needed = n;
-    int64_t blocks = (waves_needed + kWavesPerDistBlock - 1) / kWavesPerDistBlock;
-    // the vector kernel: enough rows per wave for its pipeline (at most 1024 workgroups, four per CU)
-    const int64_t max_blocks = vector_path_ok(d, dtype, keys, keys) ? 1024 : 65536;
-    if (blocks > max_blocks) blocks = max_blocks;
-    const dim3 grid(static_cast<unsigned>(blocks));
     const bool vec = vector_path_ok(d, dtype, keys, keys);
     const int cpl = vec ? pow2_at_least((d / vec_elems(dtype) + kWave - 1) / kWave) : 0;
+    // a wave per row, or per block of 64 rows (short rows on the vector kernel)
+    const int64_t waves_needed = vec && cpl <= 4 ? (n + kWave - 1) / kWave : n;
+    int64_t blocks = (waves_needed + kWavesPerDistBlock - 1) / kWavesPerDistBlock;
+    // the vector kernel: enough rows per wave for its pipeline (at most 1024 workgroups, four per CU)
+    const int64_t max_blocks = vec ? 1024 : 65536;
+    if (blocks > max_blocks) blocks = max_blocks;
+    const dim3 grid(static_cast<unsigned>(blocks));
 #define KNN_SQN(DT)                                                                                 \
     do {                                                                                            \
         if (!vec) {                                                                                 \

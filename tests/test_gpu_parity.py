@@ -242,6 +242,34 @@ def test_precomputed_norms_give_identical_results():
     torch.testing.assert_close(norms, ref, rtol=1e-5, atol=1e-5)
 
 
+# The key-norm pre-pass against the distance kernel's own norms: the distance from a zero query is
+# fma(-2, 0, 0 + ||k||^2) = ||k||^2, bit for bit the norm the kernel made on the fly.  Rows of at most 4 KB
+# go to the pre-pass's waves in blocks of 64 (row counts off a multiple of 64, and beyond 4096 waves x 64
+# rows so that waves take several blocks); longer rows and rows off the 16-byte grid take the other forms.
+NORM_CASES = [(65, 64, torch.float32), (1000, 256, torch.float32), (4097, 2048, torch.bfloat16),
+              (300001, 1024, torch.float16), (263000, 512, torch.bfloat16), (333, 8192, torch.bfloat16),
+              (777, 100, torch.float32), (501, 330, torch.bfloat16)]
+
+
+@pytest.mark.parametrize("n,d,dtype", NORM_CASES, ids=[f"{c[0]}x{c[1]}-{str(c[2])[6:]}" for c in NORM_CASES])
+def test_norm_prepass_equals_on_the_fly_norms(n, d, dtype):
+    _say(f"key-norm pre-pass n={n} d={d} {dtype}")
+    g = torch.Generator(device="cuda")
+    g.manual_seed(n + d)
+    keys = torch.randn((n, d), device="cuda", generator=g).to(dtype)
+    norms = knn.key_sqnorms(keys)
+    zero = torch.zeros((1, d), dtype=dtype, device="cuda")
+    ko, qo = np.array([0, n]), np.array([0, 1])
+    on_the_fly = knn.distances(zero, keys, torch.as_tensor(ko, device="cuda"), torch.as_tensor(qo, device="cuda"),
+                               key_offsets_host=ko, query_offsets_host=qo)
+    torch.cuda.synchronize()
+    assert torch.equal(norms, on_the_fly[0])
+    ref = keys.double().pow(2).sum(1)
+    assert ((norms.double() - ref).abs() / ref).max().item() < 1e-5
+    del keys, on_the_fly
+    _free()
+
+
 # Rows of 16 chunks per lane (d = 8192 for 16-bit keys, d = 4096 for fp32) stream in two halves that add
 # into one sum; d = 4096 bf16 streams whole rows.  Integer coordinates in both halves of every row make every
 # distance an exact integer, so ids and distances must equal the oracle's bit for bit, with the key norms
