@@ -30,6 +30,10 @@ PEAK_MFMA_16BIT_TFLOPS = 2500.0  # MI355X dense bf16 / fp16 matrix cores, publis
 # The workloads of the per-config block, with the timed steps of each.
 PER_CONFIG_STEPS = {"tiny": 200, "decode_7b": 200, "ragged_batch": 20, "decode_70b": 20, "specverify_seq": 10,
                     "specverify_static": 10}
+# Workloads whose steps are also timed as replays of a HIP graph (steps short enough for the host's
+# per-call launch work to show).
+GRAPH_REPLAY = ("tiny", "decode_7b")
+GRAPH_STEPS = 50  # steps captured in one graph
 PMC_FILE = os.path.join(ROOT, "profiles", "dist_kernel_{workload}_pmc.json")
 # The sources the distance kernels are built from (a change makes committed counters stale).
 DIST_SOURCES = ("dist_kernels.hip", "mfma_kernels.hip", "mfma_packed.hip", "mfma_device.h", "knnlm_device.h",
@@ -349,6 +353,22 @@ def _events_ms(torch, fn, n):
     return e0.elapsed_time(e1) / n
 
 
+def _graph_ms(torch, fn, steps, replays):
+    """Average ms per step of fn(0..steps-1) captured once in a HIP graph, over `replays` replays after an
+    untimed one (the same work as the eager calls, without the host's per-call launches)."""
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=side):
+        for i in range(steps):
+            fn(i)
+    torch.cuda.synchronize()
+    graph.replay()
+    ms = _events_ms(torch, lambda i: graph.replay(), replays) / steps
+    del graph
+    return ms
+
+
 def time_config(name, steps, stream_gbs, with_oracle):
     """One workload at full size: the whole step, the distance stage alone and distance + top-r, each over
     `steps` back-to-back calls (two key buffers alternate when the keys would fit the last-level cache), the
@@ -417,6 +437,11 @@ def time_config(name, steps, stream_gbs, with_oracle):
         out["matrix_cores"] = {"alg_flops": 2 * macs, "tflops": round(tflops, 1),
                                "frac_of_dense_peak": round(tflops / PEAK_MFMA_16BIT_TFLOPS, 4)}
         out["packed_keys"] = time_packed(knn, torch, w, bufs, hints, steps, dist_bytes, step_bytes)
+    if name in GRAPH_REPLAY:
+        g_ms = _graph_ms(torch, full, GRAPH_STEPS, max(steps // GRAPH_STEPS, 2))
+        out["graph_replay"] = {"steps_per_graph": GRAPH_STEPS, "ms_per_step": round(g_ms, 5),
+                               "queries_per_s": round(B / (g_ms / 1e3), 1),
+                               "step_hbm_frac": round(step_bytes / (g_ms / 1e3) / 1e9 / PEAK_HBM_GBS, 4)}
     del probs, bufs
     if with_oracle:
         out["oracle"] = oracle_estimate(w, spec, macs)
