@@ -18,6 +18,7 @@ import torch
 
 import oracle
 import parity
+import select_paths
 from workloads import gen
 
 pytestmark = pytest.mark.gpu
@@ -406,29 +407,44 @@ def test_split_and_one_workgroup_select_agree():
 
 def _sampled_positions(path, n):
     """Key positions whose distances the sampled threshold of each select path reads."""
-    if path == "split":  # 1024 runs of 4 consecutive keys, a run starting every n / 1024 (at a multiple of 4)
+    if path in ("parts", "groups"):  # parts kernel: 1024 runs of 4 consecutive keys, one every n / 1024 (at a multiple of 4)
         starts = ((np.arange(1024, dtype=np.int64) * n) >> 10) & ~3
         return (starts[:, None] + np.arange(4)).ravel()
     t = np.arange(1024)
     return (t & 15) * 4096 + 4 * t + ((t >> 4) & 3)  # one-workgroup path: a key per thread's registers
 
 
-# One query (the row is split over 16 workgroups) and 20 queries on one set
-# (too many parts for one pass of the chip, so one workgroup per query).
-@pytest.mark.parametrize("path,B", [("split", 1), ("one-workgroup", 20)])
-def test_adversarial_row_takes_the_streamed_path(path, B):
-    """Keys at the positions the select samples are far away and every other
-    key sits on the query: the sampled threshold then keeps more than the
-    candidate capacity, the streamed path over the whole row takes over, and
-    the answer (ties broken by index) is still exact."""
+# (path, queries, V) on one 64K-key set of width 16: the split select over 16 workgroups per row, from the
+# parts kernel's sample (two queries and a vocabulary too large for the sliced finish) or from the distance
+# stage's group minima (one query), and 20 queries (too many parts for one pass of the chip, so one
+# workgroup per query).
+SAMPLED_PATHS = [("parts", 2, 600001), ("groups", 1, 50), ("one-workgroup", 20, 50)]
+
+
+def _check_path(path, B, n, d, r, V):
+    if path != "one-workgroup":
+        assert select_paths.split_path(B, d, 2, 1, n, B, r, V) == path
+
+
+@pytest.mark.parametrize("path,B,V", SAMPLED_PATHS, ids=[c[0] for c in SAMPLED_PATHS])
+def test_adversarial_row_takes_the_streamed_path(path, B, V):
+    """Keys at the positions the parts kernel and the one-workgroup select
+    sample are far away and every other key sits on the query: their sampled
+    threshold then keeps more than the candidate capacity.  On the group
+    minima every group holds keys at distance 0, so every minimum is 0 and
+    every group is listed, more than the list holds.  Either way the streamed
+    path over the whole row takes over, and the answer (ties broken by index)
+    is still exact."""
     _say(f"adversarial sample ({path})")
     n, d, r = 65536, 16, 1000
+    _check_path(path, B, n, d, r, V)
     sampled = _sampled_positions(path, n)
     k = np.zeros((n, d), np.float32)
     k[sampled] = 3.0
     q = np.zeros((B, d), np.float32)
     vals = (np.arange(n) % 50).astype(np.int32)
-    p_lm = np.full((B, 50), 0.02, np.float32)
+    p_lm = np.zeros((B, V), np.float32)
+    p_lm[:, :50] = 0.02
     tq, tk, tv, tko, tqo, tp = _tensor_inputs(q, k, vals, p_lm, [0, n], [0, B], torch.bfloat16)
     p_m, ids, dists = knn.mixture(tq, tk, tv, tko, tqo, tp, r, 0.1, 0.5)
     torch.cuda.synchronize()
@@ -439,11 +455,16 @@ def test_adversarial_row_takes_the_streamed_path(path, B):
     # every neighbour is at distance 0: equal weights 1/r on tokens i % 50
     counts = np.bincount(vals[expect], minlength=50).astype(np.float64)
     want = 0.5 * 0.02 + 0.5 * counts / r
-    np.testing.assert_allclose(p_m.cpu().numpy(), np.broadcast_to(want, (B, 50)), rtol=0, atol=1e-6)
+    pm = p_m.cpu().numpy()
+    np.testing.assert_allclose(pm[:, :50], np.broadcast_to(want, (B, 50)), rtol=0, atol=1e-6)
+    assert not pm[:, 50:].any()
 
 
-@pytest.mark.parametrize("path,B", [("split", 1), ("one-workgroup", 20)])
-def test_sample_keeps_fewer_than_r_takes_the_streamed_path(path, B):
+FEWER_PATHS = [c for c in SAMPLED_PATHS if c[0] != "groups"]  # at least r groups, hence keys, lie below theirs
+
+
+@pytest.mark.parametrize("path,B,V", FEWER_PATHS, ids=[c[0] for c in FEWER_PATHS])
+def test_sample_keeps_fewer_than_r_takes_the_streamed_path(path, B, V):
     """The keys at the sampled positions are the nearest of the row, at many
     different distances, and every other key is far away: the sampled
     threshold then keeps about a hundred keys, fewer than r, and the streamed
@@ -451,6 +472,7 @@ def test_sample_keeps_fewer_than_r_takes_the_streamed_path(path, B):
     every distance exact, so ids and distances equal the oracle's bit for bit."""
     _say(f"sample keeps fewer than r ({path})")
     n, d, r = 65536, 16, 1000
+    _check_path(path, B, n, d, r, V)
     sampled = _sampled_positions(path, n)
     j = np.arange(sampled.size)
     k = np.full((n, d), 100.0, np.float32)
@@ -460,7 +482,8 @@ def test_sample_keeps_fewer_than_r_takes_the_streamed_path(path, B):
     q = np.zeros((B, d), np.float32)
     rng = np.random.default_rng(97)
     vals = rng.integers(0, 50, n).astype(np.int32)
-    p_lm = np.full((B, 50), 0.02, np.float32)
+    p_lm = np.zeros((B, V), np.float32)
+    p_lm[:, :50] = 0.02
     tq, tk, tv, tko, tqo, tp = _tensor_inputs(q, k, vals, p_lm, [0, n], [0, B], torch.bfloat16)
     p_m, ids, dists = knn.mixture(tq, tk, tv, tko, tqo, tp, r, 0.1, 0.5)
     torch.cuda.synchronize()
@@ -474,31 +497,47 @@ def test_sample_keeps_fewer_than_r_takes_the_streamed_path(path, B):
     np.testing.assert_allclose(p_m.cpu().numpy(), ref, rtol=0, atol=1e-5)
 
 
-# (case, V): 40,000 keys of width 4, two queries and a mixture -- the split select (ten parts per row, each
-# keeping its keys below a threshold sampled across the row) and its finish, sliced by 4096-entry pieces of
-# p_M.  V = 10001 takes the mixture's scalar path, V = 32000 its 16-byte path.
-SPLIT_SLICED = [("threshold", 32000), ("threshold", 10001), ("all-equal-fallback", 32000)]
+# (case, V) over two layouts, each with a mixture whose finish is sliced by 4096-entry pieces of p_M:
+# "one-set": 40,000 keys of width 4 and two queries, the split select from the group minima (ten parts per
+# row, 16-row distance tiles); "32-sets": 32 sets of 4096 keys with a query each, the split select from the
+# parts kernel's sample (64-row distance tiles record no group minima).  V = 10001 takes the mixture's
+# scalar path, V = 32000 its 16-byte path.
+SPLIT_SLICED = [("threshold", 32000), ("threshold", 10001), ("all-equal", 32000)]
 
 
+@pytest.mark.parametrize("layout", ["one-set", "32-sets"])
 @pytest.mark.parametrize("case,V", SPLIT_SLICED, ids=[f"{c}-V{v}" for c, v in SPLIT_SLICED])
 @pytest.mark.parametrize("rrc", [False, True], ids=["fixed-lambda", "rrc"])
-def test_split_select_sliced_finish_exact_integers(case, V, rrc):
+def test_split_select_sliced_finish_exact_integers(case, V, rrc, layout):
     """Integer keys (a, b, c, 0) with a, b, c in [-60, 60] give exact distances in many distinct values, so the
-    sampled threshold keeps somewhat more than r keys; with every key equal it keeps the whole row and the
-    finish falls back to the streamed select (ties by index).  ids and distances bit for bit against the
-    oracle, p_M within 1e-5 (with RRC, lambda_t within 1e-6)."""
-    _say(f"split select, sliced finish: {case}, V={V}, rrc={rrc}")
-    n, d, B, r = 40000, 4, 2, 1024
+    threshold keeps somewhat more than r keys.  With every key equal, the group minima list every group, more
+    than the list holds, and the finish falls back to the streamed select; the parts kernel's threshold keeps
+    each whole 4096-key row, which the finish still sorts (ties by index).  ids and distances bit for bit
+    against the oracle, p_M within 1e-5 (with RRC, lambda_t within 1e-6)."""
+    _say(f"split select, sliced finish: {layout}, {case}, V={V}, rrc={rrc}")
     rng = np.random.default_rng(98)
+    d = 4
+    if layout == "one-set":
+        n, B, r = 40000, 2, 1024
+        ko, qo = np.array([0, n]), np.array([0, B])
+        q = np.zeros((B, d), np.float32)
+        q[:, 3] = [2, 5]
+        q[1, 0] = 7
+    else:
+        B, r = 32, 256
+        n = 4096 * B
+        ko, qo = np.arange(B + 1) * 4096, np.arange(B + 1)
+        q = np.zeros((B, d), np.float32)
+        q[:, :3] = rng.integers(-30, 31, (B, 3))
+        q[:, 3] = np.arange(B) % 5
+    sizes = np.diff(ko)
+    assert select_paths.split_path(B, d, 4, len(sizes), int(sizes.max()), int(np.diff(qo).max()), r, V) == (
+        "groups" if layout == "one-set" else "parts")
     k = np.zeros((n, d), np.float32)
-    if case != "all-equal-fallback":
+    if case != "all-equal":
         k[:, :3] = rng.integers(-60, 61, (n, 3))
-    q = np.zeros((B, d), np.float32)
-    q[:, 3] = [2, 5]
-    q[1, 0] = 7
     vals = rng.integers(0, V, n).astype(np.int32)
     p_lm = rng.dirichlet(np.ones(V), B).astype(np.float32)
-    ko, qo = np.array([0, n]), np.array([0, B])
     tq, tk, tv, tko, tqo, tp = _tensor_inputs(q, k, vals, p_lm, ko, qo, torch.float32)
     prob = knn.MixtureProblem(tq, tk, tv, tko, tqo, tp, r, 0.05, 0.4, key_offsets_host=ko, query_offsets_host=qo)
     o_ids, o_d = oracle.select(q, k, "f32", ko, qo, r)
