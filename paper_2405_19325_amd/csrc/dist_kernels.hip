@@ -355,18 +355,19 @@ __global__ __launch_bounds__(kDistThreads) void k_dist_elem(DistArgs a) {
 // kernel (so the values equal its on-the-fly norms bit for bit), over a fixed
 // grid, two rows in flight per wave in register sets used in turn (half-row
 // sets for 16-chunk rows), every load unconditional (rows past the end read
-// row 0).  Rows of at most 4 KB (BLOCKED) go to the waves in blocks of 64
-// consecutive rows: lane i keeps the norm of the block's row i, and the
-// block's 64 norms leave in one 256-byte store (a store per row, 63 lanes of
-// it idle, held such rows near 70% of 8 TB/s).  Longer rows stride over the
-// waves one at a time, each norm stored as it is made.
-template <knn_dtype DT, int CPL>
+// row 0).  With BLOCKED (rows of at most 4 KB, enough of them to give every
+// wave of the grid a block) the waves take blocks of 64 consecutive rows:
+// lane i keeps the norm of the block's row i, and the block's 64 norms leave
+// in one 256-byte store (a store per row, 63 lanes of it idle, held such rows
+// near 70% of 8 TB/s).  Otherwise the rows stride over the waves one at a
+// time, each norm stored as it is made.
+template <knn_dtype DT, int CPL, bool BLOCKED>
 __global__ __launch_bounds__(kDistThreads) void k_sqnorm_vec(const void *keys, int64_t n, int64_t d, float *out) {
     constexpr int EB = Elem<DT>::BYTES;
     constexpr int CPS = CPL > 8 ? 8 : CPL;  // chunks per set
     constexpr int SPR = CPL / CPS;          // sets per row
     constexpr int D = 2 * SPR;              // sets in flight: two rows
-    constexpr bool BLOCKED = CPL <= 4;
+    static_assert(!BLOCKED || CPL <= 4, "blocks of short rows");
     const int lane = threadIdx.x & (kWave - 1);
     const int64_t wave_global = (static_cast<int64_t>(blockIdx.x) * kDistThreads + threadIdx.x) / kWave;
     const int64_t nwaves = static_cast<int64_t>(gridDim.x) * (kDistThreads / kWave);
@@ -613,11 +614,12 @@ hipError_t launch_key_sqnorms(const void *keys, int64_t n, int64_t d, knn_dtype 
     if (n == 0) return hipSuccess;
     const bool vec = vector_path_ok(d, dtype, keys, keys);
     const int cpl = vec ? pow2_at_least((d / vec_elems(dtype) + kWave - 1) / kWave) : 0;
-    // a wave per row, or per block of 64 rows (short rows on the vector kernel)
-    const int64_t waves_needed = vec && cpl <= 4 ? (n + kWave - 1) / kWave : n;
-    int64_t blocks = (waves_needed + kWavesPerDistBlock - 1) / kWavesPerDistBlock;
     // the vector kernel: enough rows per wave for its pipeline (at most 1024 workgroups, four per CU)
     const int64_t max_blocks = vec ? 1024 : 65536;
+    // blocks of 64 short rows where they fill every wave of that grid
+    const bool blocked = vec && cpl <= 4 && n >= kWave * kWavesPerDistBlock * max_blocks;
+    const int64_t waves_needed = blocked ? (n + kWave - 1) / kWave : n;  // a wave per block, or per row
+    int64_t blocks = (waves_needed + kWavesPerDistBlock - 1) / kWavesPerDistBlock;
     if (blocks > max_blocks) blocks = max_blocks;
     const dim3 grid(static_cast<unsigned>(blocks));
 #define KNN_SQN(DT)                                                                                 \
@@ -625,12 +627,15 @@ hipError_t launch_key_sqnorms(const void *keys, int64_t n, int64_t d, knn_dtype 
         if (!vec) {                                                                                 \
             hipLaunchKernelGGL((k_sqnorm_elem<DT>), grid, dim3(kDistThreads), 0, stream, keys, n, d, out); \
         } else {                                                                                    \
-            switch (cpl) {                                                                          \
-            case 1: hipLaunchKernelGGL((k_sqnorm_vec<DT, 1>), grid, dim3(kDistThreads), 0, stream, keys, n, d, out); break; \
-            case 2: hipLaunchKernelGGL((k_sqnorm_vec<DT, 2>), grid, dim3(kDistThreads), 0, stream, keys, n, d, out); break; \
-            case 4: hipLaunchKernelGGL((k_sqnorm_vec<DT, 4>), grid, dim3(kDistThreads), 0, stream, keys, n, d, out); break; \
-            case 8: hipLaunchKernelGGL((k_sqnorm_vec<DT, 8>), grid, dim3(kDistThreads), 0, stream, keys, n, d, out); break; \
-            case 16: hipLaunchKernelGGL((k_sqnorm_vec<DT, 16>), grid, dim3(kDistThreads), 0, stream, keys, n, d, out); break; \
+            switch (cpl * 2 + (blocked ? 1 : 0)) {                                                  \
+            case 2: hipLaunchKernelGGL((k_sqnorm_vec<DT, 1, false>), grid, dim3(kDistThreads), 0, stream, keys, n, d, out); break; \
+            case 3: hipLaunchKernelGGL((k_sqnorm_vec<DT, 1, true>), grid, dim3(kDistThreads), 0, stream, keys, n, d, out); break; \
+            case 4: hipLaunchKernelGGL((k_sqnorm_vec<DT, 2, false>), grid, dim3(kDistThreads), 0, stream, keys, n, d, out); break; \
+            case 5: hipLaunchKernelGGL((k_sqnorm_vec<DT, 2, true>), grid, dim3(kDistThreads), 0, stream, keys, n, d, out); break; \
+            case 8: hipLaunchKernelGGL((k_sqnorm_vec<DT, 4, false>), grid, dim3(kDistThreads), 0, stream, keys, n, d, out); break; \
+            case 9: hipLaunchKernelGGL((k_sqnorm_vec<DT, 4, true>), grid, dim3(kDistThreads), 0, stream, keys, n, d, out); break; \
+            case 16: hipLaunchKernelGGL((k_sqnorm_vec<DT, 8, false>), grid, dim3(kDistThreads), 0, stream, keys, n, d, out); break; \
+            case 32: hipLaunchKernelGGL((k_sqnorm_vec<DT, 16, false>), grid, dim3(kDistThreads), 0, stream, keys, n, d, out); break; \
             default: return hipErrorInvalidValue;                                                   \
             }                                                                                       \
         }                                                                                           \

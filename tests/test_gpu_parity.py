@@ -244,9 +244,10 @@ def test_precomputed_norms_give_identical_results():
 
 
 # The key-norm pre-pass against the distance kernel's own norms: the distance from a zero query is
-# fma(-2, 0, 0 + ||k||^2) = ||k||^2, bit for bit the norm the kernel made on the fly.  Rows of at most 4 KB
-# go to the pre-pass's waves in blocks of 64 (row counts off a multiple of 64, and beyond 4096 waves x 64
-# rows so that waves take several blocks); longer rows and rows off the 16-byte grid take the other forms.
+# fma(-2, 0, 0 + ||k||^2) = ||k||^2, bit for bit the norm the kernel made on the fly.  At least 262,144 rows
+# of at most 4 KB go to the pre-pass's waves in blocks of 64 (row counts off a multiple of 64, and beyond
+# 4096 waves x 64 rows so that waves take several blocks); fewer or longer rows stride one at a time, and
+# rows off the 16-byte grid take the element kernel.
 NORM_CASES = [(65, 64, torch.float32), (1000, 256, torch.float32), (4097, 2048, torch.bfloat16),
               (300001, 1024, torch.float16), (263000, 512, torch.bfloat16), (333, 8192, torch.bfloat16),
               (777, 100, torch.float32), (501, 330, torch.bfloat16)]
